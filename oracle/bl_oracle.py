@@ -1,0 +1,323 @@
+"""fp64 CPU oracle of the band-limited FFT convolution layer.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import or call
+this module: only the tests, the package's smoke check and the benchmark's
+CPU-baseline leg use it.  It shares no code with the HIP library.
+
+What it computes (Dziedzic et al., "Band-limited Training and Inference for
+Convolutional Neural Networks", ICML 2019):
+
+* Sec. 3, Eq. (1)/(2): the band-limited convolution  x *_c y  is the inverse
+  FFT of the product of the two spectra, each multiplied by a 0/1 mask M_c
+  that keeps a low-frequency band.
+* Sec. 3.2.1: input and filter are zero-padded so that the FFT's circular
+  correlation equals the linear one (no wrapped-around filter data).
+* Sec. 3.2.2 and Fig. 2: only the half-plane rfft spectrum is stored
+  (conjugate symmetry); the band is shrunk layer by layer in L-shaped layers
+  taken from the top-left and bottom-left corners of that half plane.
+* Sec. 3.1 / Sec. 4.1: the compression rate c is the fraction of the
+  half-spectrum coefficients that are discarded.
+* Abstract, Sec. 1: the band limit holds in forward and back-propagation;
+  the weight gradient is projected onto the kept frequencies.
+
+Readings taken where the paper is silent or ambiguous (each one is a
+decision, listed with its reason in the design notes of the repository):
+
+* R1 FFT grid: (L_h, L_w) = (H + p_top + p_bottom, W + p_left + p_right),
+  the padded input size; an explicit grid override (e.g. the map-reuse size
+  N + max(K-1, G-1) of Sec. 3.2.3) is accepted.
+* R2 band shape: keep bin (u, v) of the half plane iff |s(u)| <= r_h and
+  v <= r_w, where s(u) is the signed row frequency; r_h = floor(L_h/2) - t,
+  r_w = floor(L_w/2) - t after peeling t L-shaped layers.  In 1-D keep the
+  prefix v <= floor(L/2) - t.
+* R3 rate -> layers: the fewest layers t with kept(t) <= (1 - c) * total,
+  evaluated in IEEE fp64 ("discard at least c"); if none qualifies, the most
+  layers that can be peeled.
+* R4 the layer computes cross-correlation (as a deep-learning conv layer),
+  i.e. the filter spectrum enters conjugated.
+* R5 the mask is applied in all three passes (forward, grad-input,
+  grad-weight), which makes the backward passes exact adjoints.
+
+Parity status: every function here is pinned by tests against brute-force
+direct correlation, direct-sum DFTs, Parseval, the adjoint identity, central
+finite differences and the worked example of the supplementary section
+"Error Incurred by 2D Convolution with Compression" (a 59x30 half spectrum
+losing one layer keeps 57x29).  The rate->layers rounding (R3) is not fixed
+by the paper: parity of that rule is unpinned beyond the worked example.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Geometry and the compression mask (Sec. 3.1, Sec. 3.2.2, Fig. 2)
+# ----------------------------------------------------------------------------
+
+
+def signed_freq(u: int, L: int) -> int:
+    """Signed frequency of FFT index u on a length-L axis (DC at 0)."""
+    return u if u <= L // 2 else u - L
+
+
+def band_2d(Lh: int, Lw: int, t: int) -> np.ndarray:
+    """Half-plane 0/1 mask [Lh][Lw//2+1] after peeling t L-shaped layers."""
+    r_h = Lh // 2 - t
+    r_w = Lw // 2 - t
+    m = np.zeros((Lh, Lw // 2 + 1), dtype=np.uint8)
+    for u in range(Lh):
+        if abs(signed_freq(u, Lh)) > r_h:
+            continue
+        for v in range(Lw // 2 + 1):
+            if v <= r_w:
+                m[u, v] = 1
+    return m
+
+
+def band_1d(L: int, t: int) -> np.ndarray:
+    """Half-spectrum 0/1 mask [L//2+1] after discarding the t highest bins."""
+    B = L // 2 + 1
+    m = np.zeros(B, dtype=np.uint8)
+    m[: B - t] = 1
+    return m
+
+
+def layers_for_rate(c: float, total: int, kept_of_t, t_max: int) -> int:
+    """Reading R3: the fewest layers t whose kept count is <= (1 - c) * total."""
+    budget = (1.0 - c) * total
+    for t in range(t_max + 1):
+        if kept_of_t(t) <= budget:
+            return t
+    return t_max
+
+
+def mask_2d(Lh: int, Lw: int, c: float):
+    """(mask [Lh][Lw//2+1] uint8, t, r_h, r_w) for compression rate c."""
+    t_max = min(Lh // 2, Lw // 2)
+    total = Lh * (Lw // 2 + 1)
+    t = layers_for_rate(c, total, lambda tt: int(band_2d(Lh, Lw, tt).sum()), t_max)
+    return band_2d(Lh, Lw, t), t, Lh // 2 - t, Lw // 2 - t
+
+
+def mask_1d(L: int, c: float):
+    """(mask [L//2+1] uint8, t, r) for compression rate c."""
+    B = L // 2 + 1
+    t = layers_for_rate(c, B, lambda tt: int(band_1d(L, tt).sum()), B - 1)
+    return band_1d(L, t), t, L // 2 - t
+
+
+def kept_bins_2d(mask: np.ndarray):
+    """Kept (u, v) pairs in the bin-major order used for stored spectra:
+    rows in increasing FFT index u (top-left corner, then bottom-left
+    corner), and within a row increasing v."""
+    return [(u, v) for u in range(mask.shape[0]) for v in range(mask.shape[1]) if mask[u, v]]
+
+
+def geometry_2d(H, W, K, pad, fft=None):
+    pt, pb, pl, pr = pad
+    Hp, Wp = H + pt + pb, W + pl + pr
+    Ho, Wo = Hp - K + 1, Wp - K + 1
+    if Ho < 1 or Wo < 1:
+        raise ValueError("filter larger than the padded input")
+    Lh, Lw = (Hp, Wp) if fft is None else fft
+    if Lh < Hp or Lw < Wp:
+        raise ValueError("FFT grid smaller than the padded input would wrap around")
+    return dict(Hp=Hp, Wp=Wp, Ho=Ho, Wo=Wo, Lh=Lh, Lw=Lw)
+
+
+def geometry_1d(L, K, pad, fft=None):
+    lo, hi = pad
+    Lp = L + lo + hi
+    Lo = Lp - K + 1
+    if Lo < 1:
+        raise ValueError("filter longer than the padded input")
+    Lf = Lp if fft is None else fft
+    if Lf < Lp:
+        raise ValueError("FFT length smaller than the padded input would wrap around")
+    return dict(Lp=Lp, Lo=Lo, L=Lf)
+
+
+# ----------------------------------------------------------------------------
+# 2-D passes (Eq. 1 with zero padding, Sec. 3.2.1; half-plane spectra, Sec. 3.2.2)
+# ----------------------------------------------------------------------------
+
+
+def _embed(a, Lh, Lw, oi, oj):
+    """Zero array of spatial size Lh x Lw holding a at offset (oi, oj)."""
+    out = np.zeros(a.shape[:-2] + (Lh, Lw), dtype=np.float64)
+    out[..., oi:oi + a.shape[-2], oj:oj + a.shape[-1]] = a
+    return out
+
+
+def _rfft2(a):
+    return np.fft.rfft2(a, axes=(-2, -1))
+
+
+def _irfft2(A, Lh, Lw):
+    return np.fft.irfft2(A, s=(Lh, Lw), axes=(-2, -1))
+
+
+def _channel_contract(A, B, conj_b: bool):
+    """Per-frequency complex product summed over a shared channel index.
+
+    A: [P, Q, h, w] complex, B: [R, Q, h, w] complex -> [P, R, h, w] with
+    out[p, r] = sum_q A[p, q] * (conj(B[r, q]) if conj_b else B[r, q]).
+    Written as one complex matrix product per frequency bin.
+    """
+    Bq = np.conj(B) if conj_b else B
+    a = np.moveaxis(A, (0, 1), (-2, -1))  # [h, w, P, Q]
+    b = np.moveaxis(Bq, (0, 1), (-1, -2))  # [h, w, Q, R]
+    return np.moveaxis(a @ b, (-2, -1), (0, 1))
+
+
+def spectra_2d(x, w, pad, c, fft=None):
+    """Masked half-plane spectra (X*M, W*M, M) of the embedded input and filter."""
+    N, C, H, W = x.shape
+    K = w.shape[-1]
+    g = geometry_2d(H, W, K, pad, fft)
+    M = mask_2d(g["Lh"], g["Lw"], c)[0]
+    X = _rfft2(_embed(np.asarray(x, np.float64), g["Lh"], g["Lw"], pad[0], pad[2])) * M
+    Wf = _rfft2(_embed(np.asarray(w, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
+    return X, Wf, M, g
+
+
+def forward_2d(x, w, pad, c, fft=None):
+    """y[n,f] = crop_{Ho x Wo} irfft2( sum_c (X[n,c] M) conj(W[f,c] M) )."""
+    X, Wf, M, g = spectra_2d(x, w, pad, c, fft)
+    Y = _channel_contract(X, Wf, conj_b=True)
+    return _irfft2(Y, g["Lh"], g["Lw"])[..., : g["Ho"], : g["Wo"]]
+
+
+def backward_input_2d(dy, w, x_hw, pad, c, fft=None):
+    """dx[n,c] = crop_{pad window} irfft2( sum_f (DY[n,f] M) (W[f,c] M) )."""
+    H, W = x_hw
+    K = w.shape[-1]
+    g = geometry_2d(H, W, K, pad, fft)
+    M = mask_2d(g["Lh"], g["Lw"], c)[0]
+    DY = _rfft2(_embed(np.asarray(dy, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
+    Wf = _rfft2(_embed(np.asarray(w, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
+    # sum over f of DY[n,f] * W[f,c]: contract DY [n,f] with W^T [c,f]
+    DX = _channel_contract(DY, np.swapaxes(Wf, 0, 1), conj_b=False)
+    full = _irfft2(DX, g["Lh"], g["Lw"])
+    return full[..., pad[0]:pad[0] + H, pad[2]:pad[2] + W]
+
+
+def backward_weight_2d(x, dy, K, pad, c, fft=None):
+    """dw[f,c] = crop_{K x K} irfft2( sum_n (X[n,c] M) conj(DY[n,f] M) )."""
+    N, C, H, W = x.shape
+    g = geometry_2d(H, W, K, pad, fft)
+    M = mask_2d(g["Lh"], g["Lw"], c)[0]
+    X = _rfft2(_embed(np.asarray(x, np.float64), g["Lh"], g["Lw"], pad[0], pad[2])) * M
+    DY = _rfft2(_embed(np.asarray(dy, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
+    # DW[f,c] = sum_n DY*[n,f] X[n,c]: contract over n
+    DW = _channel_contract(np.swapaxes(X, 0, 1), np.swapaxes(DY, 0, 1), conj_b=True)  # [c, f]
+    return np.swapaxes(_irfft2(DW, g["Lh"], g["Lw"])[..., :K, :K], 0, 1)
+
+
+def kept_spectrum_2d(a, offset, Lh, Lw, c):
+    """Bin-major kept spectrum [B][planes] of real planes a[..., h, w] placed at
+    offset (oi, oj) in the Lh x Lw grid (what the library stores for x and dy)."""
+    M = mask_2d(Lh, Lw, c)[0]
+    A = _rfft2(_embed(np.asarray(a, np.float64), Lh, Lw, offset[0], offset[1]))
+    bins = kept_bins_2d(M)
+    flat = A.reshape((-1,) + A.shape[-2:])
+    return np.stack([flat[:, u, v] for (u, v) in bins], axis=0)
+
+
+def kept_filter_spectrum_2d(w, Lh, Lw, c):
+    """Bin-major kept filter spectrum [B][C_in][C_out] (the library's layout)."""
+    M = mask_2d(Lh, Lw, c)[0]
+    Wf = _rfft2(_embed(np.asarray(w, np.float64), Lh, Lw, 0, 0))  # [F, C, h, w]
+    bins = kept_bins_2d(M)
+    return np.stack([Wf[:, :, u, v].T for (u, v) in bins], axis=0)
+
+
+# ----------------------------------------------------------------------------
+# 1-D passes (the time-series variant of Sec. 3.2.2: keep the low prefix)
+# ----------------------------------------------------------------------------
+
+
+def _embed1(a, L, o):
+    out = np.zeros(a.shape[:-1] + (L,), dtype=np.float64)
+    out[..., o:o + a.shape[-1]] = a
+    return out
+
+
+def forward_1d(x, w, pad, c, fft=None):
+    N, C, Lx = x.shape
+    K = w.shape[-1]
+    g = geometry_1d(Lx, K, pad, fft)
+    M = mask_1d(g["L"], c)[0]
+    X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
+    Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
+    Y = _channel_contract(X[..., None, :], Wf[..., None, :], conj_b=True)[..., 0, :]
+    return np.fft.irfft(Y, n=g["L"])[..., : g["Lo"]]
+
+
+def backward_input_1d(dy, w, Lx, pad, c, fft=None):
+    K = w.shape[-1]
+    g = geometry_1d(Lx, K, pad, fft)
+    M = mask_1d(g["L"], c)[0]
+    DY = np.fft.rfft(_embed1(np.asarray(dy, np.float64), g["L"], 0)) * M
+    Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
+    DX = _channel_contract(DY[..., None, :], np.swapaxes(Wf, 0, 1)[..., None, :], conj_b=False)[..., 0, :]
+    return np.fft.irfft(DX, n=g["L"])[..., pad[0]:pad[0] + Lx]
+
+
+def backward_weight_1d(x, dy, K, pad, c, fft=None):
+    N, C, Lx = x.shape
+    g = geometry_1d(Lx, K, pad, fft)
+    M = mask_1d(g["L"], c)[0]
+    X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
+    DY = np.fft.rfft(_embed1(np.asarray(dy, np.float64), g["L"], 0)) * M
+    DW = _channel_contract(np.swapaxes(X, 0, 1)[..., None, :], np.swapaxes(DY, 0, 1)[..., None, :],
+                           conj_b=True)[..., 0, :]
+    return np.swapaxes(np.fft.irfft(DW, n=g["L"])[..., :K], 0, 1)
+
+
+def kept_spectrum_1d(a, offset, L, c):
+    M = mask_1d(L, c)[0]
+    A = np.fft.rfft(_embed1(np.asarray(a, np.float64), L, offset))
+    flat = A.reshape(-1, A.shape[-1])
+    return np.ascontiguousarray(flat[:, M.astype(bool)].T)
+
+
+def kept_filter_spectrum_1d(w, L, c):
+    M = mask_1d(L, c)[0]
+    Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), L, 0))  # [F, C, B]
+    return np.ascontiguousarray(np.transpose(Wf[:, :, M.astype(bool)], (2, 1, 0)))
+
+
+# ----------------------------------------------------------------------------
+# Dimension-generic front door used by tests and the benchmark's CPU leg
+# ----------------------------------------------------------------------------
+
+
+def forward(x, w, pad, c, fft=None):
+    return forward_1d(x, w, pad, c, fft) if x.ndim == 3 else forward_2d(x, w, pad, c, fft)
+
+
+def backward_input(dy, w, x_spatial, pad, c, fft=None):
+    if dy.ndim == 3:
+        return backward_input_1d(dy, w, x_spatial[0], pad, c, fft)
+    return backward_input_2d(dy, w, x_spatial, pad, c, fft)
+
+
+def backward_weight(x, dy, K, pad, c, fft=None):
+    return backward_weight_1d(x, dy, K, pad, c, fft) if x.ndim == 3 else backward_weight_2d(x, dy, K, pad, c, fft)
+
+
+def mask(ndim, L, c):
+    """Mask for a grid: ndim=1 -> L is an int; ndim=2 -> L is (Lh, Lw)."""
+    return mask_1d(L, c)[0] if ndim == 1 else mask_2d(L[0], L[1], c)[0]
+
+
+def plan_info(ndim, L, c):
+    """(r_h, r_w, kept, total, c_eff) of the mask rule, for comparison with the
+    library's plan report (1-D: r_h = 0, r_w = r)."""
+    if ndim == 1:
+        m, t, r = mask_1d(L, c)
+        kept, total = int(m.sum()), m.size
+        return 0, r, kept, total, 1.0 - kept / total
+    m, t, r_h, r_w = mask_2d(L[0], L[1], c)
+    kept, total = int(m.sum()), m.size
+    return r_h, r_w, kept, total, 1.0 - kept / total
