@@ -1,0 +1,252 @@
+"""Benchmark of the band-limited FFT convolution layer on one MI355X.
+
+One step = forward + grad-input + grad-weight (with map reuse) of every layer
+of the workload at compression rate c, on synthetic inputs already resident
+in HBM.  Default workload: the 3-layer FCN time-series stack (batch 64,
+length 512; channels 1->128->256->128, filters 8/5/3, 'same' padding), c = 0.5.
+
+Prints ONE JSON line: value = TFLOP-equiv/s, where the equivalent work of a
+layer is that of the direct convolution, 3 passes x 2 N C_in C_out Lo K^d
+flops.  Also reported: ms per layer for every c of the workload, the
+roofline of the dominant kernel (per-launch HIP events inside the library)
+and the fp64 CPU oracle timed on a bounded sample (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
+MFMA_F32_PEAK_TF = 157.3   # MI355X dense fp32 matrix, TFLOP/s
+RIDGE = MFMA_F32_PEAK_TF * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload index (1..5)")
+    ap.add_argument("--c", type=float, default=0.5, help="compression rate of the headline value")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the per-c sweep")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--table", default=None, help="also write a per-config/per-c table (JSON lines) here")
+    return ap.parse_args()
+
+
+class Layer:
+    """Device state of one layer: plan, inputs, outputs and workspace."""
+
+    def __init__(self, torch, blconv, layer, arrays, c, dev):
+        self.layer = layer
+        self.plan = blconv.plan_for_layer(layer, c)
+        x, w, dy = arrays
+        self.x, self.w, self.dy = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        self.y = torch.empty(self.plan.y_shape(), device=dev)
+        self.dx = torch.empty(self.plan.x_shape(), device=dev)
+        self.dw = torch.empty(self.plan.w_shape(), device=dev)
+        self.ws = self.plan.workspace(dev)
+        self.blconv = blconv
+
+    def step(self):
+        b = self.blconv
+        self.plan.forward(self.x, self.w, self.y, self.ws)
+        self.plan.backward_input(self.dy, self.w, self.dx, self.ws, flags=b.BL_REUSE_W)
+        self.plan.backward_weight(self.x, self.dy, self.dw, self.ws, flags=b.BL_REUSE_X | b.BL_REUSE_DY)
+
+
+def time_steps(torch, layers, steps, warmup):
+    """Median-free whole-loop timing: ms per step and ms per layer (events between layers)."""
+    for _ in range(warmup):
+        for L in layers:
+            L.step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(layers) + 1)] for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for s in range(steps):
+        for i, L in enumerate(layers):
+            ev[s][i].record()
+            L.step()
+        ev[s][-1].record()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    per_layer = [float(np.median([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)]))
+                 for i in range(len(layers))]
+    return total_ms / steps, per_layer, wall
+
+
+def roofline(torch, blconv, layers, steps):
+    """Per-kernel HIP-event timing inside the library over `steps` steps."""
+    prof = blconv.Profile(capacity=64 * steps * len(layers))
+    torch.cuda.synchronize()
+    with prof:
+        for _ in range(steps):
+            for L in layers:
+                L.step()
+    torch.cuda.synchronize()
+    recs = prof.records()
+    prof.release()
+    agg = {}
+    for name, ms, nb, nf in recs:
+        a = agg.setdefault(name, [0, 0.0, 0.0, 0.0])
+        a[0] += 1; a[1] += ms; a[2] += nb; a[3] += nf
+    kernels = {}
+    for name, (n, ms, nb, nf) in agg.items():
+        s = ms * 1e-3
+        kernels[name] = {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms,
+                         "GBps": nb / s / 1e9, "TFLOPs": nf / s / 1e12 if nf else None,
+                         "hbm_frac": nb / s / 1e9 / HBM_PEAK_GBS,
+                         "mfma_frac": (nf / s / 1e12 / MFMA_F32_PEAK_TF) if nf else None,
+                         "ai": (nf / nb) if nf else None}
+    dom = max(agg, key=lambda k: agg[k][1])
+    n, ms, nb, nf = agg[dom]
+    s = ms * 1e-3
+    if nf and nf / nb > RIDGE:
+        roof = {"kernel": dom, "bound": "mfma", "achieved": nf / s / 1e12, "peak": MFMA_F32_PEAK_TF,
+                "unit": "TFLOP/s", "frac": nf / s / 1e12 / MFMA_F32_PEAK_TF, "traffic": None,
+                "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_flops": nf / n}
+    else:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": nb / s / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": nb / s / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_bytes": nb / n}
+    return roof, kernels
+
+
+def cpu_baseline(cfg, c, target_s):
+    """The fp64 oracle on a bounded sample: the first n samples of the batch."""
+    from oracle import bl_oracle as bo
+    from paper_1911_09287_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    layers = synth.CONFIGS[cfg].layers
+    arrays = [synth.layer_inputs(cfg, i) for i in range(len(layers))]
+
+    def run(n):
+        t = time.perf_counter()
+        flops = 0.0
+        for L, (x, w, dy) in zip(layers, arrays):
+            xs, dys = x[:n], dy[:n]
+            spatial = (L.H,) if L.ndim == 1 else (L.H, L.W)
+            bo.forward(xs, w, L.pad, c)
+            bo.backward_input(dys, w, spatial, L.pad, c)
+            bo.backward_weight(xs, dys, L.K, L.pad, c)
+            flops += 3 * L.direct_flops() * n / L.N
+        return time.perf_counter() - t, flops
+
+    N = layers[0].N
+    n = 1
+    dt, _ = run(n)  # also warms up
+    while n < N and dt * (2 if n * 2 <= N else N / n) < target_s:
+        n = min(N, n * 2)
+        dt, _ = run(n)
+    reps, total, flops = 0, 0.0, 0.0
+    while total < target_s * 0.5 or reps == 0:
+        dt, f = run(n)
+        total += dt; flops += f; reps += 1
+    return {"value": flops / total / 1e12, "unit": "TFLOP-equiv/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 NumPy oracle, fwd+grad-input+grad-weight of all {len(layers)} layers at c={c} on the "
+                      f"first {n} of {N} samples, {reps} repetition(s), {total:.1f} s; numpy.fft single-threaded, "
+                      f"BLAS threads={threads}, host CPUs={len(os.sched_getaffinity(0))}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the band-limited layer is built and measured on a single "
+              "MI355X; run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_1911_09287_amd import blconv, synth
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    blconv.load()
+    dev = torch.device("cuda:0")
+    cfg = synth.CONFIGS[args.config]
+    arrays = [synth.layer_inputs(args.config, i) for i in range(len(cfg.layers))]
+    eq_flops = sum(3 * L.direct_flops() for L in cfg.layers)
+
+    def build(c):
+        return [Layer(torch, blconv, L, a, c, dev) for L, a in zip(cfg.layers, arrays)]
+
+    layers = build(args.c)
+    ms, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup)
+    roof, kernels = roofline(torch, blconv, layers, max(1, min(args.steps, 10)))
+    value = eq_flops / (ms * 1e-3) / 1e12
+
+    per_c = []
+    if not args.no_sweep:
+        for c in cfg.rates:
+            Ls = layers if c == args.c else build(c)
+            m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup)
+            per_c.append({"c": c, "c_eff": [L.plan.c_eff for L in Ls], "ms_per_step": m,
+                          "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12})
+            del Ls
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(args.config, args.c, args.cpu_seconds)
+
+    out = {
+        "metric": "band-limited conv fwd+bwd TFLOP-equiv/s (ms/layer vs c; %HBM / %MFMA peak)",
+        "value": value,
+        "unit": "TFLOP-equiv/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "config_index": args.config, "c": args.c,
+                   "layers": [L.name for L in cfg.layers], "batch": cfg.layers[0].N,
+                   "c_eff": [L.plan.c_eff for L in layers], "ms_per_layer": per_layer,
+                   "equiv_gflop_per_step": eq_flops / 1e9},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "per_c": per_c,
+        "wall_s_timed": wall,
+    }
+    print(json.dumps(out), flush=True)
+
+    if args.table:
+        with open(args.table, "w") as fh:
+            for ci in sorted(synth.CONFIGS):
+                cf = synth.CONFIGS[ci]
+                arr = [synth.layer_inputs(ci, i) for i in range(len(cf.layers))]
+                for c in cf.rates:
+                    for li, (L, a) in enumerate(zip(cf.layers, arr)):
+                        Ls = [Layer(torch, blconv, L, a, c, dev)]
+                        m, _, _ = time_steps(torch, Ls, args.steps, args.warmup)
+                        r, ks = roofline(torch, blconv, Ls, 5)
+                        fh.write(json.dumps({"config": ci, "layer": L.name, "c": c, "c_eff": Ls[0].plan.c_eff,
+                                             "ms": m, "tflop_equiv_s": 3 * L.direct_flops() / (m * 1e-3) / 1e12,
+                                             "kernels": ks}) + "\n")
+                        fh.flush()
+                        del Ls
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,171 @@
+/*
+ * blconv.h -- band-limited FFT convolution layer for AMD Instinct MI355X (gfx950).
+ *
+ * The layer of Dziedzic et al., "Band-limited Training and Inference for
+ * Convolutional Neural Networks" (ICML 2019):
+ *
+ *   Sec. 3, Eq. (1)/(2)  y = F^-1{ (F_x M_c) . conj(F_w M_c) }: the spectra of
+ *                        input and filter are multiplied element-wise after a
+ *                        0/1 low-pass mask M_c, summed over input channels and
+ *                        transformed back.  The layer computes cross-correlation
+ *                        (the filter spectrum enters conjugated), like a
+ *                        deep-learning convolution layer.
+ *   Sec. 3.2.1           input and filter are zero-padded so that the circular
+ *                        correlation of the FFT equals the linear one.
+ *   Sec. 3.2.2, Fig. 2   only the rfft half plane [L_h][L_w/2+1] is kept; the band
+ *                        shrinks in L-shaped layers from the top-left and
+ *                        bottom-left corners: bin (u, v) is kept iff
+ *                        |s(u)| <= r_h and v <= r_w, with s(u) the signed row
+ *                        frequency, r_h = L_h/2 - t, r_w = L_w/2 - t (integer
+ *                        halves).  In 1-D the kept set is the prefix v <= L/2 - t.
+ *   Sec. 3.1, Sec. 4.1   c is the fraction of half-spectrum coefficients
+ *                        discarded.  The number of peeled layers t is the
+ *                        smallest t with kept(t) <= (1 - c) * total, evaluated in
+ *                        IEEE double ("discard at least c"); if no t qualifies,
+ *                        the most layers that can be peeled.
+ *   Abstract, Sec. 1     the band limit holds in forward and back-propagation:
+ *                        grad-input and grad-weight apply the same mask, so the
+ *                        weight gradient is projected onto the kept frequencies.
+ *   Sec. 3.2.3           map reuse: the spectra of the input and the filter
+ *                        computed by the forward pass are kept (here: in the
+ *                        caller's workspace) and reused by the backward passes.
+ *
+ * FFT grid: by default the padded input size, L_h = H + pad_lo[0] + pad_hi[0]
+ * and L_w = W + pad_lo[1] + pad_hi[1] (1-D: L = length + pad_lo[0] + pad_hi[0]);
+ * this is the smallest grid on which none of the three passes wraps around.
+ * A larger grid (e.g. the map-reuse size N + max(K-1, G-1) of Sec. 3.2.3) may
+ * be requested with fft_h / fft_w; it changes results only when c > 0.
+ *
+ * Layouts (all contiguous, fp32, PyTorch order):
+ *   2-D: x [N][C_in][H][W], w [C_out][C_in][K][K], y and dy [N][C_out][Ho][Wo],
+ *        dx [N][C_in][H][W], dw [C_out][C_in][K][K];
+ *   1-D: x [N][C_in][L],    w [C_out][C_in][K],    y and dy [N][C_out][Lo],
+ *        dx [N][C_in][L],   dw [C_out][C_in][K];
+ *   with Ho = H + pad_lo[0] + pad_hi[0] - K + 1 (and likewise Wo, Lo); stride 1,
+ *   no dilation, no groups, no bias.
+ *
+ * Ownership: the caller owns every device buffer (x, w, y, dy, dx, dw and the
+ * workspace ws).  A plan is host memory only; creating, querying and destroying
+ * it makes no HIP call.  The compute calls allocate nothing, make no host
+ * synchronisation and enqueue their kernels on `stream` (a hipStream_t, passed
+ * as void*; NULL = the default stream).
+ *
+ * Errors: every call returns a bl_status_t.  Arguments are validated on the host
+ * before anything is enqueued; a call that returns an error has enqueued no
+ * kernel, except BL_ERR_HIP, which reports a failed launch (work enqueued before
+ * it by the same call may have run).
+ *
+ * Threading: a plan is immutable after creation; calls with distinct
+ * workspaces may run concurrently from several threads and streams.
+ */
+#ifndef BLCONV_H
+#define BLCONV_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BL_OK = 0,
+  BL_ERR_INVALID_ARG = 1,         /* null pointer, non-positive size, c outside [0,1), grid too small */
+  BL_ERR_UNSUPPORTED = 2,         /* valid but outside what this library implements (e.g. K > 8) */
+  BL_ERR_WORKSPACE_TOO_SMALL = 3, /* reserved for callers that check bl_conv_workspace_size */
+  BL_ERR_HIP = 4,                 /* a HIP launch or runtime call failed */
+  BL_ERR_OOM = 5                  /* host allocation failed */
+} bl_status_t;
+
+typedef struct {
+  int ndim;          /* 1 or 2 */
+  int N, C_in, C_out;
+  int H, W;          /* 2-D: input height and width.  1-D: H = sequence length, W = 1 */
+  int K;             /* filter size: K x K (2-D) or K taps (1-D); 1 <= K <= 8 */
+  int pad_lo[2];     /* leading zeros: [0] rows (1-D: the sequence), [1] columns (1-D: 0) */
+  int pad_hi[2];     /* trailing zeros, same axes */
+  double c;          /* compression rate, 0 <= c < 1 */
+  int fft_h, fft_w;  /* 0 = padded size; else an FFT grid at least the padded size (1-D: fft_h) */
+  unsigned flags;    /* reserved, must be 0 */
+} bl_conv_desc_t;
+
+typedef struct bl_conv_plan_s* bl_conv_plan_t;
+
+/* Flags of the compute calls (map reuse, Sec. 3.2.3).  Every compute call
+ * leaves in the workspace the spectra it computed: forward the input spectrum
+ * X and the filter spectrum W, backward_input the output-gradient spectrum DY
+ * and W, backward_weight X and DY.  A REUSE flag skips recomputing that
+ * spectrum and reads the copy in the workspace instead; the caller asserts that
+ * the tensor it came from has not changed since, which the library cannot
+ * check.  The tensor pointer may then be NULL. */
+#define BL_REUSE_X  0x1u  /* forward, backward_weight: reuse X */
+#define BL_REUSE_W  0x2u  /* forward, backward_input: reuse W */
+#define BL_REUSE_DY 0x4u  /* backward_weight: reuse DY */
+
+/* Build a plan: geometry, the number of peeled layers t for rate c, the kept
+ * bin set and the workspace layout.  Host only. */
+bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_desc_t* desc);
+bl_status_t bl_conv_plan_destroy(bl_conv_plan_t plan);
+
+/* Grid, kept-set radii, counts and the effective rate c_eff = 1 - kept/total.
+ * 1-D: fft_h = L, fft_w = 1, r_h = 0, r_w = r.  Any output pointer may be NULL. */
+bl_status_t bl_conv_plan_info(bl_conv_plan_t plan, int* fft_h, int* fft_w, int* r_h, int* r_w,
+                              long* kept, long* total, double* c_eff);
+
+/* Copy the 0/1 half-plane mask to host memory: n must equal total;
+ * row-major [fft_h][fft_w/2+1] (1-D: [L/2+1]). */
+bl_status_t bl_conv_plan_get_mask(bl_conv_plan_t plan, unsigned char* host_mask, size_t n);
+
+/* Kept bins in the order the stored spectra use (bin-major): rows in
+ * increasing FFT index u, within a row increasing v.  n must equal kept;
+ * u and v are host arrays (1-D: u = 0). */
+bl_status_t bl_conv_plan_get_bins(bl_conv_plan_t plan, int* u, int* v, size_t n);
+
+/* Workspace bytes needed by the compute calls of this plan. */
+bl_status_t bl_conv_workspace_size(bl_conv_plan_t plan, size_t* bytes);
+
+/* Byte offsets of the stored spectra inside the workspace (any pointer may be
+ * NULL).  All are interleaved complex64, bin-major:
+ *   X  [kept][N][C_in], W [kept][C_in][C_out], DY [kept][N][C_out]. */
+bl_status_t bl_conv_workspace_layout(bl_conv_plan_t plan, size_t* off_x, size_t* off_w, size_t* off_dy);
+
+/* y = band-limited correlation of x with w (Eq. 1).  Writes X and W to ws. */
+bl_status_t bl_conv_forward(bl_conv_plan_t plan, const float* x, const float* w, float* y,
+                            void* ws, unsigned flags, void* stream);
+
+/* dx = gradient of <dy, y> with respect to x: the same mask on the spectrum of
+ * dy times the (unconjugated) filter spectrum, summed over output channels,
+ * inverse-transformed and cropped to the unpadded input window.  Writes DY and
+ * W to ws. */
+bl_status_t bl_conv_backward_input(bl_conv_plan_t plan, const float* dy, const float* w, float* dx,
+                                   void* ws, unsigned flags, void* stream);
+
+/* dw = gradient of <dy, y> with respect to w, projected onto the kept band:
+ * sum over the batch of X times conj(DY) per kept bin, inverse-transformed and
+ * cropped to the K x K filter support.  Writes X and DY to ws. */
+bl_status_t bl_conv_backward_weight(bl_conv_plan_t plan, const float* x, const float* dy, float* dw,
+                                    void* ws, unsigned flags, void* stream);
+
+const char* bl_status_string(bl_status_t status);
+
+/* Per-kernel timing, for measurement tools.  While enabled, every kernel the
+ * compute calls enqueue is bracketed by two HIP events on the same stream
+ * (up to `capacity` launches; later launches are not timed).  bl_profile_begin
+ * creates the events (it is the only call that allocates) and must not be
+ * called while work from a previous profile is in flight.  After the stream
+ * has been synchronised, bl_profile_count / bl_profile_get return each
+ * launch's kernel name (a static string), its duration in milliseconds and
+ * its algorithmic cost: the compulsory HBM bytes (every input read once, every
+ * output written once) and, for the channel contraction, the real flops of
+ * the complex products (8 per complex multiply-add).  Output pointers may be
+ * NULL.  bl_profile_end stops recording; bl_profile_release frees the events. */
+bl_status_t bl_profile_begin(int capacity);
+bl_status_t bl_profile_end(void);
+int bl_profile_count(void);
+bl_status_t bl_profile_get(int i, const char** kernel, float* ms, double* bytes, double* flops);
+bl_status_t bl_profile_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BLCONV_H */

@@ -1,0 +1,677 @@
+// HIP kernels and compute entry points of the band-limited convolution, gfx950.
+//
+// Stages of one pass (bin-major spectra [kept bin][plane] complex64):
+//   spec_fwd   zero-pad + real 2-D DFT + band mask of real planes (x or dy):
+//              a row pass that emits only kept columns v <= r_w, then a column
+//              pass over the nonzero input rows that emits only kept rows.
+//              Discarded coefficients are never formed (Sec. 3.2.2, Fig. 2).
+//   spec_filt  filter spectrum at the kept bins, a K x K-tap DFT per bin.
+//   contract   per kept bin, a complex matrix product over channels
+//              (the Hadamard product fused with the channel sum, Sec. 3.3) on
+//              fp32 MFMA, with the complex product embedded in a real one.
+//   spec_inv   zero-fill + inverse real 2-D DFT + crop: only kept bins are read
+//              and only the cropped window is written.
+//   wgrad_idft inverse DFT of the kept weight-gradient bins onto the K x K taps
+//              (the projected weight gradient, Sec. 1).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <mutex>
+#include <vector>
+
+#include "plan.hpp"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr size_t kMaxLds = 64 * 1024;
+
+// e^{sign * 2 pi i k / L}, evaluated in double and rounded once to fp32.
+__device__ inline float2 unit_root(int k, int L, double sign) {
+  double s, c;
+  sincospi(2.0 * (double)k / (double)L, &s, &c);
+  return make_float2((float)c, (float)(sign * s));
+}
+
+__device__ inline void fill_roots(float2* tab, int L, double sign) {
+  for (int k = threadIdx.x; k < L; k += blockDim.x) tab[k] = unit_root(k, L, sign);
+}
+
+__device__ inline int kept_row(int r, int r_h, int Lh, int R) { return r <= r_h ? r : r + (Lh - R); }
+
+// ---------------------------------------------------------------------------
+// spec_fwd: real planes [P][Hin][Win] placed at (oi, oj) of the Lh x Lw grid ->
+// kept spectrum out[b * P + p].  TP planes per block.
+// ---------------------------------------------------------------------------
+struct FwdGeom {
+  int Hin, Win, oi, oj;
+  int Lh, Lw, r_h, R, V;
+  long P;
+  int TP;
+};
+
+__global__ __launch_bounds__(kThreads) void k_spec_fwd(const float* __restrict__ in, float2* __restrict__ out,
+                                                       FwdGeom g) {
+  extern __shared__ float2 smem[];
+  float2* twh = smem;                       // Lh
+  float2* tww = twh + g.Lh;                 // Lw
+  const int Ts = g.Hin * g.V + 1;           // padded plane stride of the row-pass result
+  float2* T = tww + g.Lw;                   // TP * Ts
+  float* xs = reinterpret_cast<float*>(T + (size_t)g.TP * Ts);  // TP * Hin * Win
+
+  const long p0 = (long)blockIdx.x * g.TP;
+  const int np = (int)min((long)g.TP, g.P - p0);
+  const int plane = g.Hin * g.Win;
+
+  fill_roots(twh, g.Lh, -1.0);
+  fill_roots(tww, g.Lw, -1.0);
+  const float* src = in + p0 * plane;
+  for (int e = threadIdx.x; e < np * plane; e += blockDim.x) xs[e] = src[e];
+  __syncthreads();
+
+  // Row pass: T[p][i][v] = sum_j x[p][i][j] e^{-2 pi i v (j + oj) / Lw}, v < V.
+  for (int e = threadIdx.x; e < np * g.Hin * g.V; e += blockDim.x) {
+    const int v = e % g.V;
+    const int pi = e / g.V;  // p * Hin + i
+    const int p = pi / g.Hin, i = pi % g.Hin;
+    const float* xr = xs + (size_t)pi * g.Win;
+    int idx = (int)(((long)v * g.oj) % g.Lw);
+    float re = 0.f, im = 0.f;
+    for (int j = 0; j < g.Win; ++j) {
+      const float2 w = tww[idx];
+      re = fmaf(xr[j], w.x, re);
+      im = fmaf(xr[j], w.y, im);
+      idx += v;
+      if (idx >= g.Lw) idx -= g.Lw;
+    }
+    T[(size_t)p * Ts + i * g.V + v] = make_float2(re, im);
+  }
+  __syncthreads();
+
+  // Column pass over kept rows u; store bin-major, planes fastest.
+  const int B = g.R * g.V;
+  for (int e = threadIdx.x; e < np * B; e += blockDim.x) {
+    const int p = e % np;
+    const int b = e / np;
+    const int r = b / g.V, v = b % g.V;
+    const int u = kept_row(r, g.r_h, g.Lh, g.R);
+    int idx = (int)(((long)u * g.oi) % g.Lh);
+    float re = 0.f, im = 0.f;
+    const float2* tc = T + (size_t)p * Ts + v;
+    for (int i = 0; i < g.Hin; ++i) {
+      const float2 a = tc[i * g.V];
+      const float2 w = twh[idx];
+      re = fmaf(a.x, w.x, fmaf(-a.y, w.y, re));
+      im = fmaf(a.x, w.y, fmaf(a.y, w.x, im));
+      idx += u;
+      if (idx >= g.Lh) idx -= g.Lh;
+    }
+    out[(size_t)b * g.P + p0 + p] = make_float2(re, im);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// spec_inv: kept spectrum in[b * P + p] -> real planes [P][OH][OW] holding the
+// grid window starting at (ci, cj), scaled by 1 / (Lh Lw).  Hermitian (c2r)
+// convention: column v contributes with weight 2 except v = 0 and the Nyquist
+// column of an even Lw, and only the real part of each term is kept.
+// ---------------------------------------------------------------------------
+struct InvGeom {
+  int OH, OW, ci, cj;
+  int Lh, Lw, r_h, R, V;
+  long P;
+  int TP;
+  float scale;
+};
+
+__global__ __launch_bounds__(kThreads) void k_spec_inv(const float2* __restrict__ in, float* __restrict__ out,
+                                                       InvGeom g) {
+  extern __shared__ float2 smem[];
+  float2* twh = smem;        // Lh, e^{+2 pi i k / Lh}
+  float2* tww = twh + g.Lh;  // Lw
+  const int B = g.R * g.V;
+  const int Ss = B + 1;
+  const int Zs = g.OH * g.V + 1;
+  float2* S = tww + g.Lw;                 // TP * Ss
+  float2* Z = S + (size_t)g.TP * Ss;      // TP * Zs
+
+  const long p0 = (long)blockIdx.x * g.TP;
+  const int np = (int)min((long)g.TP, g.P - p0);
+
+  fill_roots(twh, g.Lh, 1.0);
+  fill_roots(tww, g.Lw, 1.0);
+  for (int e = threadIdx.x; e < np * B; e += blockDim.x) {
+    const int p = e % np, b = e / np;
+    S[(size_t)p * Ss + b] = in[(size_t)b * g.P + p0 + p];
+  }
+  __syncthreads();
+
+  // Column pass: Z[p][i][v] = sum_r S[p][r][v] e^{+2 pi i u_r (ci + i) / Lh}.
+  for (int e = threadIdx.x; e < np * g.OH * g.V; e += blockDim.x) {
+    const int v = e % g.V;
+    const int t2 = e / g.V;
+    const int i = t2 % g.OH, p = t2 / g.OH;
+    const int m = (g.ci + i) % g.Lh;
+    float re = 0.f, im = 0.f;
+    const float2* sc = S + (size_t)p * Ss + v;
+    int idx = 0;  // (u * m) mod Lh, u = 0 first
+    for (int r = 0; r < g.R; ++r) {
+      if (r == g.r_h + 1) idx = (int)(((long)(r + g.Lh - g.R) * m) % g.Lh);
+      const float2 a = sc[r * g.V];
+      const float2 w = twh[idx];
+      re = fmaf(a.x, w.x, fmaf(-a.y, w.y, re));
+      im = fmaf(a.x, w.y, fmaf(a.y, w.x, im));
+      idx += m;
+      if (idx >= g.Lh) idx -= g.Lh;
+    }
+    Z[(size_t)p * Zs + i * g.V + v] = make_float2(re, im);
+  }
+  __syncthreads();
+
+  // Row pass: y[p][i][j] = scale * sum_v h_v Re(Z[p][i][v] e^{+2 pi i v (cj + j) / Lw}).
+  const int nyq = (g.Lw % 2 == 0) ? g.Lw / 2 : -1;
+  float* dst = out + p0 * (long)g.OH * g.OW;
+  for (int e = threadIdx.x; e < np * g.OH * g.OW; e += blockDim.x) {
+    const int j = e % g.OW;
+    const int t2 = e / g.OW;
+    const int i = t2 % g.OH, p = t2 / g.OH;
+    const int m = (g.cj + j) % g.Lw;
+    const float2* zr = Z + (size_t)p * Zs + i * g.V;
+    float acc = 0.f;
+    int idx = 0;
+    for (int v = 0; v < g.V; ++v) {
+      const float2 a = zr[v];
+      const float2 w = tww[idx];
+      const float h = (v == 0 || v == nyq) ? 1.f : 2.f;
+      acc = fmaf(h, fmaf(a.x, w.x, -a.y * w.y), acc);
+      idx += m;
+      if (idx >= g.Lw) idx -= g.Lw;
+    }
+    dst[e] = acc * g.scale;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// spec_filt: w [F][C][Kh][Kw] -> W[b][c][f] at the kept bins (origin placement).
+// One thread per (c, f) pair; blockIdx.y strides over chunks of bins.
+// ---------------------------------------------------------------------------
+struct FiltGeom {
+  int F, C, Kh, Kw;
+  int Lh, Lw, r_h, R, V;
+  int bins_per_block;
+};
+
+template <int KH, int KW>
+__global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, float2* __restrict__ out,
+                                                        FiltGeom g) {
+  extern __shared__ float2 smem[];
+  float2* twh = smem;
+  float2* tww = twh + g.Lh;
+  fill_roots(twh, g.Lh, -1.0);
+  fill_roots(tww, g.Lw, -1.0);
+  __syncthreads();
+  const long CF = (long)g.C * g.F;
+  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;  // q = c * F + f
+  if (q >= CF) return;
+  const int c = (int)(q / g.F), f = (int)(q % g.F);
+  float tap[KH][KW];
+  const float* wp = w + ((size_t)f * g.C + c) * KH * KW;
+#pragma unroll
+  for (int a = 0; a < KH; ++a)
+#pragma unroll
+    for (int b = 0; b < KW; ++b) tap[a][b] = wp[a * KW + b];
+  const int B = g.R * g.V;
+  const int b0 = blockIdx.y * g.bins_per_block;
+  const int b1 = min(B, b0 + g.bins_per_block);
+  for (int bin = b0; bin < b1; ++bin) {
+    const int r = bin / g.V, v = bin % g.V;
+    const int u = kept_row(r, g.r_h, g.Lh, g.R);
+    float re = 0.f, im = 0.f;
+#pragma unroll
+    for (int a = 0; a < KH; ++a) {
+      // row sum over columns: sum_b tap[a][b] e^{-2 pi i v b / Lw}
+      float rr = 0.f, ri = 0.f;
+#pragma unroll
+      for (int b = 0; b < KW; ++b) {
+        const float2 t = tww[(v * b) % g.Lw];
+        rr = fmaf(tap[a][b], t.x, rr);
+        ri = fmaf(tap[a][b], t.y, ri);
+      }
+      const float2 t = twh[(u * a) % g.Lh];
+      re = fmaf(rr, t.x, fmaf(-ri, t.y, re));
+      im = fmaf(rr, t.y, fmaf(ri, t.x, im));
+    }
+    out[(size_t)bin * CF + q] = make_float2(re, im);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// wgrad_idft: DW[b][c][f] -> dw[f][c][a][b'] = scale * sum_{kept (u, v)}
+//   h_v Re(DW[u, v][c][f] e^{+2 pi i (u a / Lh + v b' / Lw)}),  a < Kh, b' < Kw.
+// ---------------------------------------------------------------------------
+template <int KH, int KW>
+__global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, float* __restrict__ dw,
+                                                         FiltGeom g, float scale) {
+  extern __shared__ float2 smem[];
+  float2* twh = smem;
+  float2* tww = twh + g.Lh;
+  fill_roots(twh, g.Lh, 1.0);
+  fill_roots(tww, g.Lw, 1.0);
+  __syncthreads();
+  const long CF = (long)g.C * g.F;
+  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= CF) return;
+  const int c = (int)(q / g.F), f = (int)(q % g.F);
+  float acc[KH][KW];
+#pragma unroll
+  for (int a = 0; a < KH; ++a)
+#pragma unroll
+    for (int b = 0; b < KW; ++b) acc[a][b] = 0.f;
+  const int nyq = (g.Lw % 2 == 0) ? g.Lw / 2 : -1;
+  for (int v = 0; v < g.V; ++v) {
+    float zr[KH], zi[KH];
+#pragma unroll
+    for (int a = 0; a < KH; ++a) { zr[a] = 0.f; zi[a] = 0.f; }
+    for (int r = 0; r < g.R; ++r) {
+      const int u = kept_row(r, g.r_h, g.Lh, g.R);
+      const float2 d = DW[(size_t)(r * g.V + v) * CF + q];
+#pragma unroll
+      for (int a = 0; a < KH; ++a) {
+        const float2 t = twh[(u * a) % g.Lh];
+        zr[a] = fmaf(d.x, t.x, fmaf(-d.y, t.y, zr[a]));
+        zi[a] = fmaf(d.x, t.y, fmaf(d.y, t.x, zi[a]));
+      }
+    }
+    const float h = (v == 0 || v == nyq) ? 1.f : 2.f;
+#pragma unroll
+    for (int b = 0; b < KW; ++b) {
+      const float2 t = tww[(v * b) % g.Lw];
+#pragma unroll
+      for (int a = 0; a < KH; ++a) acc[a][b] = fmaf(h, fmaf(zr[a], t.x, -zi[a] * t.y), acc[a][b]);
+    }
+  }
+  float* o = dw + ((size_t)f * g.C + c) * KH * KW;
+#pragma unroll
+  for (int a = 0; a < KH; ++a)
+#pragma unroll
+    for (int b = 0; b < KW; ++b) o[a * KW + b] = acc[a][b] * scale;
+}
+
+// ---------------------------------------------------------------------------
+// contract: per kept bin, O[m][n] = sum_k A[m][k] * op(B[k][n]) in complex64,
+// op = conj or identity.  The complex product is embedded in a real GEMM:
+// A is read as a real [M x 2K] matrix (interleaved re/im), B as the real
+// [2K x 2N] matrix of 2x2 blocks [[br, -bi], [bi, br]] (conj) or
+// [[br, bi], [-bi, br]] (identity), and the real output [M x 2N] is the
+// interleaved complex O.  fp32 MFMA 32x32x2: each 2-deep real k step is one
+// complex k.  Block tile: 64 rows x 32 complex columns, 16 complex k per stage;
+// wave w owns rows 32*(w/2).. and complex columns 16*(w%2)...
+// ---------------------------------------------------------------------------
+struct ContractArgs {
+  int M, N, K;
+  long sAm, sAk, sBk, sBn, ldo;  // element strides (complex units)
+  long bA, bB, bO;               // per-bin strides
+  int tiles_n;
+};
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int CBM = 64, CBN = 32, CBK = 16;
+
+template <bool A_K_CONTIG, bool B_N_CONTIG, bool CONJ>
+__global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict__ A, const float2* __restrict__ Bm,
+                                                       float2* __restrict__ O, ContractArgs g) {
+  __shared__ float As[2][CBK][CBM];
+  __shared__ float Bs[2][CBK][CBN];
+  const int bin = blockIdx.y;
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  const int m0 = tm * CBM, n0 = tn * CBN;
+  const float2* Ab = A + (size_t)bin * g.bA;
+  const float2* Bb = Bm + (size_t)bin * g.bB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 16;
+
+  // B operand selection for lane: real column j = lane % 32 -> complex column
+  // wn + j/2, part bcol = j & 1; real k row a = lane / 32.
+  const int a_part = lane >> 5;
+  const int jcol = lane & 31;
+  const int bcol = jcol & 1;
+  const int bn = wn + (jcol >> 1);
+  const int b_src = (a_part == bcol) ? 0 : 1;  // take br on the diagonal, bi off it
+  float b_sign = 1.f;
+  if (CONJ && a_part == 0 && bcol == 1) b_sign = -1.f;
+  if (!CONJ && a_part == 1 && bcol == 0) b_sign = -1.f;
+
+  floatx16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+
+  for (int k0 = 0; k0 < g.K; k0 += CBK) {
+    // A tile: 64 rows x 16 complex k
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      int m, k;
+      if (A_K_CONTIG) {
+        const int e = tid * 4 + it;  // 0..1023
+        m = e >> 4; k = e & 15;
+      } else {
+        const int e = tid * 4 + it;
+        k = e >> 6; m = e & 63;
+      }
+      float2 v = make_float2(0.f, 0.f);
+      if (m0 + m < g.M && k0 + k < g.K) v = Ab[(size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk];
+      As[0][k][m] = v.x;
+      As[1][k][m] = v.y;
+    }
+    // B tile: 16 complex k x 32 complex n
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      int k, n;
+      const int e = tid * 2 + it;  // 0..511
+      if (B_N_CONTIG) { k = e >> 5; n = e & 31; }
+      else { n = e >> 4; k = e & 15; }
+      float2 v = make_float2(0.f, 0.f);
+      if (n0 + n < g.N && k0 + k < g.K) v = Bb[(size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn];
+      Bs[0][k][n] = v.x;
+      Bs[1][k][n] = v.y;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < CBK; ++s) {
+      const float av = As[a_part][s][wm + (lane & 31)];
+      const float bv = b_sign * Bs[b_src][s][bn];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // D[i][j]: VGPR v holds row 8*(v/4) + 4*(lane/32) + v%4, column lane%32.
+  float* Of = reinterpret_cast<float*>(O + (size_t)bin * g.bO);
+  const int n = n0 + bn;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int i = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    const int m = m0 + wm + i;
+    if (m < g.M && n < g.N) Of[((size_t)m * g.ldo + n) * 2 + bcol] = acc[v];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-kernel timing (bl_profile_*)
+// ---------------------------------------------------------------------------
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  int cap = 0, used = 0;
+  std::vector<hipEvent_t> ev;
+  std::vector<const char*> names;
+  std::vector<double> bytes, flops;
+} g_prof;
+
+int prof_slot(const char* name, double bytes, double flops) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.used >= g_prof.cap) return -1;
+  g_prof.names[g_prof.used] = name;
+  g_prof.bytes[g_prof.used] = bytes;
+  g_prof.flops[g_prof.used] = flops;
+  return g_prof.used++;
+}
+
+// Launch with optional event timing.  `bytes` and `flops` are the launch's
+// algorithmic HBM traffic (compulsory reads + writes) and arithmetic, reported
+// with the timing so that measurement tools can place it on a roofline.
+template <typename Launch>
+bl_status_t timed_launch(const char* name, double bytes, double flops, hipStream_t s, Launch&& launch) {
+  const int slot = prof_slot(name, bytes, flops);
+  if (slot >= 0 && hipEventRecord(g_prof.ev[2 * slot], s) != hipSuccess) return BL_ERR_HIP;
+  launch();
+  if (hipGetLastError() != hipSuccess) return BL_ERR_HIP;
+  if (slot >= 0 && hipEventRecord(g_prof.ev[2 * slot + 1], s) != hipSuccess) return BL_ERR_HIP;
+  return BL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap) {
+  int tp = (int)std::min<long>(cap, P);
+  while (tp > 1 && fixed_bytes + tp * per_plane_bytes > kMaxLds) --tp;
+  return std::max(tp, 1);
+}
+
+// Real planes [P][Hin][Win] at offset (oi, oj) -> bin-major kept spectrum.
+bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+                            int oj, hipStream_t s) {
+  FwdGeom g{Hin, Win, oi, oj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0};
+  const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
+  const size_t per = (size_t)(Hin * p->V + 1) * sizeof(float2) + (size_t)Hin * Win * sizeof(float);
+  if (fixed + per > kMaxLds) return BL_ERR_UNSUPPORTED;
+  g.TP = planes_per_block(fixed, per, P, 16);
+  const size_t lds = fixed + g.TP * per;
+  const long blocks = (P + g.TP - 1) / g.TP;
+  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
+  return timed_launch("spec_fwd", bytes, 0.0, s, [&] {
+    hipLaunchKernelGGL(k_spec_fwd, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
+  });
+}
+
+bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                            int cj, hipStream_t s) {
+  InvGeom g{OH, OW, ci, cj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0, 1.0f / ((float)p->Lh * (float)p->Lw)};
+  const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
+  const size_t per = (size_t)(p->R * p->V + 1 + OH * p->V + 1) * sizeof(float2);
+  if (fixed + per > kMaxLds) return BL_ERR_UNSUPPORTED;
+  g.TP = planes_per_block(fixed, per, P, 16);
+  const size_t lds = fixed + g.TP * per;
+  const long blocks = (P + g.TP - 1) / g.TP;
+  const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
+  return timed_launch("spec_inv", bytes, 0.0, s, [&] {
+    hipLaunchKernelGGL(k_spec_inv, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
+  });
+}
+
+#define BL_FILT_CASES(X) \
+  X(1, 1) X(1, 2) X(1, 3) X(1, 4) X(1, 5) X(1, 6) X(1, 7) X(1, 8) \
+  X(2, 2) X(3, 3) X(4, 4) X(5, 5) X(6, 6) X(7, 7) X(8, 8)
+
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* out, hipStream_t s) {
+  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
+  const long CF = (long)p->Cin * p->Cout;
+  const int B = p->R * p->V;
+  const long xblocks = (CF + kThreads - 1) / kThreads;
+  // aim for about 1024 blocks in all
+  int chunks = (int)std::max<long>(1, std::min<long>(B, (1024 + xblocks - 1) / xblocks));
+  g.bins_per_block = (B + chunks - 1) / chunks;
+  chunks = (B + g.bins_per_block - 1) / g.bins_per_block;
+  const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
+  dim3 grid((unsigned)xblocks, (unsigned)chunks);
+  const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * 8;
+#define X(a, b)                                                                                 \
+  if (p->Kh == a && p->Kw == b)                                                                 \
+    return timed_launch("spec_filt", bytes, 0.0, s, [&] {                                      \
+      hipLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, w, out, g);        \
+    });
+  BL_FILT_CASES(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, hipStream_t s) {
+  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
+  const long CF = (long)p->Cin * p->Cout;
+  const long blocks = (CF + kThreads - 1) / kThreads;
+  const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
+  const float scale = 1.0f / ((float)p->Lh * (float)p->Lw);
+  const double bytes = (double)CF * p->kept * 8 + (double)CF * p->Kh * p->Kw * 4;
+#define X(a, b)                                                                                       \
+  if (p->Kh == a && p->Kw == b)                                                                       \
+    return timed_launch("wgrad_idft", bytes, 0.0, s, [&] {                                           \
+      hipLaunchKernelGGL((k_wgrad_idft<a, b>), dim3((unsigned)blocks), dim3(kThreads), lds, s, DW, dw, g, \
+                         scale);                                                                      \
+    });
+  BL_FILT_CASES(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+enum class Contract { Forward, GradInput, GradWeight };
+
+bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+                            hipStream_t s) {
+  ContractArgs g{};
+  const long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
+  switch (which) {
+    case Contract::Forward:  // Y[n][f] = sum_c X[n][c] conj(W[c][f])
+      g.M = (int)N; g.N = (int)Co; g.K = (int)Ci;
+      g.sAm = Ci; g.sAk = 1; g.sBk = Co; g.sBn = 1; g.ldo = Co;
+      g.bA = N * Ci; g.bB = Ci * Co; g.bO = N * Co;
+      break;
+    case Contract::GradInput:  // DX[n][c] = sum_f DY[n][f] W[c][f]
+      g.M = (int)N; g.N = (int)Ci; g.K = (int)Co;
+      g.sAm = Co; g.sAk = 1; g.sBk = 1; g.sBn = Co; g.ldo = Ci;
+      g.bA = N * Co; g.bB = Ci * Co; g.bO = N * Ci;
+      break;
+    case Contract::GradWeight:  // DW[c][f] = sum_n X[n][c] conj(DY[n][f])
+      g.M = (int)Ci; g.N = (int)Co; g.K = (int)N;
+      g.sAm = 1; g.sAk = Ci; g.sBk = Co; g.sBn = 1; g.ldo = Co;
+      g.bA = N * Ci; g.bB = N * Co; g.bO = Ci * Co;
+      break;
+  }
+  const int tiles_m = (g.M + CBM - 1) / CBM;
+  g.tiles_n = (g.N + CBN - 1) / CBN;
+  if (B > 65535) return BL_ERR_UNSUPPORTED;
+  dim3 grid((unsigned)(tiles_m * g.tiles_n), (unsigned)B);
+  // complex MAC = 8 real flops; compulsory traffic: both operands and the result once
+  const double flops = 8.0 * B * g.M * g.N * g.K;
+  const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
+  switch (which) {
+    case Contract::Forward:
+      return timed_launch("contract_fwd", bytes, flops, s, [&] {
+        hipLaunchKernelGGL((k_contract<true, true, true>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      });
+    case Contract::GradInput:
+      return timed_launch("contract_dgrad", bytes, flops, s, [&] {
+        hipLaunchKernelGGL((k_contract<true, false, false>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      });
+    case Contract::GradWeight:
+      return timed_launch("contract_wgrad", bytes, flops, s, [&] {
+        hipLaunchKernelGGL((k_contract<false, true, true>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      });
+  }
+  return BL_ERR_INVALID_ARG;
+}
+
+inline float2* ws_at(void* ws, size_t off) { return reinterpret_cast<float2*>(static_cast<char*>(ws) + off); }
+
+#define BL_TRY(expr)                    \
+  do {                                  \
+    bl_status_t st_ = (expr);           \
+    if (st_ != BL_OK) return st_;       \
+  } while (0)
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI compute entry points
+// ---------------------------------------------------------------------------
+extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const float* w, float* y, void* ws,
+                                       unsigned flags, void* stream) {
+  if (!p || !y || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~(BL_REUSE_X | BL_REUSE_W)) return BL_ERR_INVALID_ARG;
+  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_W) && !w)) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* X = ws_at(ws, p->off_X);
+  float2* Wf = ws_at(ws, p->off_W);
+  float2* T = ws_at(ws, p->off_T);
+  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  if (!(flags & BL_REUSE_X))
+    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, s));
+  return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
+}
+
+extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy, const float* w, float* dx,
+                                              void* ws, unsigned flags, void* stream) {
+  if (!p || !dy || !dx || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~BL_REUSE_W) return BL_ERR_INVALID_ARG;
+  if (!(flags & BL_REUSE_W) && !w) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* Wf = ws_at(ws, p->off_W);
+  float2* DY = ws_at(ws, p->off_DY);
+  float2* T = ws_at(ws, p->off_T);
+  BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
+  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, s));
+  return launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s);
+}
+
+extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x, const float* dy, float* dw,
+                                               void* ws, unsigned flags, void* stream) {
+  if (!p || !dw || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~(BL_REUSE_X | BL_REUSE_DY)) return BL_ERR_INVALID_ARG;
+  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_DY) && !dy)) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* X = ws_at(ws, p->off_X);
+  float2* DY = ws_at(ws, p->off_DY);
+  float2* DW = ws_at(ws, p->off_DW);
+  if (!(flags & BL_REUSE_X))
+    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  if (!(flags & BL_REUSE_DY))
+    BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
+  BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, s));
+  return launch_wgrad_idft(p, DW, dw, s);
+}
+
+// ---------------------------------------------------------------------------
+// Profiling entry points
+// ---------------------------------------------------------------------------
+extern "C" bl_status_t bl_profile_begin(int capacity) {
+  if (capacity <= 0) return BL_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if ((int)g_prof.ev.size() < 2 * capacity) {
+    for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+    g_prof.ev.assign(2 * capacity, nullptr);
+    for (auto& e : g_prof.ev)
+      if (hipEventCreate(&e) != hipSuccess) return BL_ERR_HIP;
+  }
+  g_prof.names.assign(capacity, nullptr);
+  g_prof.bytes.assign(capacity, 0.0);
+  g_prof.flops.assign(capacity, 0.0);
+  g_prof.cap = capacity;
+  g_prof.used = 0;
+  g_prof.on = true;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_profile_end(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  return BL_OK;
+}
+
+extern "C" int bl_profile_count(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  return g_prof.used;
+}
+
+extern "C" bl_status_t bl_profile_get(int i, const char** kernel, float* ms, double* bytes, double* flops) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (i < 0 || i >= g_prof.used) return BL_ERR_INVALID_ARG;
+  if (kernel) *kernel = g_prof.names[i];
+  if (bytes) *bytes = g_prof.bytes[i];
+  if (flops) *flops = g_prof.flops[i];
+  if (ms) {
+    if (hipEventElapsedTime(ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]) != hipSuccess) return BL_ERR_HIP;
+  }
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_profile_release(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.names.clear();
+  g_prof.cap = g_prof.used = 0;
+  g_prof.on = false;
+  return BL_OK;
+}

@@ -1,0 +1,168 @@
+// Host plan of the band-limited convolution: geometry, kept band, workspace.
+// Pure host code; makes no HIP call, so plans can be built and inspected on a
+// machine without a GPU.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "plan.hpp"
+
+namespace {
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Kept count after peeling t L-shaped layers (Sec. 3.2.2, Fig. 2): rows with
+// |s(u)| <= Lh/2 - t times columns v <= Lw/2 - t of the half plane.
+long kept_after(int t, int Lh, int Lw, int ndim) {
+  if (ndim == 1) return (long)(Lw / 2 + 1 - t);
+  int r_h = Lh / 2 - t, r_w = Lw / 2 - t;
+  return (long)bl_rows_for_radius(r_h, Lh) * (long)(r_w + 1);
+}
+
+}  // namespace
+
+extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_desc_t* d) {
+  if (!out || !d) return BL_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (d->ndim != 1 && d->ndim != 2) return BL_ERR_INVALID_ARG;
+  if (d->N <= 0 || d->C_in <= 0 || d->C_out <= 0 || d->H <= 0 || d->K <= 0) return BL_ERR_INVALID_ARG;
+  if (d->pad_lo[0] < 0 || d->pad_hi[0] < 0 || d->pad_lo[1] < 0 || d->pad_hi[1] < 0) return BL_ERR_INVALID_ARG;
+  if (!(d->c >= 0.0 && d->c < 1.0)) return BL_ERR_INVALID_ARG;  // also rejects NaN
+  if (d->fft_h < 0 || d->fft_w < 0) return BL_ERR_INVALID_ARG;
+  if (d->flags != 0) return BL_ERR_INVALID_ARG;
+  if (d->ndim == 1 && (d->W != 1 || d->pad_lo[1] != 0 || d->pad_hi[1] != 0 || d->fft_w > 1))
+    return BL_ERR_INVALID_ARG;
+  if (d->ndim == 2 && d->W <= 0) return BL_ERR_INVALID_ARG;
+  if (d->K > 8) return BL_ERR_UNSUPPORTED;
+
+  bl_conv_plan_s* p = new (std::nothrow) bl_conv_plan_s();
+  if (!p) return BL_ERR_OOM;
+  p->desc = *d;
+  p->ndim = d->ndim;
+  p->N = d->N; p->Cin = d->C_in; p->Cout = d->C_out;
+  if (d->ndim == 2) {
+    p->Hi = d->H; p->Wi = d->W; p->Kh = d->K; p->Kw = d->K;
+    p->pt = d->pad_lo[0]; p->pb = d->pad_hi[0]; p->pl = d->pad_lo[1]; p->pr = d->pad_hi[1];
+  } else {
+    p->Hi = 1; p->Wi = d->H; p->Kh = 1; p->Kw = d->K;
+    p->pt = 0; p->pb = 0; p->pl = d->pad_lo[0]; p->pr = d->pad_hi[0];
+  }
+  p->Hp = p->Hi + p->pt + p->pb;
+  p->Wp = p->Wi + p->pl + p->pr;
+  p->Ho = p->Hp - p->Kh + 1;
+  p->Wo = p->Wp - p->Kw + 1;
+  if (p->Ho < 1 || p->Wo < 1) { delete p; return BL_ERR_INVALID_ARG; }
+  if (d->ndim == 2) {
+    p->Lh = d->fft_h ? d->fft_h : p->Hp;
+    p->Lw = d->fft_w ? d->fft_w : p->Wp;
+  } else {
+    p->Lh = 1;
+    p->Lw = d->fft_h ? d->fft_h : p->Wp;
+  }
+  if (p->Lh < p->Hp || p->Lw < p->Wp) { delete p; return BL_ERR_INVALID_ARG; }
+  if (p->Lw > 4096 || p->Lh > 4096) { delete p; return BL_ERR_UNSUPPORTED; }
+  p->Wh = p->Lw / 2 + 1;
+  p->total = (long)p->Lh * (long)p->Wh;
+
+  // Rate -> layers: the fewest t with kept(t) <= (1 - c) * total, in double.
+  int t_max = (d->ndim == 1) ? p->Wh - 1 : std::min(p->Lh / 2, p->Lw / 2);
+  const double budget = (1.0 - d->c) * (double)p->total;
+  int t = t_max;
+  for (int tt = 0; tt <= t_max; ++tt) {
+    if ((double)kept_after(tt, p->Lh, p->Lw, d->ndim) <= budget) { t = tt; break; }
+  }
+  p->t = t;
+  if (d->ndim == 1) {
+    p->r_h = 0;
+    p->r_w = p->Wh - 1 - t;
+    p->R = 1;
+  } else {
+    p->r_h = p->Lh / 2 - t;
+    p->r_w = p->Lw / 2 - t;
+    p->R = bl_rows_for_radius(p->r_h, p->Lh);
+  }
+  p->V = p->r_w + 1;
+  p->kept = (long)p->R * p->V;
+  p->c_eff = 1.0 - (double)p->kept / (double)p->total;
+
+  p->mask.assign((size_t)p->total, 0);
+  for (int r = 0; r < p->R; ++r) {
+    int u = bl_kept_row(r, p->r_h, p->Lh, p->R);
+    for (int v = 0; v < p->V; ++v) p->mask[(size_t)u * p->Wh + v] = 1;
+  }
+
+  const size_t cb = 8;  // complex64
+  const size_t B = (size_t)p->kept;
+  size_t o = 0;
+  p->off_X = o;  o = align_up(o + B * p->N * p->Cin * cb, 256);
+  p->off_W = o;  o = align_up(o + B * p->Cin * p->Cout * cb, 256);
+  p->off_DY = o; o = align_up(o + B * p->N * p->Cout * cb, 256);
+  p->off_T = o;  o = align_up(o + B * p->N * (size_t)std::max(p->Cin, p->Cout) * cb, 256);
+  p->off_DW = o; o = align_up(o + B * p->Cin * p->Cout * cb, 256);
+  p->ws_bytes = o;
+  *out = p;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_plan_destroy(bl_conv_plan_t p) {
+  if (!p) return BL_ERR_INVALID_ARG;
+  delete p;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_plan_info(bl_conv_plan_t p, int* fft_h, int* fft_w, int* r_h, int* r_w,
+                                         long* kept, long* total, double* c_eff) {
+  if (!p) return BL_ERR_INVALID_ARG;
+  if (fft_h) *fft_h = p->ndim == 1 ? p->Lw : p->Lh;
+  if (fft_w) *fft_w = p->ndim == 1 ? 1 : p->Lw;
+  if (r_h) *r_h = p->r_h;
+  if (r_w) *r_w = p->r_w;
+  if (kept) *kept = p->kept;
+  if (total) *total = p->total;
+  if (c_eff) *c_eff = p->c_eff;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_plan_get_mask(bl_conv_plan_t p, unsigned char* m, size_t n) {
+  if (!p || !m || n != (size_t)p->total) return BL_ERR_INVALID_ARG;
+  std::memcpy(m, p->mask.data(), n);
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_plan_get_bins(bl_conv_plan_t p, int* u, int* v, size_t n) {
+  if (!p || !u || !v || n != (size_t)p->kept) return BL_ERR_INVALID_ARG;
+  size_t b = 0;
+  for (int r = 0; r < p->R; ++r)
+    for (int vv = 0; vv < p->V; ++vv, ++b) {
+      u[b] = bl_kept_row(r, p->r_h, p->Lh, p->R);
+      v[b] = vv;
+    }
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_workspace_size(bl_conv_plan_t p, size_t* bytes) {
+  if (!p || !bytes) return BL_ERR_INVALID_ARG;
+  *bytes = p->ws_bytes;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_workspace_layout(bl_conv_plan_t p, size_t* off_x, size_t* off_w, size_t* off_dy) {
+  if (!p) return BL_ERR_INVALID_ARG;
+  if (off_x) *off_x = p->off_X;
+  if (off_w) *off_w = p->off_W;
+  if (off_dy) *off_dy = p->off_DY;
+  return BL_OK;
+}
+
+extern "C" const char* bl_status_string(bl_status_t s) {
+  switch (s) {
+    case BL_OK: return "ok";
+    case BL_ERR_INVALID_ARG: return "invalid argument";
+    case BL_ERR_UNSUPPORTED: return "unsupported configuration";
+    case BL_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case BL_ERR_HIP: return "HIP error";
+    case BL_ERR_OOM: return "out of host memory";
+  }
+  return "unknown status";
+}

@@ -1,0 +1,43 @@
+// Internal plan structure shared by the host plan code and the launchers.
+//
+// Every problem is held in "row form": a 2-D layer is an Hi x Wi plane on an
+// Lh x Lw grid; a 1-D layer is a single row (Hi = 1, Lh = 1) of length Wi on a
+// grid of length Lw.  With Lh = 1 the kept-row set is {u = 0} and the 2-D
+// kernels reduce to the 1-D transform, so one set of kernels serves both.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/blconv.h"
+
+struct bl_conv_plan_s {
+  bl_conv_desc_t desc;
+  int ndim;
+  int N, Cin, Cout;
+  // row form
+  int Hi, Wi;          // input plane
+  int Kh, Kw;          // filter support
+  int pt, pb, pl, pr;  // zero padding
+  int Hp, Wp;          // padded input
+  int Ho, Wo;          // output plane
+  int Lh, Lw;          // FFT grid
+  int Wh;              // half-plane width Lw/2 + 1
+  int t, r_h, r_w;     // peeled layers and radii of the kept band
+  int R, V;            // kept rows and kept columns
+  long kept, total;
+  double c_eff;
+  std::vector<uint8_t> mask;  // [Lh][Wh]
+  // workspace layout (bytes)
+  size_t off_X, off_W, off_DY, off_T, off_DW, ws_bytes;
+};
+
+// FFT row index of the r-th kept row: the top-left corner (u = 0..r_h) first,
+// then the bottom-left corner (u = Lh - r_h .. Lh - 1).
+inline int bl_kept_row(int r, int r_h, int Lh, int R) { return r <= r_h ? r : r + (Lh - R); }
+
+// Number of kept rows for radius r on an axis of length L.
+inline int bl_rows_for_radius(int r, int L) {
+  return (L % 2 == 0 && r == L / 2) ? L : 2 * r + 1;
+}

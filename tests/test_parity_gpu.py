@@ -1,0 +1,166 @@
+"""GPU parity: the HIP library against the fp64 oracle on identical inputs.
+
+Bar: relative Frobenius error <= 1e-4 for y, dx and dw (fp32 path vs fp64
+oracle); stored spectra <= 1e-5 at unit level; masks byte-equal (CPU test).
+Every compute call goes through the C ABI (ctypes binding).
+"""
+import numpy as np
+import pytest
+
+from oracle import bl_oracle as bo
+from paper_1911_09287_amd import blconv, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+SPEC_TOL = 1e-5
+
+
+def rel(a, b):
+    return float(np.linalg.norm(np.ravel(a - b)) / max(np.linalg.norm(np.ravel(b)), 1e-30))
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _torch
+    if not _torch.cuda.is_available():
+        pytest.skip("no GPU")
+    blconv.load()
+    return _torch
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def gpu_passes(torch, layer, c, x, w, dy, reuse=True, poison=True, fft=None):
+    plan = blconv.plan_for_layer(layer, c, fft)
+    dev = torch.device("cuda:0")
+    ws = plan.workspace(dev)
+    if poison:
+        ws.fill_(0xFF)  # every float32 word of the workspace is a NaN
+    xt, wt, dyt = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+    nan = float("nan")
+    y = torch.full(plan.y_shape(), nan, device=dev) if poison else torch.empty(plan.y_shape(), device=dev)
+    dx = torch.full(plan.x_shape(), nan, device=dev) if poison else torch.empty(plan.x_shape(), device=dev)
+    dw = torch.full(plan.w_shape(), nan, device=dev) if poison else torch.empty(plan.w_shape(), device=dev)
+    plan.forward(xt, wt, y, ws)
+    plan.backward_input(dyt, wt, dx, ws, flags=blconv.BL_REUSE_W if reuse else 0)
+    plan.backward_weight(xt, dyt, dw, ws, flags=(blconv.BL_REUSE_X | blconv.BL_REUSE_DY) if reuse else 0)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy(), plan, ws
+
+
+def oracle_passes(layer, c, x, w, dy, fft=None):
+    spatial = (layer.H,) if layer.ndim == 1 else (layer.H, layer.W)
+    return (bo.forward(x, w, layer.pad, c, fft), bo.backward_input(dy, w, spatial, layer.pad, c, fft),
+            bo.backward_weight(x, dy, layer.K, layer.pad, c, fft))
+
+
+CASES = [(cfg, li, c) for cfg in sorted(synth.CONFIGS) for li in range(len(synth.CONFIGS[cfg].layers))
+         for c in synth.CONFIGS[cfg].rates]
+
+
+@pytest.mark.parametrize("cfg,li,c", CASES, ids=[f"C{a}-L{b}-c{c}" for a, b, c in CASES])
+def test_config_parity(torch, cfg, li, c):
+    layer = synth.CONFIGS[cfg].layers[li]
+    say(f"[parity] config {cfg} layer {layer.name} c={c}")
+    x, w, dy = synth.layer_inputs(cfg, li)
+    y, dx, dw, plan, ws = gpu_passes(torch, layer, c, x, w, dy)
+    ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+    errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+    say(f"    rel err y={errs[0]:.2e} dx={errs[1]:.2e} dw={errs[2]:.2e} kept={plan.kept}/{plan.total}")
+    assert all(np.isfinite(a).all() for a in (y, dx, dw))
+    assert max(errs) <= TOL, errs
+
+
+def test_stored_spectra_match_oracle(torch):
+    """Unit level: X, W and DY left in the workspace vs the oracle's kept spectra."""
+    for cfg, li, c in ((1, 0, 0.5), (3, 0, 0.25), (2, 1, 0.5), (5, 0, 0.75), (3, 3, 0.0)):
+        layer = synth.CONFIGS[cfg].layers[li]
+        say(f"[spectra] config {cfg} layer {layer.name} c={c}")
+        x, w, dy = synth.layer_inputs(cfg, li)
+        _, _, _, plan, ws = gpu_passes(torch, layer, c, x, w, dy)
+        if layer.ndim == 2:
+            Lh, Lw = plan.fft
+            X = bo.kept_spectrum_2d(x, (layer.pad[0], layer.pad[2]), Lh, Lw, c)
+            DY = bo.kept_spectrum_2d(dy, (0, 0), Lh, Lw, c)
+            Wf = bo.kept_filter_spectrum_2d(w, Lh, Lw, c)
+        else:
+            L = plan.fft[0]
+            X = bo.kept_spectrum_1d(x, layer.pad[0], L, c)
+            DY = bo.kept_spectrum_1d(dy, 0, L, c)
+            Wf = bo.kept_filter_spectrum_1d(w, L, c)
+        gX = plan.spectrum(ws, "X").cpu().numpy().reshape(X.shape)
+        gW = plan.spectrum(ws, "W").cpu().numpy().reshape(Wf.shape)
+        gDY = plan.spectrum(ws, "DY").cpu().numpy().reshape(DY.shape)
+        assert rel(gX, X) <= SPEC_TOL and rel(gW, Wf) <= SPEC_TOL and rel(gDY, DY) <= SPEC_TOL
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_random_small_layers(torch, ndim):
+    """Odd and even sizes, asymmetric padding, larger grids, ragged tiles."""
+    rng = np.random.default_rng(40 + ndim)
+    for i in range(24):
+        layer = synth.random_layer(rng, ndim, max_hw=20, max_c=70, max_n=5, max_k=8 if ndim == 1 else 6)
+        if ndim == 2 and layer.K > 8:
+            continue
+        c = float(rng.choice([0.0, 0.1, 0.5, 0.9]))
+        fft = None
+        if rng.random() < 0.3:
+            if ndim == 1:
+                fft = layer.H + layer.pad[0] + layer.pad[1] + int(rng.integers(0, 5))
+            else:
+                fft = (layer.H + layer.pad[0] + layer.pad[1] + int(rng.integers(0, 4)),
+                       layer.W + layer.pad[2] + layer.pad[3] + int(rng.integers(0, 4)))
+        say(f"[random] ndim={ndim} #{i} {layer} c={c} fft={fft}")
+        x, w, dy = synth.random_inputs(layer, 500 + i)
+        y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
+        ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
+        assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL
+
+
+def test_reuse_flags_give_identical_results(torch):
+    for cfg, li, c in ((1, 0, 0.5), (2, 0, 0.25), (4, 1, 0.75)):
+        layer = synth.CONFIGS[cfg].layers[li]
+        say(f"[reuse] config {cfg} layer {layer.name} c={c}")
+        x, w, dy = synth.layer_inputs(cfg, li)
+        a = gpu_passes(torch, layer, c, x, w, dy, reuse=True)
+        b = gpu_passes(torch, layer, c, x, w, dy, reuse=False)
+        for u, v in zip(a[:3], b[:3]):
+            assert np.array_equal(u, v)
+
+
+def test_adjoint_identity_fp32(torch):
+    """<dy, y> = <dx, x> = <dw, w> on the GPU path: the three passes are adjoint."""
+    for cfg, li, c in ((1, 0, 0.5), (3, 1, 0.25), (2, 2, 0.75), (5, 0, 0.5)):
+        layer = synth.CONFIGS[cfg].layers[li]
+        say(f"[adjoint] config {cfg} layer {layer.name} c={c}")
+        x, w, dy = synth.layer_inputs(cfg, li)
+        y, dx, dw, _, _ = gpu_passes(torch, layer, c, x, w, dy)
+        a = float((dy.astype(np.float64) * y).sum())
+        b = float((dx.astype(np.float64) * x).sum())
+        d = float((dw.astype(np.float64) * w).sum())
+        scale = float(np.abs(dy).astype(np.float64).ravel() @ np.abs(y).astype(np.float64).ravel())
+        assert abs(a - b) <= 1e-5 * scale and abs(a - d) <= 1e-5 * scale
+
+
+def test_edge_cases(torch):
+    """Degenerate shapes: 1x1 maps, K = 1, a filter as large as the padded input,
+    a single channel and sample, the highest rate (DC only)."""
+    cases = [
+        synth.Layer("one_pixel", 2, 1, 1, 1, 1, 1, 1, (0, 0, 0, 0), "blur"),
+        synth.Layer("k_eq_input", 2, 2, 3, 2, 5, 5, 5, (0, 0, 0, 0), "blur"),
+        synth.Layer("k1", 2, 3, 5, 7, 6, 9, 1, (0, 0, 0, 0), "blur"),
+        synth.Layer("pad_only", 2, 1, 2, 2, 1, 1, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("len1", 1, 2, 2, 2, 1, 1, 1, (0, 0), "walk"),
+        synth.Layer("k8_1d", 1, 3, 2, 3, 8, 1, 8, (0, 0), "walk"),
+        synth.Layer("wide", 2, 1, 1, 1, 2, 40, 3, (1, 1, 1, 1), "blur"),
+    ]
+    for layer in cases:
+        for c in (0.0, 0.5, 0.999):
+            say(f"[edge] {layer.name} c={c}")
+            x, w, dy = synth.random_inputs(layer, 11)
+            y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
+            ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+            assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL, (layer.name, c)

@@ -1,0 +1,153 @@
+"""Host plan of the C-ABI library against the oracle (CPU only, no GPU calls).
+
+The library's kept mask must equal the oracle's byte for byte; its counts,
+radii and c_eff must agree; its bin order must be the documented one; and
+invalid descriptors must be rejected with the documented status codes.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import bl_oracle as bo
+from paper_1911_09287_amd import blconv, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(blconv.LIB_PATH), reason="libblconv.so not built")
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "blconv.h")).read()
+    declared = set(re.findall(r"\b(bl_[a-z_]+)\s*\(", header))
+    lib = blconv.load()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert declared == set(blconv.EXPORTED)
+
+
+def _grid(layer):
+    if layer.ndim == 1:
+        return layer.H + layer.pad[0] + layer.pad[1]
+    return (layer.H + layer.pad[0] + layer.pad[1], layer.W + layer.pad[2] + layer.pad[3])
+
+
+@pytest.mark.parametrize("cfg", sorted(synth.CONFIGS))
+def test_config_masks_match_oracle(cfg):
+    for layer in synth.CONFIGS[cfg].layers:
+        for c in (0.0, 0.25, 0.5, 0.75) + synth.CONFIGS[cfg].rates:
+            plan = blconv.plan_for_layer(layer, c)
+            L = _grid(layer)
+            assert (plan.mask() == bo.mask(layer.ndim, L, c)).all()
+            r_h, r_w, kept, total, ceff = bo.plan_info(layer.ndim, L, c)
+            assert (plan.r_h, plan.r_w, plan.kept, plan.total) == (r_h, r_w, kept, total)
+            assert plan.c_eff == ceff
+            assert plan.c_eff >= c - 1e-15 or plan.kept == 1
+
+
+def test_random_grids_and_rates_match_oracle():
+    rng = np.random.default_rng(7)
+    for _ in range(300):
+        if rng.random() < 0.5:
+            L = int(rng.integers(1, 1100))
+            c = float(rng.random())
+            layer = synth.Layer("r", 1, 1, 1, 1, L, 1, 1, (0, 0), "walk")
+            plan = blconv.plan_for_layer(layer, c)
+            assert (plan.mask() == bo.mask(1, L, c)).all()
+        else:
+            Lh, Lw = int(rng.integers(1, 70)), int(rng.integers(1, 70))
+            c = float(rng.choice([rng.random(), 0.25, 0.5, 0.75, 0.0]))
+            layer = synth.Layer("r", 2, 1, 1, 1, Lh, Lw, 1, (0, 0, 0, 0), "blur")
+            plan = blconv.plan_for_layer(layer, c)
+            assert (plan.mask() == bo.mask(2, (Lh, Lw), c)).all(), (Lh, Lw, c)
+
+
+def test_grid_override_worked_example():
+    # 3x32x32 input, 5x5 filter, grid 59 (the map-reuse size): one layer -> 57 x 29
+    plan = blconv.Plan(2, 1, 3, 1, (32, 32), 5, (0, 0, 0, 0), 0.066, fft=(59, 59))
+    assert plan.fft == (59, 59) and plan.total == 59 * 30
+    assert plan.kept == 57 * 29
+    assert round(100 * plan.c_eff, 2) == 6.61
+
+
+def test_bins_order_is_documented_order():
+    for (Lh, Lw, c) in ((34, 34, 0.5), (9, 7, 0.3), (6, 6, 0.75), (1, 519, 0.25)):
+        if Lh == 1:
+            layer = synth.Layer("r", 1, 1, 1, 1, Lw, 1, 1, (0, 0), "walk")
+            m = bo.mask(1, Lw, c)
+            expect = [(0, v) for v in range(m.size) if m[v]]
+        else:
+            layer = synth.Layer("r", 2, 1, 1, 1, Lh, Lw, 1, (0, 0, 0, 0), "blur")
+            expect = bo.kept_bins_2d(bo.mask(2, (Lh, Lw), c))
+        u, v = blconv.plan_for_layer(layer, c).bins()
+        assert list(zip(u.tolist(), v.tolist())) == expect
+
+
+def test_workspace_layout_is_disjoint_and_large_enough():
+    for cfg in sorted(synth.CONFIGS):
+        for layer in synth.CONFIGS[cfg].layers:
+            p = blconv.plan_for_layer(layer, 0.0)
+            sizes = {"X": p.kept * p.N * p.C_in * 8, "W": p.kept * p.C_in * p.C_out * 8,
+                     "DY": p.kept * p.N * p.C_out * 8}
+            spans = sorted((p.offsets[k], p.offsets[k] + sizes[k]) for k in sizes)
+            for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+                assert a1 <= b0
+            assert spans[-1][1] <= p.workspace_bytes
+            assert all(o % 256 == 0 for o in p.offsets.values())
+
+
+def _create(**kw):
+    lib = blconv.load()
+    d = blconv.Desc()
+    base = dict(ndim=2, N=1, C_in=1, C_out=1, H=8, W=8, K=3, c=0.0)
+    base.update({k: v for k, v in kw.items() if k not in ("pad_lo", "pad_hi")})
+    for k, v in base.items():
+        setattr(d, k, v)
+    for k in ("pad_lo", "pad_hi"):
+        if k in kw:
+            getattr(d, k)[0], getattr(d, k)[1] = kw[k]
+    h = ctypes.c_void_p()
+    code = lib.bl_conv_plan_create(ctypes.byref(h), ctypes.byref(d))
+    if code == 0:
+        lib.bl_conv_plan_destroy(h)
+    return code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(ndim=3), 1), (dict(N=0), 1), (dict(C_in=-1), 1), (dict(C_out=0), 1), (dict(H=0), 1),
+    (dict(W=0), 1), (dict(K=0), 1), (dict(K=9), 2), (dict(K=9, H=20, W=20), 2),
+    (dict(c=1.0), 1), (dict(c=-0.1), 1), (dict(c=float("nan")), 1), (dict(c=0.999), 0),
+    (dict(pad_lo=(-1, 0)), 1), (dict(fft_h=9, fft_w=8), 0), (dict(fft_h=9, fft_w=7), 1), (dict(fft_h=7), 1), (dict(fft_h=12, fft_w=10), 0),
+    (dict(flags=1), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
+    (dict(ndim=1, W=1, H=10), 0), (dict(ndim=1, W=2, H=10), 1), (dict(ndim=1, W=1, H=10, pad_lo=(0, 1)), 1),
+    (dict(ndim=1, W=1, H=10, fft_w=4), 1), (dict(ndim=1, W=1, H=10, fft_h=9), 1),
+])
+def test_plan_create_validation(kw, code):
+    assert _create(**kw) == code
+
+
+def test_null_arguments_are_rejected_without_gpu():
+    lib = blconv.load()
+    assert lib.bl_conv_plan_create(None, None) == 1
+    assert lib.bl_conv_plan_destroy(None) == 1
+    assert lib.bl_conv_plan_info(None, None, None, None, None, None, None, None) == 1
+    assert lib.bl_conv_workspace_size(None, None) == 1
+    # compute calls validate on the host before touching the GPU
+    assert lib.bl_conv_forward(None, None, None, None, None, 0, None) == 1
+    assert lib.bl_conv_backward_input(None, None, None, None, None, 0, None) == 1
+    assert lib.bl_conv_backward_weight(None, None, None, None, None, 0, None) == 1
+    p = blconv.Plan(2, 1, 1, 1, (8, 8), 3, (1, 1, 1, 1), 0.5)
+    h = p._h
+    assert lib.bl_conv_forward(h, None, None, None, None, 0, None) == 1
+    # bad flags
+    assert lib.bl_conv_forward(h, 8, 8, 8, 8, 0x4, None) == 1
+    assert lib.bl_conv_backward_input(h, 8, 8, 8, 8, 0x1, None) == 1
+    assert lib.bl_conv_backward_weight(h, 8, 8, 8, 8, 0x2, None) == 1
+    # wrong sizes for host copies
+    m = np.zeros(p.total + 1, np.uint8)
+    assert lib.bl_conv_plan_get_mask(h, m.ctypes.data, m.size) == 1
+    assert lib.bl_status_string(3) == b"workspace too small"
