@@ -1,0 +1,174 @@
+// C ABI compute entry points, stage dispatch and per-kernel timing.
+#include <mutex>
+#include <vector>
+
+#include "common.hpp"
+
+namespace blc {
+
+// ---------------------------------------------------------------------------
+// Per-kernel timing
+// ---------------------------------------------------------------------------
+namespace {
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  int cap = 0, used = 0;
+  std::vector<hipEvent_t> ev;
+  std::vector<const char*> names;
+  std::vector<double> bytes, flops;
+} g_prof;
+}  // namespace
+
+int prof_slot(const char* name, double bytes, double flops) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.used >= g_prof.cap) return -1;
+  g_prof.names[g_prof.used] = name;
+  g_prof.bytes[g_prof.used] = bytes;
+  g_prof.flops[g_prof.used] = flops;
+  return g_prof.used++;
+}
+
+hipEvent_t prof_event(int slot, int end) { return g_prof.ev[2 * slot + end]; }
+
+// ---------------------------------------------------------------------------
+// Stage dispatch: the fast transform for the shape when there is one, else
+// the direct pruned DFT.
+// ---------------------------------------------------------------------------
+bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+                            int oj, hipStream_t s) {
+  if (p->Lh == 1) {
+    bl_status_t st = launch_bluestein_fwd(p, in, out, P, Win, oj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
+  return launch_spec_fwd_direct(p, in, out, P, Hin, Win, oi, oj, s);
+}
+
+bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                            int cj, hipStream_t s) {
+  if (p->Lh == 1) {
+    bl_status_t st = launch_bluestein_inv(p, in, out, P, OW, cj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
+  return launch_spec_inv_direct(p, in, out, P, OH, OW, ci, cj, s);
+}
+
+namespace {
+inline float2* ws_at(void* ws, size_t off) { return reinterpret_cast<float2*>(static_cast<char*>(ws) + off); }
+
+#define BL_TRY(expr)                    \
+  do {                                  \
+    bl_status_t st_ = (expr);           \
+    if (st_ != BL_OK) return st_;       \
+  } while (0)
+
+
+}  // namespace
+}  // namespace blc
+
+using namespace blc;
+
+// ---------------------------------------------------------------------------
+// C ABI compute entry points
+// ---------------------------------------------------------------------------
+extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const float* w, float* y, void* ws,
+                                       unsigned flags, void* stream) {
+  if (!p || !y || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~(BL_REUSE_X | BL_REUSE_W)) return BL_ERR_INVALID_ARG;
+  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_W) && !w)) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* X = ws_at(ws, p->off_X);
+  float2* Wf = ws_at(ws, p->off_W);
+  float2* T = ws_at(ws, p->off_T);
+  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  if (!(flags & BL_REUSE_X))
+    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, s));
+  return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
+}
+
+extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy, const float* w, float* dx,
+                                              void* ws, unsigned flags, void* stream) {
+  if (!p || !dy || !dx || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~BL_REUSE_W) return BL_ERR_INVALID_ARG;
+  if (!(flags & BL_REUSE_W) && !w) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* Wf = ws_at(ws, p->off_W);
+  float2* DY = ws_at(ws, p->off_DY);
+  float2* T = ws_at(ws, p->off_T);
+  BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
+  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, s));
+  return launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s);
+}
+
+extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x, const float* dy, float* dw,
+                                               void* ws, unsigned flags, void* stream) {
+  if (!p || !dw || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~(BL_REUSE_X | BL_REUSE_DY)) return BL_ERR_INVALID_ARG;
+  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_DY) && !dy)) return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float2* X = ws_at(ws, p->off_X);
+  float2* DY = ws_at(ws, p->off_DY);
+  float2* DW = ws_at(ws, p->off_DW);
+  if (!(flags & BL_REUSE_X))
+    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  if (!(flags & BL_REUSE_DY))
+    BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
+  BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, s));
+  return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
+}
+
+// ---------------------------------------------------------------------------
+// Profiling entry points
+// ---------------------------------------------------------------------------
+extern "C" bl_status_t bl_profile_begin(int capacity) {
+  if (capacity <= 0) return BL_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if ((int)g_prof.ev.size() < 2 * capacity) {
+    for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+    g_prof.ev.assign(2 * capacity, nullptr);
+    for (auto& e : g_prof.ev)
+      if (hipEventCreate(&e) != hipSuccess) return BL_ERR_HIP;
+  }
+  g_prof.names.assign(capacity, nullptr);
+  g_prof.bytes.assign(capacity, 0.0);
+  g_prof.flops.assign(capacity, 0.0);
+  g_prof.cap = capacity;
+  g_prof.used = 0;
+  g_prof.on = true;
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_profile_end(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  return BL_OK;
+}
+
+extern "C" int bl_profile_count(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  return g_prof.used;
+}
+
+extern "C" bl_status_t bl_profile_get(int i, const char** kernel, float* ms, double* bytes, double* flops) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (i < 0 || i >= g_prof.used) return BL_ERR_INVALID_ARG;
+  if (kernel) *kernel = g_prof.names[i];
+  if (bytes) *bytes = g_prof.bytes[i];
+  if (flops) *flops = g_prof.flops[i];
+  if (ms) {
+    if (hipEventElapsedTime(ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]) != hipSuccess) return BL_ERR_HIP;
+  }
+  return BL_OK;
+}
+
+extern "C" bl_status_t bl_profile_release(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.names.clear();
+  g_prof.cap = g_prof.used = 0;
+  g_prof.on = false;
+  return BL_OK;
+}

@@ -1,0 +1,476 @@
+// 1-D kept spectra by Bluestein's chirp-z identity (gfx950).
+//
+// A length-L DFT evaluated only at n_out consecutive outputs from n_in
+// consecutive inputs is a linear convolution with a chirp: with
+// c[m] = exp(-i pi m^2 / L) and nk = (n^2 + k^2 - (k - n)^2) / 2,
+//   sum_n a[n] exp(-2 pi i n k / L) = c[k] sum_n (a[n] c[n]) conj(c[k - n]).
+// The convolution is done as a circular one over a power-of-two FFT of size
+// M >= n_in + n_out - 1, so no wrap-around reaches the kept outputs.  This
+// serves any sequence length (the FCN layers of the time-series experiments
+// use 519 = 3 * 173, 516 and 514 = 2 * 257 points, where a mixed-radix FFT
+// would need 173- and 257-point stages).
+//
+// Forward (real rows -> kept bins, Sec. 3.2.2: only v <= r_w is produced):
+//   pre[j] = c[j + oj], filter[d] = conj(c[d - oj]), X[v] = c[v] * conv[v].
+// Inverse (kept bins -> real rows, Hermitian weights h_v, crop offset cj):
+//   pre[v] = h_v conj(c[v]), filter[d] = c[d + cj],
+//   y[j] = Re(conj(c[j + cj]) * conv[j]) / L.
+// Series are taken in groups of 16 consecutive ones (so each 128-byte line of
+// the bin-major spectrum is written by one block); each wave runs its
+// series' two M-point FFTs as radix-16/8/4 Stockham passes through its own
+// LDS buffer, the first pass reading HBM directly and the last one writing
+// HBM directly.  Blocks are persistent; the chirp filter's spectrum is
+// computed once per block by all its threads.
+#include <algorithm>
+#include <cmath>
+
+#include "common.hpp"
+
+namespace blc {
+namespace {
+
+// e^{-2 pi i k / 32}, k < 16.
+constexpr float kW32c[16] = {1.0f, 0.98078528040323043f, 0.92387953251128674f, 0.83146961230254524f,
+                             0.70710678118654757f, 0.55557023301960218f, 0.38268343236508984f, 0.19509032201612833f,
+                             0.0f, -0.19509032201612819f, -0.38268343236508973f, -0.55557023301960196f,
+                             -0.70710678118654746f, -0.83146961230254535f, -0.92387953251128674f,
+                             -0.98078528040323043f};
+constexpr float kW32s[16] = {0.0f, -0.19509032201612825f, -0.38268343236508978f, -0.55557023301960218f,
+                             -0.70710678118654746f, -0.83146961230254524f, -0.92387953251128674f,
+                             -0.98078528040323043f, -1.0f, -0.98078528040323043f, -0.92387953251128674f,
+                             -0.83146961230254546f, -0.70710678118654757f, -0.55557023301960218f,
+                             -0.38268343236508989f, -0.19509032201612861f};
+
+// a * e^{-2 pi i k / R} for a compile-time k (after unrolling), R <= 32.
+template <int R>
+__device__ __forceinline__ float2 rot(float2 a, int k) {
+  if (k == 0) return a;
+  if (4 * k == R) return make_float2(a.y, -a.x);
+  const float c = kW32c[k * (32 / R)], s = kW32s[k * (32 / R)];
+  return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.x, s, a.y * c));
+}
+
+// In-register R-point DFT (natural order in and out), radix-2 decimation in time.
+template <int R>
+struct RegFft {
+  static __device__ __forceinline__ void run(float2* v) {
+    float2 e[R / 2], o[R / 2];
+#pragma unroll
+    for (int k = 0; k < R / 2; ++k) {
+      e[k] = v[2 * k];
+      o[k] = v[2 * k + 1];
+    }
+    RegFft<R / 2>::run(e);
+    RegFft<R / 2>::run(o);
+#pragma unroll
+    for (int k = 0; k < R / 2; ++k) {
+      const float2 t = rot<R>(o[k], k);
+      v[k] = cadd(e[k], t);
+      v[k + R / 2] = csub(e[k], t);
+    }
+  }
+};
+template <>
+struct RegFft<1> {
+  static __device__ __forceinline__ void run(float2*) {}
+};
+
+// LDS index with one pad slot per 16 elements (spreads strided accesses over banks).
+__device__ __forceinline__ int pidx(int n) { return n + (n >> 4); }
+template <int M>
+constexpr int padded() { return M + M / 16; }
+
+// Orders the LDS accesses of one wave: everything a wave wrote before this
+// point is seen by its later reads (LDS executes a wave's accesses in order;
+// the fences keep the compiler from moving accesses across).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One Stockham autosort pass of radix R over M points, done by one wave (lane
+// = 0..63) or by a whole block (NT threads; then it synchronises the block).
+// load(i) returns element i of the input sequence and store(i, v) takes
+// element i of the output sequence, so the first pass can read HBM and the
+// last pass can write anywhere; in between the data stay in LDS.
+// Twiddles: with `tw` set, tw[k * (R - 1) + r - 1] = w_{Ns R}^{r k} (a per-pass
+// table whose rows are read with an odd stride, free of bank conflicts);
+// otherwise roots[r k M / (Ns R)] of the M-point root table.
+template <int M, int R, int NT, class LoadF, class StoreF>
+__device__ __forceinline__ void stockham_pass(int Ns, int t, const float2* roots, const float2* tw, LoadF&& load,
+                                              StoreF&& store) {
+  constexpr int NB = M / R;
+  constexpr int PER = NB >= NT ? NB / NT : 1;
+  const bool active = NB >= NT || t < NB;
+  float2 v[PER][R];
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int j = t + q * NT;
+#pragma unroll
+      for (int r = 0; r < R; ++r) v[q][r] = load(j + r * NB);
+    }
+  }
+  if constexpr (NT == 64) wave_sync(); else __syncthreads();
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int j = t + q * NT;
+      const int k = j & (Ns - 1);
+      if (Ns > 1) {
+        if (tw) {
+#pragma unroll
+          for (int r = 1; r < R; ++r) v[q][r] = cmul(v[q][r], tw[k * (R - 1) + r - 1]);
+        } else {
+          const int step = M / (Ns * R);
+#pragma unroll
+          for (int r = 1; r < R; ++r) v[q][r] = cmul(v[q][r], roots[r * k * step]);
+        }
+      }
+      RegFft<R>::run(v[q]);
+      const int base = (j - k) * R + k;
+#pragma unroll
+      for (int r = 0; r < R; ++r) store(base + r * Ns, v[q][r]);
+    }
+  }
+  if constexpr (NT == 64) wave_sync(); else __syncthreads();
+}
+
+// Radix sequence of the per-wave FFTs: M = 1024: 16, 16, 4; 512: 8, 8, 8;
+// 256: 4, 4, 4, 4.  Pass p has span Ns_p = product of the earlier radices.
+template <int M>
+struct WavePlan;
+template <>
+struct WavePlan<1024> {
+  static constexpr int n = 3;
+  static constexpr int R[3] = {16, 16, 4};
+};
+template <>
+struct WavePlan<512> {
+  static constexpr int n = 3;
+  static constexpr int R[3] = {8, 8, 8};
+};
+template <>
+struct WavePlan<256> {
+  static constexpr int n = 4;
+  static constexpr int R[4] = {4, 4, 4, 4};
+};
+
+// Offset of pass p's twiddle table inside the packed per-pass tables (passes
+// with Ns > 1 only; sum of Ns (R - 1) over them is M - R_0 < M).
+template <int M>
+constexpr int tw_offset(int p) {
+  int off = 0, Ns = 1;
+  for (int i = 0; i < p; ++i) {
+    if (Ns > 1) off += Ns * (WavePlan<M>::R[i] - 1);
+    Ns *= WavePlan<M>::R[i];
+  }
+  return off;
+}
+template <int M>
+constexpr int span(int p) {
+  int Ns = 1;
+  for (int i = 0; i < p; ++i) Ns *= WavePlan<M>::R[i];
+  return Ns;
+}
+
+// Build the packed per-pass twiddle tables of the wave FFT into `tw`.
+template <int M>
+__device__ __forceinline__ void build_pass_twiddles(float2* tw, const float2* roots, int t, int nt) {
+#pragma unroll
+  for (int p = 1; p < WavePlan<M>::n; ++p) {
+    const int R = WavePlan<M>::R[p], Ns = span<M>(p), off = tw_offset<M>(p);
+    for (int e = t; e < Ns * (R - 1); e += nt) {
+      const int k = e / (R - 1), r = e % (R - 1) + 1;
+      tw[off + e] = roots[r * k * (M / (Ns * R))];
+    }
+  }
+}
+
+// Forward M-point FFT by one wave: the first pass reads through load0, the
+// last pass writes through storeN, the passes in between use `buf` (padded).
+template <int M, class L0, class SN>
+__device__ __forceinline__ void wave_fft(float2* buf, int lane, const float2* tw, L0&& load0, SN&& storeN) {
+  auto lb = [buf](int i) { return buf[pidx(i)]; };
+  auto sb = [buf](int i, float2 v) { buf[pidx(i)] = v; };
+  using WP = WavePlan<M>;
+  if constexpr (WP::n == 3) {
+    stockham_pass<M, WP::R[0], 64>(1, lane, nullptr, nullptr, load0, sb);
+    stockham_pass<M, WP::R[1], 64>(span<M>(1), lane, nullptr, tw + tw_offset<M>(1), lb, sb);
+    stockham_pass<M, WP::R[2], 64>(span<M>(2), lane, nullptr, tw + tw_offset<M>(2), lb, storeN);
+  } else {
+    stockham_pass<M, WP::R[0], 64>(1, lane, nullptr, nullptr, load0, sb);
+    stockham_pass<M, WP::R[1], 64>(span<M>(1), lane, nullptr, tw + tw_offset<M>(1), lb, sb);
+    stockham_pass<M, WP::R[2], 64>(span<M>(2), lane, nullptr, tw + tw_offset<M>(2), lb, sb);
+    stockham_pass<M, WP::R[3], 64>(span<M>(3), lane, nullptr, tw + tw_offset<M>(3), lb, storeN);
+  }
+}
+
+// Forward M-point FFT in place in `buf` by the whole block (NT threads).
+template <int M, int NT>
+__device__ __forceinline__ void block_fft(float2* buf, int t, const float2* roots) {
+  auto lb = [buf](int i) { return buf[pidx(i)]; };
+  auto sb = [buf](int i, float2 v) { buf[pidx(i)] = v; };
+  int Ns = 1;
+  for (; Ns * 4 <= M; Ns *= 4) stockham_pass<M, 4, NT>(Ns, t, roots, nullptr, lb, sb);
+  if (Ns < M) stockham_pass<M, 2, NT>(Ns, t, roots, nullptr, lb, sb);
+}
+
+struct BlueArgs {
+  int n_in, n_out;     // inputs and outputs of the chirp convolution per FFT
+  int L;               // DFT length
+  int V;               // kept bins per series
+  int off_in, off_out; // DFT index of input 0 and of output 0
+  int nyq;             // Nyquist bin (L even) or -1
+  long P;              // number of series
+  float out_scale;     // extra output scale (inverse: 1 / L)
+  float2 root_hi[16], root_lo[64];    // e^{-2 pi i k / M} = hi[k >> 6] * lo[k & 63]
+  float2 chirp_hi[64], chirp_lo[64];  // e^{-i pi q / L} = hi[q >> 6] * lo[q & 63], q < 2L
+};
+
+constexpr int kSeriesPerGroup = 16;
+constexpr int kWaves = 4;
+
+// c[m] = e^{-i pi m^2 / L} (m^2 reduced mod 2L exactly), conjugated for the inverse.
+template <bool INV>
+__device__ __forceinline__ float2 chirp(const BlueArgs& a, int m) {
+  const unsigned mm = (unsigned)(m < 0 ? -m : m);
+  const int q = (int)((mm * mm) % (2u * (unsigned)a.L));
+  const float2 c = cmul(a.chirp_hi[q >> 6], a.chirp_lo[q & 63]);
+  return INV ? cconj(c) : c;
+}
+
+// Modes: bit 0 = inverse (bins -> real rows), bit 1 = two series per FFT.
+//   forward, single:  inputs x[0..Win), outputs X[0..V)
+//   inverse, single:  inputs h_v Y[v], v < V; outputs y[0..OW)
+//   forward, paired:  input x1 + i x2; outputs Z[k], k = -(V-1)..V-1, then
+//                     X1 = (Z[k] + conj Z[-k]) / 2, X2 = (Z[k] - conj Z[-k]) / 2i
+//                     (both spectra of real rows are conjugate-symmetric)
+//   inverse, paired:  input the conjugate-symmetric extensions of Y1 and Y2
+//                     over k = -(V-1)..V-1 as Y1 + i Y2 (real DC parts); the
+//                     real and imaginary parts of the result are y1 and y2.
+template <int M, int MODE>
+__global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restrict__ in_, void* __restrict__ out_,
+                                                           BlueArgs a) {
+  constexpr bool INV = MODE & 1, PACK = MODE >= 2;
+  extern __shared__ float2 sm[];
+  constexpr int PM = padded<M>();
+  float2* tw = sm;                // M: packed per-pass twiddle tables
+  float2* F = tw + M;             // PM: spectrum of the chirp filter
+  float2* pre = F + PM;           // n_in
+  float2* post = pre + a.n_in;    // n_out
+  float2* bufs = post + a.n_out;  // kWaves x PM: per-wave FFT buffers
+  float2* roots = bufs;           // M: e^{-2 pi i k / M}, only while the tables are built
+  const int tid = threadIdx.x;
+
+  for (int k = tid; k < M; k += blockDim.x) roots[k] = cmul(a.root_hi[k >> 6], a.root_lo[k & 63]);
+  for (int k = tid; k < a.n_in; k += blockDim.x) {
+    float2 c = chirp<INV>(a, k + a.off_in);
+    if (INV && !PACK && k != 0 && k != a.nyq) c = cscale(c, 2.f);
+    pre[k] = c;
+  }
+  const float osc = a.out_scale / (float)M * (PACK && !INV ? 0.5f : 1.0f);
+  for (int k = tid; k < a.n_out; k += blockDim.x) post[k] = cscale(chirp<INV>(a, k + a.off_out), osc);
+  for (int m = tid; m < M; m += blockDim.x) {
+    const int d = m < a.n_out ? m : m - M;
+    float2 h = make_float2(0.f, 0.f);
+    if (d >= -(a.n_in - 1)) h = cconj(chirp<INV>(a, d + a.off_out - a.off_in));
+    F[pidx(m)] = h;
+  }
+  __syncthreads();
+  build_pass_twiddles<M>(tw, roots, tid, blockDim.x);
+  block_fft<M, 64 * kWaves>(F, tid, roots);  // ends with a block barrier: roots are free again
+
+  const int wave = tid >> 6, lane = tid & 63;
+  float2* buf = bufs + wave * PM;
+  const float* xin = static_cast<const float*>(in_);
+  const float2* yin = static_cast<const float2*>(in_);
+  const long P = a.P;
+  const long groups = (P + kSeriesPerGroup - 1) / kSeriesPerGroup;
+  constexpr int SPF = PACK ? 2 : 1;  // series per FFT
+  for (long g = blockIdx.x; g < groups; g += gridDim.x) {
+    for (int sl = wave * SPF; sl < kSeriesPerGroup; sl += kWaves * SPF) {
+      const long s1 = g * kSeriesPerGroup + sl;
+      if (s1 >= P) break;
+      const long s2 = s1 + 1;
+      const bool two = PACK && s2 < P;
+      // FFT of the pre-chirped input, straight from HBM; the last pass
+      // multiplies by the filter spectrum and conjugates (inverse via conj).
+      auto load_in = [&](int n) {
+        float2 v = make_float2(0.f, 0.f);
+        if (n < a.n_in) {
+          if constexpr (MODE == 0) {
+            v = make_float2(xin[(size_t)s1 * a.n_in + n], 0.f);
+          } else if constexpr (MODE == 1) {
+            v = yin[(size_t)n * P + s1];
+          } else if constexpr (MODE == 2) {
+            v = make_float2(xin[(size_t)s1 * a.n_in + n], two ? xin[(size_t)s2 * a.n_in + n] : 0.f);
+          } else {
+            const int k = n - (a.V - 1);
+            const int kk = k < 0 ? -k : k;
+            const float2 y1 = yin[(size_t)kk * P + s1];
+            const float2 y2 = two ? yin[(size_t)kk * P + s2] : make_float2(0.f, 0.f);
+            if (k > 0) v = make_float2(y1.x - y2.y, y1.y + y2.x);
+            else if (k < 0) v = make_float2(y1.x + y2.y, y2.x - y1.y);
+            else v = make_float2(y1.x, y2.x);
+          }
+          v = cmul(v, pre[n]);
+        }
+        return v;
+      };
+      auto store_prod = [&](int i, float2 v) { buf[pidx(i)] = cconj(cmul(v, F[pidx(i)])); };
+      wave_fft<M>(buf, lane, tw, load_in, store_prod);
+      // second FFT; its last pass writes the outputs with the post chirp
+      auto load_buf = [&](int i) { return buf[pidx(i)]; };
+      auto store_out = [&](int i, float2 v) {
+        if (i < a.n_out) {
+          const float2 r = cmul(post[i], cconj(v));
+          if constexpr (MODE == 0) {
+            static_cast<float2*>(out_)[(size_t)i * P + s1] = r;
+          } else if constexpr (MODE == 1) {
+            static_cast<float*>(out_)[(size_t)s1 * a.n_out + i] = r.x;
+          } else if constexpr (MODE == 2) {
+            buf[pidx(i)] = r;  // split below
+          } else {
+            static_cast<float*>(out_)[(size_t)s1 * a.n_out + i] = r.x;
+            if (two) static_cast<float*>(out_)[(size_t)s2 * a.n_out + i] = r.y;
+          }
+        }
+      };
+      wave_fft<M>(buf, lane, tw, load_buf, store_out);
+      if constexpr (MODE == 2) {
+        // Z[k] sits at index k + V - 1
+        float2* X = static_cast<float2*>(out_);
+        for (int v = lane; v < a.V; v += 64) {
+          const float2 zp = buf[pidx(a.V - 1 + v)];
+          const float2 zm = cconj(buf[pidx(a.V - 1 - v)]);
+          X[(size_t)v * P + s1] = cadd(zp, zm);
+          if (two) {
+            const float2 d = csub(zp, zm);
+            X[(size_t)v * P + s2] = make_float2(d.y, -d.x);
+          }
+        }
+        wave_sync();
+      }
+    }
+  }
+}
+
+int g_cu_count[64];
+
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (g_cu_count[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    g_cu_count[dev] = n;
+  }
+  return g_cu_count[dev];
+}
+
+template <int M, int MODE>
+bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+  // host-side seeds of the root and chirp tables, in double precision
+  for (int i = 0; i < M / 64; ++i) {
+    const double t = -2.0 * M_PI * 64.0 * i / M;
+    a.root_hi[i] = make_float2((float)std::cos(t), (float)std::sin(t));
+  }
+  for (int i = 0; i < 64; ++i) {
+    const double t = -2.0 * M_PI * i / M;
+    a.root_lo[i] = make_float2((float)std::cos(t), (float)std::sin(t));
+  }
+  for (int i = 0; i * 64 < 2 * a.L; ++i) {
+    const double t = -M_PI * 64.0 * i / a.L;
+    a.chirp_hi[i] = make_float2((float)std::cos(t), (float)std::sin(t));
+  }
+  for (int i = 0; i < 64; ++i) {
+    const double t = -M_PI * i / a.L;
+    a.chirp_lo[i] = make_float2((float)std::cos(t), (float)std::sin(t));
+  }
+  const size_t lds = (size_t)(M + (1 + kWaves) * padded<M>() + a.n_in + a.n_out) * sizeof(float2);
+  if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
+  const long groups = (a.P + kSeriesPerGroup - 1) / kSeriesPerGroup;
+  const long blocks = std::min<long>(groups, 2L * device_cus());
+  return timed_launch(name, bytes, 0.0, s, [&] {
+    hipLaunchKernelGGL((k_bluestein<M, MODE>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, in, out, a);
+  });
+}
+
+int fft_size_for(int need) {
+  int M = 256;
+  while (M < need) M *= 2;
+  return M;
+}
+
+template <int MODE>
+bl_status_t launch_mode(BlueArgs& a, int M, const void* in, void* out, const char* name, double bytes,
+                        hipStream_t s) {
+  if (M == 256) return launch_m<256, MODE>(a, in, out, name, bytes, s);
+  if (M == 512) return launch_m<512, MODE>(a, in, out, name, bytes, s);
+  if (M == 1024) return launch_m<1024, MODE>(a, in, out, name, bytes, s);
+  return BL_ERR_UNSUPPORTED;
+}
+
+// Chooses between one series per FFT and two (when the conjugate-symmetric
+// output or input range fits the same FFT size).
+bl_status_t launch_any(BlueArgs& a, bool inv, int other, const void* in, void* out, const char* name,
+                       double bytes, hipStream_t s) {
+  if (2 * a.L > 64 * 64) return BL_ERR_UNSUPPORTED;
+  if ((long)a.V * other < 2048) return BL_ERR_UNSUPPORTED;  // the direct DFT is as cheap
+  const int M1 = fft_size_for(a.V + other - 1);
+  const int M2 = fft_size_for(2 * a.V - 1 + other - 1);
+  const bool pack = a.P >= 2 && 2 * (a.V - 1) < a.L && M2 <= M1 && M2 <= 1024;
+  if (!pack && M1 > 1024) return BL_ERR_UNSUPPORTED;
+  if (!inv) {
+    a.n_in = other;
+    if (pack) {
+      a.n_out = 2 * a.V - 1;
+      a.off_out = -(a.V - 1);
+      return launch_mode<2>(a, M2, in, out, name, bytes, s);
+    }
+    a.n_out = a.V;
+    a.off_out = 0;
+    return launch_mode<0>(a, M1, in, out, name, bytes, s);
+  }
+  a.n_out = other;
+  if (pack) {
+    a.n_in = 2 * a.V - 1;
+    a.off_in = -(a.V - 1);
+    return launch_mode<3>(a, M2, in, out, name, bytes, s);
+  }
+  a.n_in = a.V;
+  a.off_in = 0;
+  return launch_mode<1>(a, M1, in, out, name, bytes, s);
+}
+
+}  // namespace
+
+bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Win, int oj,
+                                 hipStream_t s) {
+  BlueArgs a{};
+  a.L = p->Lw;
+  a.V = p->V;
+  a.off_in = oj;
+  a.nyq = (p->Lw % 2 == 0) ? p->Lw / 2 : -1;
+  a.P = P;
+  a.out_scale = 1.0f;
+  const double bytes = (double)P * Win * 4 + (double)P * p->V * 8;
+  return launch_any(a, false, Win, in, out, "spec_fwd_1d", bytes, s);
+}
+
+bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
+                                 hipStream_t s) {
+  BlueArgs a{};
+  a.L = p->Lw;
+  a.V = p->V;
+  a.off_out = cj;
+  a.nyq = (p->Lw % 2 == 0) ? p->Lw / 2 : -1;
+  a.P = P;
+  a.out_scale = 1.0f / (float)p->Lw;
+  const double bytes = (double)P * p->V * 8 + (double)P * OW * 4;
+  return launch_any(a, true, OW, in, out, "spec_inv_1d", bytes, s);
+}
+
+}  // namespace blc

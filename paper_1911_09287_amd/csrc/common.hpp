@@ -1,0 +1,74 @@
+// Internal declarations shared by the kernel files and the entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "plan.hpp"
+
+namespace blc {
+
+constexpr int kThreads = 256;
+constexpr size_t kMaxLds = 64 * 1024;
+
+// ---- per-kernel timing (bl_profile_*) -------------------------------------
+// Reserve a timing slot for one launch; -1 when profiling is off or full.
+int prof_slot(const char* name, double bytes, double flops);
+hipEvent_t prof_event(int slot, int end);
+
+// Launch with optional event timing.  `bytes` and `flops` are the launch's
+// algorithmic HBM traffic (compulsory reads + writes) and arithmetic, reported
+// with the timing so that measurement tools can place it on a roofline.
+template <typename Launch>
+bl_status_t timed_launch(const char* name, double bytes, double flops, hipStream_t s, Launch&& launch) {
+  const int slot = prof_slot(name, bytes, flops);
+  if (slot >= 0 && hipEventRecord(prof_event(slot, 0), s) != hipSuccess) return BL_ERR_HIP;
+  launch();
+  if (hipGetLastError() != hipSuccess) return BL_ERR_HIP;
+  if (slot >= 0 && hipEventRecord(prof_event(slot, 1), s) != hipSuccess) return BL_ERR_HIP;
+  return BL_OK;
+}
+
+// ---- device helpers ---------------------------------------------------------
+__device__ inline float2 cmul(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+__device__ inline float2 cconj(float2 a) { return make_float2(a.x, -a.y); }
+__device__ inline float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ inline float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ inline float2 cscale(float2 a, float s) { return make_float2(a.x * s, a.y * s); }
+
+// FFT row index of the r-th kept row.
+__device__ inline int kept_row_d(int r, int r_h, int Lh, int R) { return r <= r_h ? r : r + (Lh - R); }
+
+// ---- stage launchers --------------------------------------------------------
+// Real planes [P][Hin][Win] placed at (oi, oj) of the grid -> kept spectrum
+// out[b * P + p] (bin-major).
+bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win,
+                            int oi, int oj, hipStream_t s);
+// Kept spectrum in[b * P + p] -> real planes [P][OH][OW] holding the grid
+// window that starts at (ci, cj), scaled by 1 / (Lh Lw).
+bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                            int cj, hipStream_t s);
+// Filter w [F][C][Kh][Kw] -> W[b][c][f].
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* out, hipStream_t s);
+// DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats.
+bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s);
+
+enum class Contract { Forward, GradInput, GradWeight };
+bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+                            hipStream_t s);
+
+// Direct (pruned DFT) transforms: any grid; used where no fast path applies.
+bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win,
+                                   int oi, int oj, hipStream_t s);
+bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW,
+                                   int ci, int cj, hipStream_t s);
+
+// 1-D transforms by Bluestein's chirp-z algorithm over a power-of-two FFT.
+// Return BL_ERR_UNSUPPORTED when the shape is outside the fast path.
+bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Win, int oj,
+                                 hipStream_t s);
+bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
+                                 hipStream_t s);
+
+}  // namespace blc

@@ -1,30 +1,24 @@
-// HIP kernels and compute entry points of the band-limited convolution, gfx950.
+// Direct (pruned DFT) transforms, filter spectrum, weight-gradient inverse
+// DFT and the per-bin channel contraction on fp32 MFMA (gfx950).
 //
-// Stages of one pass (bin-major spectra [kept bin][plane] complex64):
-//   spec_fwd   zero-pad + real 2-D DFT + band mask of real planes (x or dy):
-//              a row pass that emits only kept columns v <= r_w, then a column
-//              pass over the nonzero input rows that emits only kept rows.
-//              Discarded coefficients are never formed (Sec. 3.2.2, Fig. 2).
-//   spec_filt  filter spectrum at the kept bins, a K x K-tap DFT per bin.
-//   contract   per kept bin, a complex matrix product over channels
-//              (the Hadamard product fused with the channel sum, Sec. 3.3) on
-//              fp32 MFMA, with the complex product embedded in a real one.
-//   spec_inv   zero-fill + inverse real 2-D DFT + crop: only kept bins are read
-//              and only the cropped window is written.
-//   wgrad_idft inverse DFT of the kept weight-gradient bins onto the K x K taps
-//              (the projected weight gradient, Sec. 1).
-#include <hip/hip_runtime.h>
-
+//   spec_fwd_direct  zero-pad + real 2-D DFT + band mask of real planes (x or
+//                    dy): a row pass that emits only kept columns v <= r_w, then
+//                    a column pass over the nonzero input rows that emits only
+//                    kept rows.  Discarded coefficients are never formed
+//                    (Sec. 3.2.2, Fig. 2).  Any grid size.
+//   spec_inv_direct  zero-fill + inverse real 2-D DFT + crop: only kept bins are
+//                    read and only the cropped window is written.  Any grid.
+//   spec_filt        filter spectrum at the kept bins, a K x K-tap DFT per bin.
+//   wgrad_idft       inverse DFT of the kept weight-gradient bins onto the
+//                    K x K taps (the projected weight gradient, Sec. 1).
+//   contract         per kept bin, a complex matrix product over channels (the
+//                    Hadamard product fused with the channel sum, Sec. 3.3).
 #include <algorithm>
-#include <mutex>
-#include <vector>
 
-#include "plan.hpp"
+#include "common.hpp"
 
+namespace blc {
 namespace {
-
-constexpr int kThreads = 256;
-constexpr size_t kMaxLds = 64 * 1024;
 
 // e^{sign * 2 pi i k / L}, evaluated in double and rounded once to fp32.
 __device__ inline float2 unit_root(int k, int L, double sign) {
@@ -37,7 +31,6 @@ __device__ inline void fill_roots(float2* tab, int L, double sign) {
   for (int k = threadIdx.x; k < L; k += blockDim.x) tab[k] = unit_root(k, L, sign);
 }
 
-__device__ inline int kept_row(int r, int r_h, int Lh, int R) { return r <= r_h ? r : r + (Lh - R); }
 
 // ---------------------------------------------------------------------------
 // spec_fwd: real planes [P][Hin][Win] placed at (oi, oj) of the Lh x Lw grid ->
@@ -94,7 +87,7 @@ __global__ __launch_bounds__(kThreads) void k_spec_fwd(const float* __restrict__
     const int p = e % np;
     const int b = e / np;
     const int r = b / g.V, v = b % g.V;
-    const int u = kept_row(r, g.r_h, g.Lh, g.R);
+    const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
     int idx = (int)(((long)u * g.oi) % g.Lh);
     float re = 0.f, im = 0.f;
     const float2* tc = T + (size_t)p * Ts + v;
@@ -225,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
   const int b1 = min(B, b0 + g.bins_per_block);
   for (int bin = b0; bin < b1; ++bin) {
     const int r = bin / g.V, v = bin % g.V;
-    const int u = kept_row(r, g.r_h, g.Lh, g.R);
+    const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
     float re = 0.f, im = 0.f;
 #pragma unroll
     for (int a = 0; a < KH; ++a) {
@@ -246,55 +239,92 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// wgrad_idft: DW[b][c][f] -> dw[f][c][a][b'] = scale * sum_{kept (u, v)}
-//   h_v Re(DW[u, v][c][f] e^{+2 pi i (u a / Lh + v b' / Lw)}),  a < Kh, b' < Kw.
+// wgrad_idft: DW[b][q] (q = c * F + f) -> dw[f][c][t], t = (a, b') < Kh x Kw:
+//   dw = sum over kept bins (u, v) of Re(DW[u, v] * E[b][t]),
+//   E[b][t] = h_v e^{+2 pi i (u a / Lh + v b' / Lw)} / (Lh Lw)
+// (the c2r inverse restricted to the filter support).  The bins are split
+// into `chunks` slices (blockIdx.y); each block tabulates E for its slice in
+// LDS and every thread reduces one q over the slice.  With more than one
+// slice the partial sums go to part[chunk][t][q] and k_wgrad_reduce adds
+// them in a fixed order, so results do not depend on scheduling.
 // ---------------------------------------------------------------------------
-template <int KH, int KW>
+struct WgradGeom {
+  int F, C, Kh, Kw, T;
+  int Lh, Lw, r_h, R, V;
+  int bins_per_chunk, chunks;
+};
+
+template <int TMAX>
 __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, float* __restrict__ dw,
-                                                         FiltGeom g, float scale) {
-  extern __shared__ float2 smem[];
-  float2* twh = smem;
-  float2* tww = twh + g.Lh;
-  fill_roots(twh, g.Lh, 1.0);
-  fill_roots(tww, g.Lw, 1.0);
-  __syncthreads();
-  const long CF = (long)g.C * g.F;
-  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= CF) return;
-  const int c = (int)(q / g.F), f = (int)(q % g.F);
-  float acc[KH][KW];
-#pragma unroll
-  for (int a = 0; a < KH; ++a)
-#pragma unroll
-    for (int b = 0; b < KW; ++b) acc[a][b] = 0.f;
+                                                         float* __restrict__ part, WgradGeom g) {
+  extern __shared__ float2 E[];  // bins_per_chunk x T
+  const int B = g.R * g.V;
+  const int b0 = blockIdx.y * g.bins_per_chunk;
+  const int nb = min(g.bins_per_chunk, B - b0);
+  const int LL = g.Lh * g.Lw;
   const int nyq = (g.Lw % 2 == 0) ? g.Lw / 2 : -1;
-  for (int v = 0; v < g.V; ++v) {
-    float zr[KH], zi[KH];
-#pragma unroll
-    for (int a = 0; a < KH; ++a) { zr[a] = 0.f; zi[a] = 0.f; }
-    for (int r = 0; r < g.R; ++r) {
-      const int u = kept_row(r, g.r_h, g.Lh, g.R);
-      const float2 d = DW[(size_t)(r * g.V + v) * CF + q];
-#pragma unroll
-      for (int a = 0; a < KH; ++a) {
-        const float2 t = twh[(u * a) % g.Lh];
-        zr[a] = fmaf(d.x, t.x, fmaf(-d.y, t.y, zr[a]));
-        zi[a] = fmaf(d.x, t.y, fmaf(d.y, t.x, zi[a]));
-      }
-    }
-    const float h = (v == 0 || v == nyq) ? 1.f : 2.f;
-#pragma unroll
-    for (int b = 0; b < KW; ++b) {
-      const float2 t = tww[(v * b) % g.Lw];
-#pragma unroll
-      for (int a = 0; a < KH; ++a) acc[a][b] = fmaf(h, fmaf(zr[a], t.x, -zi[a] * t.y), acc[a][b]);
-    }
+  const double inv = 1.0 / (double)LL;
+  for (int e = threadIdx.x; e < nb * g.T; e += blockDim.x) {
+    const int bb = e / g.T, t = e % g.T;
+    const int bin = b0 + bb;
+    const int r = bin / g.V, v = bin % g.V;
+    const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
+    const int ta = t / g.Kw, tb = t % g.Kw;
+    const long idx = ((long)u * ta * g.Lw + (long)v * tb * g.Lh) % LL;
+    double sn, cs;
+    sincospi(2.0 * (double)idx / (double)LL, &sn, &cs);
+    const double h = (v == 0 || v == nyq) ? inv : 2.0 * inv;
+    E[e] = make_float2((float)(h * cs), (float)(h * sn));
   }
-  float* o = dw + ((size_t)f * g.C + c) * KH * KW;
+  __syncthreads();
+  const long Q = (long)g.C * g.F;
+  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  float acc[TMAX];
 #pragma unroll
-  for (int a = 0; a < KH; ++a)
+  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
+  const float2* src = DW + (size_t)b0 * Q + q;
+  for (int bb = 0; bb < nb; ++bb) {
+    const float2 d = src[(size_t)bb * Q];
+    const float2* Eb = E + bb * g.T;
 #pragma unroll
-    for (int b = 0; b < KW; ++b) o[a * KW + b] = acc[a][b] * scale;
+    for (int t = 0; t < TMAX; ++t)
+      if (t < g.T) acc[t] = fmaf(d.x, Eb[t].x, fmaf(-d.y, Eb[t].y, acc[t]));
+  }
+  if (g.chunks == 1) {
+    const int c = (int)(q / g.F), f = (int)(q % g.F);
+    float* o = dw + ((size_t)f * g.C + c) * g.T;
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t)
+      if (t < g.T) o[t] = acc[t];
+  } else {
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t)
+      if (t < g.T) part[((size_t)blockIdx.y * g.T + t) * Q + q] = acc[t];
+  }
+}
+
+// One thread per (q, t): sums the slices in a fixed order (eight independent
+// partial sums, combined pairwise at the end).
+__global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restrict__ part, float* __restrict__ dw,
+                                                           WgradGeom g) {
+  const long Q = (long)g.C * g.F;
+  const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;  // e = t * Q + q
+  if (e >= Q * g.T) return;
+  const long q = e % Q;
+  const int t = (int)(e / Q);
+  const size_t stride = (size_t)g.T * Q;
+  const float* src = part + e;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (; k + 8 <= g.chunks; k += 8) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s[i] += src[(size_t)(k + i) * stride];
+  }
+  for (int i = 0; k < g.chunks; ++k, ++i) s[i] += src[(size_t)k * stride];
+  const float tot = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+  const int c = (int)(q / g.F), f = (int)(q % g.F);
+  dw[((size_t)f * g.C + c) * g.T + t] = tot;
 }
 
 // ---------------------------------------------------------------------------
@@ -396,51 +426,20 @@ __global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict_
   }
 }
 
-// ---------------------------------------------------------------------------
-// Per-kernel timing (bl_profile_*)
-// ---------------------------------------------------------------------------
-struct Profiler {
-  std::mutex mu;
-  bool on = false;
-  int cap = 0, used = 0;
-  std::vector<hipEvent_t> ev;
-  std::vector<const char*> names;
-  std::vector<double> bytes, flops;
-} g_prof;
-
-int prof_slot(const char* name, double bytes, double flops) {
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  if (!g_prof.on || g_prof.used >= g_prof.cap) return -1;
-  g_prof.names[g_prof.used] = name;
-  g_prof.bytes[g_prof.used] = bytes;
-  g_prof.flops[g_prof.used] = flops;
-  return g_prof.used++;
-}
-
-// Launch with optional event timing.  `bytes` and `flops` are the launch's
-// algorithmic HBM traffic (compulsory reads + writes) and arithmetic, reported
-// with the timing so that measurement tools can place it on a roofline.
-template <typename Launch>
-bl_status_t timed_launch(const char* name, double bytes, double flops, hipStream_t s, Launch&& launch) {
-  const int slot = prof_slot(name, bytes, flops);
-  if (slot >= 0 && hipEventRecord(g_prof.ev[2 * slot], s) != hipSuccess) return BL_ERR_HIP;
-  launch();
-  if (hipGetLastError() != hipSuccess) return BL_ERR_HIP;
-  if (slot >= 0 && hipEventRecord(g_prof.ev[2 * slot + 1], s) != hipSuccess) return BL_ERR_HIP;
-  return BL_OK;
-}
-
-// ---------------------------------------------------------------------------
-// Launchers
-// ---------------------------------------------------------------------------
 int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap) {
   int tp = (int)std::min<long>(cap, P);
   while (tp > 1 && fixed_bytes + tp * per_plane_bytes > kMaxLds) --tp;
   return std::max(tp, 1);
 }
 
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+
 // Real planes [P][Hin][Win] at offset (oi, oj) -> bin-major kept spectrum.
-bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s) {
   FwdGeom g{Hin, Win, oi, oj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0};
   const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
@@ -450,12 +449,12 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* ou
   const size_t lds = fixed + g.TP * per;
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
-  return timed_launch("spec_fwd", bytes, 0.0, s, [&] {
+  return timed_launch("spec_fwd_direct", bytes, 0.0, s, [&] {
     hipLaunchKernelGGL(k_spec_fwd, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
   });
 }
 
-bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s) {
   InvGeom g{OH, OW, ci, cj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0, 1.0f / ((float)p->Lh * (float)p->Lw)};
   const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
@@ -465,7 +464,7 @@ bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* ou
   const size_t lds = fixed + g.TP * per;
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
-  return timed_launch("spec_inv", bytes, 0.0, s, [&] {
+  return timed_launch("spec_inv_direct", bytes, 0.0, s, [&] {
     hipLaunchKernelGGL(k_spec_inv, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
   });
 }
@@ -496,25 +495,34 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* ou
   return BL_ERR_UNSUPPORTED;
 }
 
-bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, hipStream_t s) {
-  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
-  const long CF = (long)p->Cin * p->Cout;
-  const long blocks = (CF + kThreads - 1) / kThreads;
-  const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
-  const float scale = 1.0f / ((float)p->Lh * (float)p->Lw);
-  const double bytes = (double)CF * p->kept * 8 + (double)CF * p->Kh * p->Kw * 4;
-#define X(a, b)                                                                                       \
-  if (p->Kh == a && p->Kw == b)                                                                       \
-    return timed_launch("wgrad_idft", bytes, 0.0, s, [&] {                                           \
-      hipLaunchKernelGGL((k_wgrad_idft<a, b>), dim3((unsigned)blocks), dim3(kThreads), lds, s, DW, dw, g, \
-                         scale);                                                                      \
+bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s) {
+  WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
+  const long Q = (long)p->Cin * p->Cout;
+  const int B = (int)p->kept;
+  g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices
+  g.bins_per_chunk = (B + g.chunks - 1) / g.chunks;
+  if (g.T > 64 || g.chunks > 65535) return BL_ERR_UNSUPPORTED;
+  const size_t lds = (size_t)g.bins_per_chunk * g.T * sizeof(float2);
+  if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
+  const long xblocks = (Q + kThreads - 1) / kThreads;
+  dim3 grid((unsigned)xblocks, (unsigned)g.chunks);
+  const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
+  bl_status_t st;
+  auto go = [&](auto kern) {
+    return timed_launch("wgrad_idft", bytes, 0.0, s, [&] {
+      hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, DW, dw, part, g);
     });
-  BL_FILT_CASES(X)
-#undef X
-  return BL_ERR_UNSUPPORTED;
+  };
+  if (g.T <= 8) st = go(k_wgrad_idft<8>);
+  else if (g.T <= 16) st = go(k_wgrad_idft<16>);
+  else if (g.T <= 32) st = go(k_wgrad_idft<32>);
+  else st = go(k_wgrad_idft<64>);
+  if (st != BL_OK || g.chunks == 1) return st;
+  const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
+  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&] {
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, part, dw, g);
+  });
 }
-
-enum class Contract { Forward, GradInput, GradWeight };
 
 bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
                             hipStream_t s) {
@@ -561,117 +569,4 @@ bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float
   return BL_ERR_INVALID_ARG;
 }
 
-inline float2* ws_at(void* ws, size_t off) { return reinterpret_cast<float2*>(static_cast<char*>(ws) + off); }
-
-#define BL_TRY(expr)                    \
-  do {                                  \
-    bl_status_t st_ = (expr);           \
-    if (st_ != BL_OK) return st_;       \
-  } while (0)
-
-}  // namespace
-
-// ---------------------------------------------------------------------------
-// C ABI compute entry points
-// ---------------------------------------------------------------------------
-extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const float* w, float* y, void* ws,
-                                       unsigned flags, void* stream) {
-  if (!p || !y || !ws) return BL_ERR_INVALID_ARG;
-  if (flags & ~(BL_REUSE_X | BL_REUSE_W)) return BL_ERR_INVALID_ARG;
-  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_W) && !w)) return BL_ERR_INVALID_ARG;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* X = ws_at(ws, p->off_X);
-  float2* Wf = ws_at(ws, p->off_W);
-  float2* T = ws_at(ws, p->off_T);
-  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
-  if (!(flags & BL_REUSE_X))
-    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, s));
-  return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
-}
-
-extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy, const float* w, float* dx,
-                                              void* ws, unsigned flags, void* stream) {
-  if (!p || !dy || !dx || !ws) return BL_ERR_INVALID_ARG;
-  if (flags & ~BL_REUSE_W) return BL_ERR_INVALID_ARG;
-  if (!(flags & BL_REUSE_W) && !w) return BL_ERR_INVALID_ARG;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* Wf = ws_at(ws, p->off_W);
-  float2* DY = ws_at(ws, p->off_DY);
-  float2* T = ws_at(ws, p->off_T);
-  BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
-  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
-  BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, s));
-  return launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s);
-}
-
-extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x, const float* dy, float* dw,
-                                               void* ws, unsigned flags, void* stream) {
-  if (!p || !dw || !ws) return BL_ERR_INVALID_ARG;
-  if (flags & ~(BL_REUSE_X | BL_REUSE_DY)) return BL_ERR_INVALID_ARG;
-  if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_DY) && !dy)) return BL_ERR_INVALID_ARG;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* X = ws_at(ws, p->off_X);
-  float2* DY = ws_at(ws, p->off_DY);
-  float2* DW = ws_at(ws, p->off_DW);
-  if (!(flags & BL_REUSE_X))
-    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  if (!(flags & BL_REUSE_DY))
-    BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
-  BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, s));
-  return launch_wgrad_idft(p, DW, dw, s);
-}
-
-// ---------------------------------------------------------------------------
-// Profiling entry points
-// ---------------------------------------------------------------------------
-extern "C" bl_status_t bl_profile_begin(int capacity) {
-  if (capacity <= 0) return BL_ERR_INVALID_ARG;
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  if ((int)g_prof.ev.size() < 2 * capacity) {
-    for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
-    g_prof.ev.assign(2 * capacity, nullptr);
-    for (auto& e : g_prof.ev)
-      if (hipEventCreate(&e) != hipSuccess) return BL_ERR_HIP;
-  }
-  g_prof.names.assign(capacity, nullptr);
-  g_prof.bytes.assign(capacity, 0.0);
-  g_prof.flops.assign(capacity, 0.0);
-  g_prof.cap = capacity;
-  g_prof.used = 0;
-  g_prof.on = true;
-  return BL_OK;
-}
-
-extern "C" bl_status_t bl_profile_end(void) {
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  g_prof.on = false;
-  return BL_OK;
-}
-
-extern "C" int bl_profile_count(void) {
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  return g_prof.used;
-}
-
-extern "C" bl_status_t bl_profile_get(int i, const char** kernel, float* ms, double* bytes, double* flops) {
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  if (i < 0 || i >= g_prof.used) return BL_ERR_INVALID_ARG;
-  if (kernel) *kernel = g_prof.names[i];
-  if (bytes) *bytes = g_prof.bytes[i];
-  if (flops) *flops = g_prof.flops[i];
-  if (ms) {
-    if (hipEventElapsedTime(ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]) != hipSuccess) return BL_ERR_HIP;
-  }
-  return BL_OK;
-}
-
-extern "C" bl_status_t bl_profile_release(void) {
-  std::lock_guard<std::mutex> lk(g_prof.mu);
-  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
-  g_prof.ev.clear();
-  g_prof.names.clear();
-  g_prof.cap = g_prof.used = 0;
-  g_prof.on = false;
-  return BL_OK;
-}
+}  // namespace blc

@@ -100,6 +100,20 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   p->off_DY = o; o = align_up(o + B * p->N * p->Cout * cb, 256);
   p->off_T = o;  o = align_up(o + B * p->N * (size_t)std::max(p->Cin, p->Cout) * cb, 256);
   p->off_DW = o; o = align_up(o + B * p->Cin * p->Cout * cb, 256);
+  // partial sums of the weight-gradient inverse DFT over bin slices: enough
+  // slices for ~1024 blocks, at least 16 bins per slice
+  {
+    const long Q = (long)p->Cin * p->Cout;
+    const long xblocks = (Q + 255) / 256;
+    const long want = (1024 + xblocks - 1) / xblocks;
+    const long maxc = std::max<long>(1, p->kept / 16);
+    long chunks = std::max<long>(1, std::min(want, maxc));
+    const long per = (p->kept + chunks - 1) / chunks;
+    chunks = (p->kept + per - 1) / per;
+    p->wg_chunks = (int)chunks;
+    p->off_Part = o;
+    o = align_up(o + (chunks > 1 ? (size_t)chunks * Q * p->Kh * p->Kw * sizeof(float) : 0), 256);
+  }
   p->ws_bytes = o;
   *out = p;
   return BL_OK;

@@ -30,7 +30,8 @@ struct bl_conv_plan_s {
   double c_eff;
   std::vector<uint8_t> mask;  // [Lh][Wh]
   // workspace layout (bytes)
-  size_t off_X, off_W, off_DY, off_T, off_DW, ws_bytes;
+  int wg_chunks;        // bin slices of the weight-gradient inverse DFT
+  size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, ws_bytes;
 };
 
 // FFT row index of the r-th kept row: the top-left corner (u = 0..r_h) first,

@@ -164,3 +164,25 @@ def test_edge_cases(torch):
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
             assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL, (layer.name, c)
+
+
+def test_1d_long_sequences(torch):
+    """1-D lengths that take the chirp-z (Bluestein) path with FFT sizes 256,
+    512 and 1024, odd and even grids, offsets, grid overrides, and lengths
+    beyond it (direct DFT path)."""
+    rng = np.random.default_rng(77)
+    for i in range(16):
+        L = int(rng.integers(60, 700))
+        K = int(rng.integers(1, 9))
+        lo, hi = int(rng.integers(0, K)), int(rng.integers(0, K))
+        layer = synth.Layer("long1d", 1, int(rng.integers(1, 4)), int(rng.integers(1, 20)),
+                            int(rng.integers(1, 20)), L, 1, K, (lo, hi), "walk")
+        c = float(rng.choice([0.0, 0.25, 0.5, 0.75, 0.9]))
+        fft = None if rng.random() < 0.6 else L + lo + hi + int(rng.integers(0, 40))
+        say(f"[long1d] #{i} L={L} K={K} pad=({lo},{hi}) c={c} fft={fft}")
+        x, w, dy = synth.random_inputs(layer, 900 + i)
+        y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
+        ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
+        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        say(f"    rel err {errs}")
+        assert max(errs) <= TOL
