@@ -40,6 +40,9 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* ou
   if (p->Lh == 1) {
     bl_status_t st = launch_bluestein_fwd(p, in, out, P, Win, oj, s);
     if (st != BL_ERR_UNSUPPORTED) return st;
+  } else {
+    bl_status_t st = launch_fft2_fwd(p, in, out, P, Hin, Win, oi, oj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
   }
   return launch_spec_fwd_direct(p, in, out, P, Hin, Win, oi, oj, s);
 }
@@ -48,6 +51,9 @@ bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* ou
                             int cj, hipStream_t s) {
   if (p->Lh == 1) {
     bl_status_t st = launch_bluestein_inv(p, in, out, P, OW, cj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  } else {
+    bl_status_t st = launch_fft2_inv(p, in, out, P, OH, OW, ci, cj, s);
     if (st != BL_ERR_UNSUPPORTED) return st;
   }
   return launch_spec_inv_direct(p, in, out, P, OH, OW, ci, cj, s);

@@ -71,4 +71,10 @@ bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float
 bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
                                  hipStream_t s);
 
+// 2-D transforms on (2 MH) x (2 MW) grids with MH, MW odd (mixed radix 2 x odd).
+bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+                            int oj, hipStream_t s);
+bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                            int cj, hipStream_t s);
+
 }  // namespace blc

@@ -1,0 +1,374 @@
+// 2-D kept spectra on grids of size (2 MH) x (2 MW) with MH, MW odd (gfx950).
+//
+// Forward (real planes -> kept bins, Sec. 3.2.1 zero padding, Sec. 3.2.2 band):
+//   row pass    one thread per input row: the real 2MW-point DFT of the padded
+//               row is one MW-point complex DFT of z[q] = x[2q] + i x[2q+1],
+//               split by conjugate symmetry; only columns v < V are kept.
+//   column pass one thread per (plane, kept column): the 2MH-point DFT over the
+//               padded rows is two MH-point DFTs (even and odd rows) and one
+//               radix-2 butterfly; only kept rows are written, bin-major.
+// Inverse (kept bins -> real window), the mirror image:
+//   column pass one thread per (plane, kept column): zero-filled 2MH-point
+//               inverse DFT as two MH-point inverse DFTs (decimation in
+//               frequency); only the rows of the output window are kept.
+//   row pass    one thread per output row: the Hermitian (c2r) 2MW-point
+//               inverse as one MW-point complex inverse DFT whose real and
+//               imaginary parts are the even and odd samples; the imaginary
+//               parts of the DC and Nyquist columns are dropped.
+// Odd-length DFTs pair inputs j and M - j, so each output pair k, M - k costs
+// (M - 1) complex x real products; all twiddles are compile-time constants.
+// A block handles G planes; rows go through LDS once for the transpose.
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace blc {
+namespace {
+
+// ---- compile-time trigonometry (Taylor series after exact reduction) --------
+constexpr double kPi = 3.141592653589793238462643383279502884;
+
+constexpr double cx_sin_small(double x) {  // |x| <= pi / 2
+  double term = x, sum = x;
+  for (int n = 1; n < 16; ++n) {
+    term *= -x * x / ((2.0 * n) * (2.0 * n + 1.0));
+    sum += term;
+  }
+  return sum;
+}
+constexpr double cx_cos_small(double x) {
+  double term = 1.0, sum = 1.0;
+  for (int n = 1; n < 16; ++n) {
+    term *= -x * x / ((2.0 * n - 1.0) * (2.0 * n));
+    sum += term;
+  }
+  return sum;
+}
+// cos and sin of 2 pi k / n, k in [0, n): reduce to the first quadrant exactly.
+constexpr double cx_cos2pi(int k, int n) {
+  // angle = 2 pi k / n = (pi / 2) * (4k / n); quadrant q = floor(4k / n)
+  const int q = (4 * k) / n;
+  const double r = (kPi / 2.0) * ((4.0 * k - (double)q * n) / n);  // in [0, pi/2)
+  switch (q & 3) {
+    case 0: return cx_cos_small(r);
+    case 1: return -cx_sin_small(r);
+    case 2: return -cx_cos_small(r);
+    default: return cx_sin_small(r);
+  }
+}
+constexpr double cx_sin2pi(int k, int n) {
+  const int q = (4 * k) / n;
+  const double r = (kPi / 2.0) * ((4.0 * k - (double)q * n) / n);
+  switch (q & 3) {
+    case 0: return cx_sin_small(r);
+    case 1: return cx_cos_small(r);
+    case 2: return -cx_sin_small(r);
+    default: return -cx_cos_small(r);
+  }
+}
+
+// cos(2 pi k / N) and sin(2 pi k / N) for k < N.
+template <int N>
+struct Trig {
+  float c[N], s[N];
+  constexpr Trig() : c(), s() {
+    for (int k = 0; k < N; ++k) {
+      c[k] = (float)cx_cos2pi(k, N);
+      s[k] = (float)cx_sin2pi(k, N);
+    }
+  }
+};
+template <int N>
+__device__ constexpr Trig<N> kTrig{};
+
+// M-point DFT (M odd) of z into Z; INV selects e^{+2 pi i jk / M}.
+template <int M, bool INV>
+__device__ __forceinline__ void dft_odd(const float2* z, float2* Z) {
+  constexpr int H = (M - 1) / 2;
+  float2 a[H + 1], b[H + 1];
+  float2 s = z[0];
+#pragma unroll
+  for (int j = 1; j <= H; ++j) {
+    a[j] = cadd(z[j], z[M - j]);
+    b[j] = csub(z[j], z[M - j]);
+    s = cadd(s, a[j]);
+  }
+  Z[0] = s;
+#pragma unroll
+  for (int k = 1; k <= H; ++k) {
+    float2 P = z[0], Q = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int j = 1; j <= H; ++j) {
+      const float c = kTrig<M>.c[(j * k) % M], sn = kTrig<M>.s[(j * k) % M];
+      P.x = fmaf(a[j].x, c, P.x);
+      P.y = fmaf(a[j].y, c, P.y);
+      Q.x = fmaf(b[j].x, sn, Q.x);
+      Q.y = fmaf(b[j].y, sn, Q.y);
+    }
+    const float2 minus = make_float2(P.x + Q.y, P.y - Q.x);  // P - iQ
+    const float2 plus = make_float2(P.x - Q.y, P.y + Q.x);   // P + iQ
+    Z[k] = INV ? plus : minus;
+    Z[M - k] = INV ? minus : plus;
+  }
+}
+
+// e^{-2 pi i k / N} (or its conjugate) as a compile-time constant.
+template <int N, bool INV>
+__device__ __forceinline__ float2 root(int k) {
+  const float c = kTrig<N>.c[k % N], s = kTrig<N>.s[k % N];
+  return make_float2(c, INV ? s : -s);
+}
+
+struct Fft2Args {
+  int Hin, Win;   // forward: input plane; inverse: output window (OH, OW)
+  int oi, oj;     // forward: placement offset; inverse: crop origin
+  int r_h, R, V;  // kept band
+  long P;         // planes
+  int G;          // planes per block
+  float scale;    // inverse: 1 / (Lh Lw)
+};
+
+// Index of kept row u (or -1): the top-left corner rows 0..r_h, then the
+// bottom-left corner rows Lh - (R - r_h - 1) .. Lh - 1.
+__device__ __forceinline__ int row_slot(int u, int r_h, int R, int LH) {
+  if (u <= r_h) return u;
+  const int r = u - (LH - R);
+  return r > r_h ? r : -1;
+}
+
+template <int MH, int MW>
+__global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, float2* __restrict__ out,
+                                                       Fft2Args g) {
+  constexpr int LH = 2 * MH, LW = 2 * MW;
+  extern __shared__ float2 sm[];
+  float* xs = reinterpret_cast<float*>(sm);  // staging: G planes x Hin rows x (Win + 1)
+  float2* T = sm;                            // row spectra: G planes x (Hin V + 1), aliases xs
+  const int tid = threadIdx.x;
+  const long p0 = (long)blockIdx.x * g.G;
+  const int np = (int)min((long)g.G, g.P - p0);
+  const int plane = g.Hin * g.Win;
+  const int WS = g.Win + 1;
+  const int PS = g.Hin * g.V + 1;
+
+  // coalesced load of the block's planes (contiguous in HBM)
+  const float* src = in + p0 * plane;
+  for (int e = tid; e < np * plane; e += blockDim.x) {
+    const int pr = e / g.Win, j = e - pr * g.Win;
+    xs[pr * WS + j] = src[e];
+  }
+  __syncthreads();
+
+  // row pass: thread = (plane, row)
+  const int nrows = np * g.Hin;
+  float2 X[MW + 1];
+  int my_p = 0, my_i = 0;
+  const bool has_row = tid < nrows;
+  if (has_row) {
+    my_p = tid / g.Hin;
+    my_i = tid - my_p * g.Hin;
+    const float* xr = xs + tid * WS;
+    float2 z[MW];
+#pragma unroll
+    for (int q = 0; q < MW; ++q) {
+      const int j0 = 2 * q - g.oj, j1 = 2 * q + 1 - g.oj;
+      z[q].x = (j0 >= 0 && j0 < g.Win) ? xr[j0] : 0.f;
+      z[q].y = (j1 >= 0 && j1 < g.Win) ? xr[j1] : 0.f;
+    }
+    float2 Z[MW];
+    dft_odd<MW, false>(z, Z);
+#pragma unroll
+    for (int v = 0; v <= MW; ++v) {
+      const float2 zv = Z[v % MW];
+      const float2 zc = cconj(Z[(MW - v) % MW]);
+      const float2 E = cscale(cadd(zv, zc), 0.5f);
+      const float2 d = csub(zv, zc);
+      const float2 O = make_float2(0.5f * d.y, -0.5f * d.x);  // d / (2i)
+      X[v] = cadd(E, cmul(root<LW, false>(v), O));
+    }
+  }
+  __syncthreads();  // all rows read from the staging area before it is overwritten
+  if (has_row) {
+#pragma unroll
+    for (int v = 0; v <= MW; ++v)
+      if (v < g.V) T[my_p * PS + my_i * g.V + v] = X[v];
+  }
+  __syncthreads();
+
+  // column pass: thread = (kept column, plane), planes fastest
+  for (int e = tid; e < np * g.V; e += blockDim.x) {
+    const int p = e % np, v = e / np;
+    const float2* tc = T + p * PS + v;
+    float2 ev[MH], od[MH];
+#pragma unroll
+    for (int q = 0; q < MH; ++q) {
+      const int i0 = 2 * q - g.oi, i1 = 2 * q + 1 - g.oi;
+      ev[q] = (i0 >= 0 && i0 < g.Hin) ? tc[i0 * g.V] : make_float2(0.f, 0.f);
+      od[q] = (i1 >= 0 && i1 < g.Hin) ? tc[i1 * g.V] : make_float2(0.f, 0.f);
+    }
+    float2 E[MH], O[MH];
+    dft_odd<MH, false>(ev, E);
+    dft_odd<MH, false>(od, O);
+    float2* dst = out + p0 + p;
+#pragma unroll
+    for (int k = 0; k < MH; ++k) {
+      const float2 t = cmul(root<LH, false>(k), O[k]);
+      const int r_lo = row_slot(k, g.r_h, g.R, LH);
+      const int r_hi = row_slot(k + MH, g.r_h, g.R, LH);
+      if (r_lo >= 0) dst[(size_t)(r_lo * g.V + v) * g.P] = cadd(E[k], t);
+      if (r_hi >= 0) dst[(size_t)(r_hi * g.V + v) * g.P] = csub(E[k], t);
+    }
+  }
+}
+
+template <int MH, int MW>
+__global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
+                                                       Fft2Args g) {
+  constexpr int LH = 2 * MH, LW = 2 * MW;
+  extern __shared__ float2 sm[];
+  float2* Zs = sm;                           // column results: G planes x (OH V + 1)
+  float* ys = reinterpret_cast<float*>(sm);  // output staging: G planes x OH x OW, aliases Zs
+  const int tid = threadIdx.x;
+  const int OH = g.Hin, OW = g.Win;
+  const long p0 = (long)blockIdx.x * g.G;
+  const int np = (int)min((long)g.G, g.P - p0);
+  const int PS = OH * g.V + 1;
+
+  // column pass: thread = (kept column, plane), planes fastest
+  for (int e = tid; e < np * g.V; e += blockDim.x) {
+    const int p = e % np, v = e / np;
+    const float2* src = in + p0 + p;
+    float2 lo[MH], hi[MH];
+#pragma unroll
+    for (int k = 0; k < MH; ++k) {
+      const int r0 = row_slot(k, g.r_h, g.R, LH);
+      const int r1 = row_slot(k + MH, g.r_h, g.R, LH);
+      lo[k] = r0 >= 0 ? src[(size_t)(r0 * g.V + v) * g.P] : make_float2(0.f, 0.f);
+      hi[k] = r1 >= 0 ? src[(size_t)(r1 * g.V + v) * g.P] : make_float2(0.f, 0.f);
+    }
+    float2 a[MH], b[MH];
+#pragma unroll
+    for (int k = 0; k < MH; ++k) {
+      a[k] = cadd(lo[k], hi[k]);
+      b[k] = cmul(root<LH, true>(k), csub(lo[k], hi[k]));
+    }
+    float2 xe[MH], xo[MH];
+    dft_odd<MH, true>(a, xe);
+    dft_odd<MH, true>(b, xo);
+    float2* zc = Zs + p * PS + v;
+#pragma unroll
+    for (int q = 0; q < MH; ++q) {
+      const int i0 = 2 * q - g.oi, i1 = 2 * q + 1 - g.oi;
+      if (i0 >= 0 && i0 < OH) zc[i0 * g.V] = xe[q];
+      if (i1 >= 0 && i1 < OH) zc[i1 * g.V] = xo[q];
+    }
+  }
+  __syncthreads();
+
+  // row pass: thread = (plane, output row)
+  const int nrows = np * OH;
+  const bool has_row = tid < nrows;
+  float yv[LW];
+  if (has_row) {
+    const int p = tid / OH, i = tid - (tid / OH) * OH;
+    const float2* zr = Zs + p * PS + i * g.V;
+    float2 Zh[MW + 1];
+#pragma unroll
+    for (int v = 0; v <= MW; ++v) Zh[v] = v < g.V ? zr[v] : make_float2(0.f, 0.f);
+    Zh[0].y = 0.f;   // c2r: imaginary parts of the DC and Nyquist columns are dropped
+    Zh[MW].y = 0.f;
+    float2 Q[MW];
+#pragma unroll
+    for (int k = 0; k < MW; ++k) {
+      const float2 zk = Zh[k], zc = cconj(Zh[MW - k]);
+      const float2 A = cadd(zk, zc);
+      const float2 B = cmul(root<LW, true>(k), csub(zk, zc));
+      Q[k] = make_float2(A.x - B.y, A.y + B.x);  // A + iB
+    }
+    float2 q[MW];
+    dft_odd<MW, true>(Q, q);
+#pragma unroll
+    for (int n = 0; n < MW; ++n) {
+      yv[2 * n] = q[n].x * g.scale;
+      yv[2 * n + 1] = q[n].y * g.scale;
+    }
+  }
+  __syncthreads();  // every row read from Zs before the staging overwrites it
+  if (has_row) {
+    float* yr = ys + tid * OW;
+#pragma unroll
+    for (int j = 0; j < LW; ++j) {
+      const int jj = j - g.oj;
+      if (jj >= 0 && jj < OW) yr[jj] = yv[j];
+    }
+  }
+  __syncthreads();
+  float* dst = out + p0 * (long)OH * OW;
+  for (int e = tid; e < np * OH * OW; e += blockDim.x) dst[e] = ys[e];
+}
+
+template <int MH, int MW>
+bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+                         int oj, hipStream_t s) {
+  Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, P, 0, 1.0f};
+  // rows of a block must fit one pass of 256 threads; LDS for staging and spectra
+  int G = std::max(1, kThreads / Hin);
+  G = (int)std::min<long>(G, P);
+  auto lds_for = [&](int gg) {
+    const size_t stage = (size_t)gg * Hin * (Win + 1) * sizeof(float);
+    const size_t spec = (size_t)gg * (Hin * p->V + 1) * sizeof(float2);
+    return std::max(stage, spec);
+  };
+  while (G > 1 && lds_for(G) > kMaxLds) --G;
+  if (Hin > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
+  g.G = G;
+  const long blocks = (P + G - 1) / G;
+  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
+  return timed_launch("spec_fwd_2d", bytes, 0.0, s, [&] {
+    hipLaunchKernelGGL((k_fft2_fwd<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
+  });
+}
+
+template <int MH, int MW>
+bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                         int cj, hipStream_t s) {
+  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, P, 0, 1.0f / ((float)p->Lh * (float)p->Lw)};
+  int G = std::max(1, kThreads / OH);
+  G = (int)std::min<long>(G, P);
+  auto lds_for = [&](int gg) {
+    const size_t spec = (size_t)gg * (OH * p->V + 1) * sizeof(float2);
+    const size_t stage = (size_t)gg * OH * OW * sizeof(float);
+    return std::max(stage, spec);
+  };
+  while (G > 1 && lds_for(G) > kMaxLds) --G;
+  if (OH > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
+  g.G = G;
+  const long blocks = (P + G - 1) / G;
+  const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
+  return timed_launch("spec_inv_2d", bytes, 0.0, s, [&] {
+    hipLaunchKernelGGL((k_fft2_inv<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
+  });
+}
+
+#define BL_FFT2_GRIDS(X) X(3, 3) X(5, 5) X(9, 9) X(17, 17) X(29, 29)
+
+}  // namespace
+
+bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+                            int oj, hipStream_t s) {
+#define X(a, b) \
+  if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_fwd_t<a, b>(p, in, out, P, Hin, Win, oi, oj, s);
+  BL_FFT2_GRIDS(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                            int cj, hipStream_t s) {
+#define X(a, b) \
+  if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_inv_t<a, b>(p, in, out, P, OH, OW, ci, cj, s);
+  BL_FFT2_GRIDS(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+}  // namespace blc

@@ -186,3 +186,30 @@ def test_1d_long_sequences(torch):
         errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
         say(f"    rel err {errs}")
         assert max(errs) <= TOL
+
+
+def test_2d_fast_grids(torch):
+    """Grids 6, 10, 18, 34, 58 (2 x odd: the mixed-radix 2-D path) reached with
+    other filter sizes, asymmetric padding, non-square inputs and grid
+    overrides, at several rates."""
+    rng = np.random.default_rng(123)
+    cases = []
+    for L in (6, 10, 18, 34, 58):
+        for _ in range(3):
+            K = int(rng.integers(1, min(L, 8) + 1))
+            pt, pb, pl, pr = (int(rng.integers(0, K)) for _ in range(4))
+            H, W = L - pt - pb, L - pl - pr
+            if H < 1 or W < 1 or H + pt + pb < K or W + pl + pr < K:
+                continue
+            cases.append((synth.Layer("fast2d", 2, int(rng.integers(1, 4)), int(rng.integers(1, 24)),
+                                      int(rng.integers(1, 24)), H, W, K, (pt, pb, pl, pr), "blur"), None))
+        # an input smaller than the grid, reached through the grid override
+        cases.append((synth.Layer("fast2d_ovr", 2, 2, 5, 7, L - 5, L - 4, 3, (1, 1, 0, 2), "blur"), (L, L)))
+    for layer, fft in cases:
+        for c in (0.0, 0.3, 0.6, 0.9):
+            say(f"[fast2d] {layer} c={c} fft={fft}")
+            x, w, dy = synth.random_inputs(layer, 77)
+            y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
+            ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
+            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            assert max(errs) <= TOL, errs
