@@ -120,12 +120,15 @@ __device__ __forceinline__ float2 root(int k) {
 }
 
 struct Fft2Args {
-  int Hin, Win;   // forward: input plane; inverse: output window (OH, OW)
-  int oi, oj;     // forward: placement offset; inverse: crop origin
-  int r_h, R, V;  // kept band
-  long P;         // planes
-  int G;          // planes per block
-  float scale;    // inverse: 1 / (Lh Lw)
+  int Hin, Win;    // forward: input plane; inverse: output window (OH, OW)
+  int oi, oj;      // forward: placement offset; inverse: crop origin
+  int r_h, R, V;   // kept band
+  unsigned P;      // planes
+  int G;           // planes per block
+  int PS;          // LDS plane stride of the column-major spectra (complex)
+  unsigned q4;     // Win / 4 (forward) or OW (inverse): divisor of the flat copy
+  unsigned magic;  // ceil(2^32 / q4) for q4 > 1: e / q4 == umulhi(e, magic) for the block's e
+  float scale;     // inverse: 1 / (Lh Lw)
 };
 
 // Index of kept row u (or -1): the top-left corner rows 0..r_h, then the
@@ -136,44 +139,49 @@ __device__ __forceinline__ int row_slot(int u, int r_h, int R, int LH) {
   return r > r_h ? r : -1;
 }
 
+// LDS layout (complex spectra, column-major per plane): S[p * PS + v * (LH + 1) + i],
+// so a column thread reads its LH rows at fixed offsets.
 template <int MH, int MW>
 __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, float2* __restrict__ out,
                                                        Fft2Args g) {
-  constexpr int LH = 2 * MH, LW = 2 * MW;
+  constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
   extern __shared__ float2 sm[];
-  float* xs = reinterpret_cast<float*>(sm);  // staging: G planes x Hin rows x (Win + 1)
-  float2* T = sm;                            // row spectra: G planes x (Hin V + 1), aliases xs
+  float* xs = reinterpret_cast<float*>(sm);  // staging: G*Hin padded grid rows of LW1 floats
+  float2* T = sm;                            // row spectra, column-major; aliases xs
   const int tid = threadIdx.x;
-  const long p0 = (long)blockIdx.x * g.G;
-  const int np = (int)min((long)g.G, g.P - p0);
-  const int plane = g.Hin * g.Win;
-  const int WS = g.Win + 1;
-  const int PS = g.Hin * g.V + 1;
+  const unsigned p0 = blockIdx.x * (unsigned)g.G;
+  const int np = (int)min((unsigned)g.G, g.P - p0);
+  const int nrows = np * g.Hin;
 
-  // coalesced load of the block's planes (contiguous in HBM)
-  const float* src = in + p0 * plane;
-  for (int e = tid; e < np * plane; e += blockDim.x) {
-    const int pr = e / g.Win, j = e - pr * g.Win;
-    xs[pr * WS + j] = src[e];
+  // each row thread zeroes the padding columns of its staging row
+  if (tid < nrows) {
+    float* xr = xs + tid * LW1;
+    for (int j = 0; j < g.oj; ++j) xr[j] = 0.f;
+    for (int j = g.oj + g.Win; j < LW; ++j) xr[j] = 0.f;
+  }
+  // coalesced copy of the block's rows into their grid columns
+  const float4* src = reinterpret_cast<const float4*>(in + (size_t)p0 * g.Hin * g.Win);
+  const unsigned n4 = (unsigned)nrows * g.q4;
+  for (unsigned e = tid; e < n4; e += blockDim.x) {
+    const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
+    const unsigned j4 = e - row * g.q4;
+    const float4 v = src[e];
+    float* xr = xs + row * LW1 + g.oj + 4 * j4;
+    xr[0] = v.x; xr[1] = v.y; xr[2] = v.z; xr[3] = v.w;
   }
   __syncthreads();
 
-  // row pass: thread = (plane, row)
-  const int nrows = np * g.Hin;
+  // row pass: thread = (plane, input row)
   float2 X[MW + 1];
   int my_p = 0, my_i = 0;
   const bool has_row = tid < nrows;
   if (has_row) {
     my_p = tid / g.Hin;
     my_i = tid - my_p * g.Hin;
-    const float* xr = xs + tid * WS;
+    const float* xr = xs + tid * LW1;
     float2 z[MW];
 #pragma unroll
-    for (int q = 0; q < MW; ++q) {
-      const int j0 = 2 * q - g.oj, j1 = 2 * q + 1 - g.oj;
-      z[q].x = (j0 >= 0 && j0 < g.Win) ? xr[j0] : 0.f;
-      z[q].y = (j1 >= 0 && j1 < g.Win) ? xr[j1] : 0.f;
-    }
+    for (int q = 0; q < MW; ++q) z[q] = make_float2(xr[2 * q], xr[2 * q + 1]);
     float2 Z[MW];
     dft_odd<MW, false>(z, Z);
 #pragma unroll
@@ -188,34 +196,37 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
   }
   __syncthreads();  // all rows read from the staging area before it is overwritten
   if (has_row) {
+    float2* tr = T + my_p * g.PS + g.oi + my_i;
 #pragma unroll
     for (int v = 0; v <= MW; ++v)
-      if (v < g.V) T[my_p * PS + my_i * g.V + v] = X[v];
+      if (v < g.V) tr[v * LH1] = X[v];
   }
   __syncthreads();
 
   // column pass: thread = (kept column, plane), planes fastest
   for (int e = tid; e < np * g.V; e += blockDim.x) {
     const int p = e % np, v = e / np;
-    const float2* tc = T + p * PS + v;
+    float2* tc = T + p * g.PS + v * LH1;
+    for (int i = 0; i < g.oi; ++i) tc[i] = make_float2(0.f, 0.f);
+    for (int i = g.oi + g.Hin; i < LH; ++i) tc[i] = make_float2(0.f, 0.f);
     float2 ev[MH], od[MH];
 #pragma unroll
     for (int q = 0; q < MH; ++q) {
-      const int i0 = 2 * q - g.oi, i1 = 2 * q + 1 - g.oi;
-      ev[q] = (i0 >= 0 && i0 < g.Hin) ? tc[i0 * g.V] : make_float2(0.f, 0.f);
-      od[q] = (i1 >= 0 && i1 < g.Hin) ? tc[i1 * g.V] : make_float2(0.f, 0.f);
+      ev[q] = tc[2 * q];
+      od[q] = tc[2 * q + 1];
     }
     float2 E[MH], O[MH];
     dft_odd<MH, false>(ev, E);
     dft_odd<MH, false>(od, O);
-    float2* dst = out + p0 + p;
+    float2* dst = out + (p0 + p) + (unsigned)v * g.P;
+    const unsigned rs = (unsigned)g.V * g.P;
 #pragma unroll
     for (int k = 0; k < MH; ++k) {
       const float2 t = cmul(root<LH, false>(k), O[k]);
       const int r_lo = row_slot(k, g.r_h, g.R, LH);
       const int r_hi = row_slot(k + MH, g.r_h, g.R, LH);
-      if (r_lo >= 0) dst[(size_t)(r_lo * g.V + v) * g.P] = cadd(E[k], t);
-      if (r_hi >= 0) dst[(size_t)(r_hi * g.V + v) * g.P] = csub(E[k], t);
+      if (r_lo >= 0) dst[r_lo * rs] = cadd(E[k], t);
+      if (r_hi >= 0) dst[r_hi * rs] = csub(E[k], t);
     }
   }
 }
@@ -223,43 +234,38 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
 template <int MH, int MW>
 __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
                                                        Fft2Args g) {
-  constexpr int LH = 2 * MH, LW = 2 * MW;
+  constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
   extern __shared__ float2 sm[];
-  float2* Zs = sm;                           // column results: G planes x (OH V + 1)
-  float* ys = reinterpret_cast<float*>(sm);  // output staging: G planes x OH x OW, aliases Zs
+  float2* Zs = sm;                           // column results, column-major per plane
+  float* ys = reinterpret_cast<float*>(sm);  // output staging: G*OH grid rows of LW1 floats; aliases Zs
   const int tid = threadIdx.x;
   const int OH = g.Hin, OW = g.Win;
-  const long p0 = (long)blockIdx.x * g.G;
-  const int np = (int)min((long)g.G, g.P - p0);
-  const int PS = OH * g.V + 1;
+  const unsigned p0 = blockIdx.x * (unsigned)g.G;
+  const int np = (int)min((unsigned)g.G, g.P - p0);
 
   // column pass: thread = (kept column, plane), planes fastest
   for (int e = tid; e < np * g.V; e += blockDim.x) {
     const int p = e % np, v = e / np;
-    const float2* src = in + p0 + p;
-    float2 lo[MH], hi[MH];
+    const float2* src = in + (p0 + p) + (unsigned)v * g.P;
+    const unsigned rs = (unsigned)g.V * g.P;
+    float2 a[MH], b[MH];
 #pragma unroll
     for (int k = 0; k < MH; ++k) {
       const int r0 = row_slot(k, g.r_h, g.R, LH);
       const int r1 = row_slot(k + MH, g.r_h, g.R, LH);
-      lo[k] = r0 >= 0 ? src[(size_t)(r0 * g.V + v) * g.P] : make_float2(0.f, 0.f);
-      hi[k] = r1 >= 0 ? src[(size_t)(r1 * g.V + v) * g.P] : make_float2(0.f, 0.f);
-    }
-    float2 a[MH], b[MH];
-#pragma unroll
-    for (int k = 0; k < MH; ++k) {
-      a[k] = cadd(lo[k], hi[k]);
-      b[k] = cmul(root<LH, true>(k), csub(lo[k], hi[k]));
+      const float2 lo = r0 >= 0 ? src[r0 * rs] : make_float2(0.f, 0.f);
+      const float2 hi = r1 >= 0 ? src[r1 * rs] : make_float2(0.f, 0.f);
+      a[k] = cadd(lo, hi);
+      b[k] = cmul(root<LH, true>(k), csub(lo, hi));
     }
     float2 xe[MH], xo[MH];
     dft_odd<MH, true>(a, xe);
     dft_odd<MH, true>(b, xo);
-    float2* zc = Zs + p * PS + v;
+    float2* zc = Zs + p * g.PS + v * LH1;
 #pragma unroll
     for (int q = 0; q < MH; ++q) {
-      const int i0 = 2 * q - g.oi, i1 = 2 * q + 1 - g.oi;
-      if (i0 >= 0 && i0 < OH) zc[i0 * g.V] = xe[q];
-      if (i1 >= 0 && i1 < OH) zc[i1 * g.V] = xo[q];
+      zc[2 * q] = xe[q];
+      zc[2 * q + 1] = xo[q];
     }
   }
   __syncthreads();
@@ -270,10 +276,10 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   float yv[LW];
   if (has_row) {
     const int p = tid / OH, i = tid - (tid / OH) * OH;
-    const float2* zr = Zs + p * PS + i * g.V;
+    const float2* zr = Zs + p * g.PS + g.oi + i;
     float2 Zh[MW + 1];
 #pragma unroll
-    for (int v = 0; v <= MW; ++v) Zh[v] = v < g.V ? zr[v] : make_float2(0.f, 0.f);
+    for (int v = 0; v <= MW; ++v) Zh[v] = v < g.V ? zr[v * LH1] : make_float2(0.f, 0.f);
     Zh[0].y = 0.f;   // c2r: imaginary parts of the DC and Nyquist columns are dropped
     Zh[MW].y = 0.f;
     float2 Q[MW];
@@ -294,28 +300,38 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   }
   __syncthreads();  // every row read from Zs before the staging overwrites it
   if (has_row) {
-    float* yr = ys + tid * OW;
+    float* yr = ys + tid * LW1;
 #pragma unroll
-    for (int j = 0; j < LW; ++j) {
-      const int jj = j - g.oj;
-      if (jj >= 0 && jj < OW) yr[jj] = yv[j];
-    }
+    for (int j = 0; j < LW; ++j) yr[j] = yv[j];
   }
   __syncthreads();
-  float* dst = out + p0 * (long)OH * OW;
-  for (int e = tid; e < np * OH * OW; e += blockDim.x) dst[e] = ys[e];
+  // coalesced copy of the cropped window (planes contiguous in HBM)
+  float* dst = out + (size_t)p0 * OH * OW;
+  const unsigned n = (unsigned)nrows * OW;
+  for (unsigned e = tid; e < n; e += blockDim.x) {
+    const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
+    const unsigned j = e - row * g.q4;
+    dst[e] = ys[row * LW1 + g.oj + j];
+  }
 }
+
+// ceil(2^32 / d) for d > 1 (d = 1 is handled by the kernels directly).
+unsigned magic_for(unsigned d) { return d > 1 ? (unsigned)((0x100000000ull + d - 1) / d) : 0u; }
 
 template <int MH, int MW>
 bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
                          int oj, hipStream_t s) {
-  Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, P, 0, 1.0f};
+  constexpr int LH = 2 * MH, LW = 2 * MW;
+  if (Win % 4 != 0 || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
+  Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)(Win / 4), 0, 1.0f};
+  g.magic = magic_for(g.q4);
+  g.PS = (p->V * (LH + 1)) | 1;
   // rows of a block must fit one pass of 256 threads; LDS for staging and spectra
   int G = std::max(1, kThreads / Hin);
   G = (int)std::min<long>(G, P);
   auto lds_for = [&](int gg) {
-    const size_t stage = (size_t)gg * Hin * (Win + 1) * sizeof(float);
-    const size_t spec = (size_t)gg * (Hin * p->V + 1) * sizeof(float2);
+    const size_t stage = (size_t)gg * Hin * (LW + 1) * sizeof(float);
+    const size_t spec = (size_t)gg * g.PS * sizeof(float2);
     return std::max(stage, spec);
   };
   while (G > 1 && lds_for(G) > kMaxLds) --G;
@@ -331,12 +347,17 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, 
 template <int MH, int MW>
 bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                          int cj, hipStream_t s) {
-  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, P, 0, 1.0f / ((float)p->Lh * (float)p->Lw)};
+  constexpr int LH = 2 * MH, LW = 2 * MW;
+  if ((double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
+  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)OW, 0,
+             1.0f / ((float)p->Lh * (float)p->Lw)};
+  g.magic = magic_for(g.q4);
+  g.PS = (p->V * (LH + 1)) | 1;
   int G = std::max(1, kThreads / OH);
   G = (int)std::min<long>(G, P);
   auto lds_for = [&](int gg) {
-    const size_t spec = (size_t)gg * (OH * p->V + 1) * sizeof(float2);
-    const size_t stage = (size_t)gg * OH * OW * sizeof(float);
+    const size_t spec = (size_t)gg * g.PS * sizeof(float2);
+    const size_t stage = (size_t)gg * OH * (LW + 1) * sizeof(float);
     return std::max(stage, spec);
   };
   while (G > 1 && lds_for(G) > kMaxLds) --G;
