@@ -47,6 +47,13 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* ou
   return launch_spec_fwd_direct(p, in, out, P, Hin, Win, oi, oj, s);
 }
 
+bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+                            float2* part, hipStream_t s) {
+  bl_status_t st = launch_contract_tiled(p, which, A, Bm, O, part, s);
+  if (st != BL_ERR_UNSUPPORTED) return st;
+  return launch_contract_generic(p, which, A, Bm, O, s);
+}
+
 bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s) {
   if (p->Lh == 1) {
@@ -89,7 +96,7 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
   if (!(flags & BL_REUSE_X))
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, s));
+  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, ws_at(ws, p->off_CPart), s));
   return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
 }
 
@@ -104,7 +111,7 @@ extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy,
   float2* T = ws_at(ws, p->off_T);
   BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
-  BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, s));
+  BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, ws_at(ws, p->off_CPart), s));
   return launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s);
 }
 
@@ -121,7 +128,7 @@ extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x,
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
   if (!(flags & BL_REUSE_DY))
     BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
-  BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, s));
+  BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, ws_at(ws, p->off_CPart), s));
   return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
 }
 

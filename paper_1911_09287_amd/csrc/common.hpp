@@ -56,7 +56,13 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
 
 enum class Contract { Forward, GradInput, GradWeight };
 bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
-                            hipStream_t s);
+                            float2* part, hipStream_t s);
+// Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
+// generic one (any strides and sizes).
+bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+                                  float2* O, float2* part, hipStream_t s);
+bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+                                    float2* O, hipStream_t s);
 
 // Direct (pruned DFT) transforms: any grid; used where no fast path applies.
 bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win,

@@ -1,0 +1,250 @@
+// Per-kept-bin complex channel contraction on fp32 MFMA (gfx950), tiled.
+//
+// For each kept bin, O[m][n] = sum_k A[m][k] op(B[k][n]) with op = conj or
+// identity: the Hadamard product of the spectra fused with the sum over a
+// channel index (Sec. 3.3).  The complex product is embedded in a real GEMM:
+// A is read as the real [M x 2K] matrix of interleaved (re, im) pairs, B as the
+// real [2K x 2N] matrix of 2x2 blocks [[br, -bi], [bi, br]] (conj) or
+// [[br, bi], [-bi, br]] (identity), expanded on the fly from the complex values
+// in LDS; the real [M x 2N] result is the interleaved complex O.  Each
+// v_mfma_f32_32x32x2f32 step consumes one complex k.
+//
+// Block tile: BM rows x 64 complex columns, 8 complex k per stage, LDS double
+// buffered with the next stage's global loads (16-byte vectors, two complex
+// values each) in flight during the current stage's MFMAs.  4 waves in a 2x2
+// grid; a wave owns BM/2 rows x 32 complex columns.  Operands are staged in
+// LDS as separate real and imaginary planes, k-major, so that each MFMA
+// operand fetch is one conflict-free 32-bit LDS read per lane.
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace blc {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+struct CgemmArgs {
+  int M, N, K;                   // complex sizes
+  unsigned sAm, sAk, sBk, sBn;   // element strides (complex units); one of each pair is 1
+  unsigned ldo;
+  unsigned long long bA, bB, bO;  // per-bin strides
+  unsigned long long split_stride;  // complex elements between the partial outputs of two k-splits
+  int tiles_n;
+  int kper;                         // complex k per split (multiple of the stage depth)
+};
+
+constexpr int kBN = 64;  // complex columns per block
+constexpr int kBK = 8;   // complex k per stage
+
+template <int BM, bool A_KC, bool B_NC, bool CONJ>
+__global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
+                                               float2* __restrict__ O, CgemmArgs g) {
+  constexpr int WM = BM / 2;   // rows per wave
+  constexpr int MI = WM / 32;  // 32-row MFMA blocks per wave
+  constexpr int NJ = 2;        // 16-complex-column MFMA blocks per wave
+  constexpr int AV = BM / 64;  // 16-byte A loads per thread per stage
+  __shared__ float As[2][2][kBK][BM];
+  __shared__ float Bs[2][2][kBK][kBN];
+
+  const int bin = blockIdx.y;
+  const int kbeg = blockIdx.z * g.kper;
+  const int kend = min(g.K, kbeg + g.kper);
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x - (blockIdx.x / g.tiles_n) * g.tiles_n;
+  const int m0 = tm * BM, n0 = tn * kBN;
+  const float2* Ab = A + bin * g.bA;
+  const float2* Bb = Bm + bin * g.bB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * WM, wn = (wave & 1) * 32;
+
+  // B operand of this lane: real column jcol = lane % 32 of a 32-wide block is
+  // complex column jcol / 2, part jcol % 2; real k row a_part = lane / 32.
+  const int a_part = lane >> 5;
+  const int jcol = lane & 31;
+  const int bcol = jcol & 1;
+  const int b_src = (a_part == bcol) ? 0 : 1;  // br on the block diagonal, bi off it
+  float b_sign = 1.f;
+  if (CONJ && a_part == 0 && bcol == 1) b_sign = -1.f;
+  if (!CONJ && a_part == 1 && bcol == 0) b_sign = -1.f;
+
+  floatx16 acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  float4 ra[AV], rb;
+  const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
+
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      const int e = tid + 256 * q;
+      int m, k;
+      if (A_KC) { m = e >> 2; k = (e & 3) * 2; }
+      else { k = e / (BM / 2); m = (e - k * (BM / 2)) * 2; }
+      ra[q] = zero4;
+      if ((m0 + m < g.M) && (k0 + k < kend))
+        ra[q] = *reinterpret_cast<const float4*>(Ab + (size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk);
+    }
+    {
+      int k, n;
+      if (B_NC) { k = tid >> 5; n = (tid & 31) * 2; }
+      else { n = tid >> 2; k = (tid & 3) * 2; }
+      rb = zero4;
+      if ((n0 + n < g.N) && (k0 + k < kend))
+        rb = *reinterpret_cast<const float4*>(Bb + (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      const int e = tid + 256 * q;
+      if (A_KC) {
+        const int m = e >> 2, k = (e & 3) * 2;
+        As[buf][0][k][m] = ra[q].x; As[buf][1][k][m] = ra[q].y;
+        As[buf][0][k + 1][m] = ra[q].z; As[buf][1][k + 1][m] = ra[q].w;
+      } else {
+        const int k = e / (BM / 2), m = (e - k * (BM / 2)) * 2;
+        As[buf][0][k][m] = ra[q].x; As[buf][1][k][m] = ra[q].y;
+        As[buf][0][k][m + 1] = ra[q].z; As[buf][1][k][m + 1] = ra[q].w;
+      }
+    }
+    if (B_NC) {
+      const int k = tid >> 5, n = (tid & 31) * 2;
+      Bs[buf][0][k][n] = rb.x; Bs[buf][1][k][n] = rb.y;
+      Bs[buf][0][k][n + 1] = rb.z; Bs[buf][1][k][n + 1] = rb.w;
+    } else {
+      const int n = tid >> 2, k = (tid & 3) * 2;
+      Bs[buf][0][k][n] = rb.x; Bs[buf][1][k][n] = rb.y;
+      Bs[buf][0][k + 1][n] = rb.z; Bs[buf][1][k + 1][n] = rb.w;
+    }
+  };
+
+  const int nst = (kend - kbeg + kBK - 1) / kBK;
+  load(kbeg);
+  store(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int cur = st & 1;
+    if (st + 1 < nst) load(kbeg + (st + 1) * kBK);
+#pragma unroll
+    for (int s = 0; s < kBK; ++s) {
+      float av[MI], bv[NJ];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) av[i] = As[cur][a_part][s][wm + 32 * i + jcol];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) bv[j] = b_sign * Bs[cur][b_src][s][wn + 16 * j + (jcol >> 1)];
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (st + 1 < nst) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
+  float* Of = reinterpret_cast<float*>(O + blockIdx.z * g.split_stride + bin * g.bO);
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int n = n0 + wn + 16 * j + (jcol >> 1);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        if (m < g.M && n < g.N) Of[((size_t)m * g.ldo + n) * 2 + bcol] = acc[i][j][v];
+      }
+    }
+}
+
+// out[i] = sum over k-splits of part[s][i], in split order.
+__global__ __launch_bounds__(256) void k_split_reduce(const float4* __restrict__ part, float4* __restrict__ out,
+                                                      unsigned long long n4, int splits) {
+  const unsigned long long i = (unsigned long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 acc = part[i];
+  for (int s = 1; s < splits; ++s) {
+    const float4 v = part[(unsigned long long)s * n4 + i];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  out[i] = acc;
+}
+
+}  // namespace
+
+// Tiled path: needs 16-byte aligned pairs of complex values along the
+// contiguous dimension of each operand; returns BL_ERR_UNSUPPORTED otherwise.
+bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+                                  float2* O, float2* part, hipStream_t s) {
+  CgemmArgs g{};
+  const unsigned long long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
+  bool a_kc = true, b_nc = true, conj = true;
+  switch (which) {
+    case Contract::Forward:  // Y[n][f] = sum_c X[n][c] conj(W[c][f])
+      g.M = (int)N; g.N = (int)Co; g.K = (int)Ci;
+      g.sAm = (unsigned)Ci; g.sAk = 1; g.sBk = (unsigned)Co; g.sBn = 1; g.ldo = (unsigned)Co;
+      g.bA = N * Ci; g.bB = Ci * Co; g.bO = N * Co;
+      a_kc = true; b_nc = true; conj = true;
+      break;
+    case Contract::GradInput:  // DX[n][c] = sum_f DY[n][f] W[c][f]
+      g.M = (int)N; g.N = (int)Ci; g.K = (int)Co;
+      g.sAm = (unsigned)Co; g.sAk = 1; g.sBk = 1; g.sBn = (unsigned)Co; g.ldo = (unsigned)Ci;
+      g.bA = N * Co; g.bB = Ci * Co; g.bO = N * Ci;
+      a_kc = true; b_nc = false; conj = false;
+      break;
+    case Contract::GradWeight:  // DW[c][f] = sum_n X[n][c] conj(DY[n][f])
+      g.M = (int)Ci; g.N = (int)Co; g.K = (int)N;
+      g.sAm = 1; g.sAk = (unsigned)Ci; g.sBk = (unsigned)Co; g.sBn = 1; g.ldo = (unsigned)Co;
+      g.bA = N * Ci; g.bB = N * Co; g.bO = Ci * Co;
+      a_kc = false; b_nc = true; conj = true;
+      break;
+  }
+  // alignment of every 2-complex vector: even strides, even sizes along the vector
+  const bool a_ok = (g.bA % 2 == 0) && (a_kc ? (g.sAm % 2 == 0 && g.K % 2 == 0) : (g.sAk % 2 == 0 && g.M % 2 == 0));
+  const bool b_ok = (g.bB % 2 == 0) && (b_nc ? (g.sBk % 2 == 0 && g.N % 2 == 0) : (g.sBn % 2 == 0 && g.K % 2 == 0));
+  if (!a_ok || !b_ok || B > 65535) return BL_ERR_UNSUPPORTED;
+  const BlContractTiling& t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
+  const bool big = t.bm == 128;
+  const int BM = t.bm;
+  const int tiles_m = (g.M + BM - 1) / BM;
+  g.tiles_n = (g.N + kBN - 1) / kBN;
+  const unsigned long long total = B * (unsigned long long)g.M * g.N;  // complex outputs
+  int splits = t.splits;
+  g.kper = (g.K + splits - 1) / splits;
+  g.kper = (g.kper + kBK - 1) / kBK * kBK;
+  splits = (g.K + g.kper - 1) / g.kper;
+  if (total % 2 != 0) splits = 1, g.kper = g.K;  // the reduction works on pairs
+  g.split_stride = total;
+  float2* dst = splits > 1 ? part : O;
+  dim3 grid((unsigned)(tiles_m * g.tiles_n), (unsigned)B, (unsigned)splits);
+  const double flops = 8.0 * B * g.M * g.N * g.K;
+  const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
+  const char* name = which == Contract::Forward ? "contract_fwd"
+                     : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
+  bl_status_t st;
+#define BL_GO(BMV, AK, BN_, CJ)                                                                    \
+  st = timed_launch(name, bytes, flops, s, [&] {                                                   \
+    hipLaunchKernelGGL((k_cgemm<BMV, AK, BN_, CJ>), grid, dim3(256), 0, s, A, Bm, dst, g);          \
+  })
+  if (which == Contract::Forward) {
+    if (big) BL_GO(128, true, true, true); else BL_GO(64, true, true, true);
+  } else if (which == Contract::GradInput) {
+    if (big) BL_GO(128, true, false, false); else BL_GO(64, true, false, false);
+  } else {
+    if (big) BL_GO(128, false, true, true); else BL_GO(64, false, true, true);
+  }
+#undef BL_GO
+  if (st != BL_OK || splits == 1) return st;
+  const unsigned long long n4 = total / 2;
+  const unsigned long long blocks = (n4 + 255) / 256;
+  return timed_launch("contract_reduce", 8.0 * total * (splits + 1), 0.0, s, [&] {
+    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)blocks), dim3(256), 0, s,
+                       reinterpret_cast<const float4*>(part), reinterpret_cast<float4*>(O), n4, splits);
+  });
+}
+
+}  // namespace blc

@@ -524,7 +524,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   });
 }
 
-bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
                             hipStream_t s) {
   ContractArgs g{};
   const long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;

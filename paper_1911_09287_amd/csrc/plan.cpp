@@ -114,6 +114,19 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
     p->off_Part = o;
     o = align_up(o + (chunks > 1 ? (size_t)chunks * Q * p->Kh * p->Kw * sizeof(float) : 0), 256);
   }
+  // split-k partial tiles of the contraction (largest of the three passes)
+  {
+    const long Bk = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
+    p->ct[0] = bl_contract_tiling(N, Co, Ci, Bk);
+    p->ct[1] = bl_contract_tiling(N, Ci, Co, Bk);
+    p->ct[2] = bl_contract_tiling(Ci, Co, N, Bk);
+    size_t need = 0;
+    const long mn[3] = {N * Co, N * Ci, Ci * Co};
+    for (int i = 0; i < 3; ++i)
+      if (p->ct[i].splits > 1) need = std::max(need, (size_t)p->ct[i].splits * Bk * mn[i] * cb);
+    p->off_CPart = o;
+    o = align_up(o + need, 256);
+  }
   p->ws_bytes = o;
   *out = p;
   return BL_OK;

@@ -12,6 +12,25 @@
 
 #include "../../include/blconv.h"
 
+// Tiling of the per-bin contraction [M x K] . [K x N] (complex) over `bins`
+// bins: tile height (64 or 128 rows, 64 complex columns) and the number of
+// k-splits, so that a launch has at least ~512 work items (2 per CU of an
+// MI355X) while each split keeps at least 32 complex k.  Split partial tiles
+// are summed in a fixed order by a separate pass (deterministic results).
+struct BlContractTiling {
+  int bm, splits;
+};
+inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
+  BlContractTiling t{M > 64 ? 128 : 64, 1};
+  const long tiles = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
+  if (tiles < 512 && t.bm == 128) {
+    t.bm = 64;
+  }
+  const long tiles2 = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
+  while (tiles2 * t.splits < 512 && K / (2 * t.splits) >= 32 && t.splits < 16) t.splits *= 2;
+  return t;
+}
+
 struct bl_conv_plan_s {
   bl_conv_desc_t desc;
   int ndim;
@@ -31,7 +50,8 @@ struct bl_conv_plan_s {
   std::vector<uint8_t> mask;  // [Lh][Wh]
   // workspace layout (bytes)
   int wg_chunks;        // bin slices of the weight-gradient inverse DFT
-  size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, ws_bytes;
+  BlContractTiling ct[3];  // contraction tiling: forward, grad-input, grad-weight
+  size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
 };
 
 // FFT row index of the r-th kept row: the top-left corner (u = 0..r_h) first,
