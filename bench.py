@@ -26,7 +26,21 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 MFMA_F32_PEAK_TF = 157.3   # MI355X dense fp32 matrix, TFLOP/s
+# fp32 vector arithmetic without packed math (the build disables it):
+# 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz
+VALU_F32_PEAK_TF = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 RIDGE = MFMA_F32_PEAK_TF * 1e12 / (HBM_PEAK_GBS * 1e9)
+VALU_RIDGE = VALU_F32_PEAK_TF * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def bound_of(name, nbytes, nflops):
+    """Roofline that applies to a kernel: its arithmetic unit when the launch's
+    algorithmic intensity is above that unit's ridge, else HBM."""
+    if nflops and name.startswith("contract") and nflops / nbytes > RIDGE:
+        return "mfma", MFMA_F32_PEAK_TF
+    if nflops and name.startswith("spec_") and nflops / nbytes > VALU_RIDGE:
+        return "alu", VALU_F32_PEAK_TF
+    return "hbm", HBM_PEAK_GBS
 
 
 def parse():
@@ -108,22 +122,26 @@ def roofline(torch, blconv, layers, steps):
     kernels = {}
     for name, (n, ms, nb, nf) in agg.items():
         s = ms * 1e-3
+        bound, peak = bound_of(name, nb, nf)
         kernels[name] = {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms,
                          "GBps": nb / s / 1e9, "TFLOPs": nf / s / 1e12 if nf else None,
                          "hbm_frac": nb / s / 1e9 / HBM_PEAK_GBS,
-                         "mfma_frac": (nf / s / 1e12 / MFMA_F32_PEAK_TF) if nf else None,
-                         "ai": (nf / nb) if nf else None}
+                         "mfma_frac": (nf / s / 1e12 / MFMA_F32_PEAK_TF) if nf and name.startswith("contract") else None,
+                         "alu_frac": (nf / s / 1e12 / VALU_F32_PEAK_TF) if nf and name.startswith("spec_") else None,
+                         "ai": (nf / nb) if nf else None, "bound": bound}
     dom = max(agg, key=lambda k: agg[k][1])
     n, ms, nb, nf = agg[dom]
     s = ms * 1e-3
-    if nf and nf / nb > RIDGE:
-        roof = {"kernel": dom, "bound": "mfma", "achieved": nf / s / 1e12, "peak": MFMA_F32_PEAK_TF,
-                "unit": "TFLOP/s", "frac": nf / s / 1e12 / MFMA_F32_PEAK_TF, "traffic": None,
-                "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_flops": nf / n}
-    else:
+    bound, peak = bound_of(dom, nb, nf)
+    if bound == "hbm":
         roof = {"kernel": dom, "bound": "hbm", "achieved": nb / s / 1e9, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": nb / s / 1e9 / HBM_PEAK_GBS, "traffic": None,
                 "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_bytes": nb / n}
+    else:
+        roof = {"kernel": dom, "bound": bound, "achieved": nf / s / 1e12, "peak": peak,
+                "unit": "TFLOP/s", "frac": nf / s / 1e12 / peak, "traffic": None,
+                "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_flops": nf / n,
+                "per_launch_bytes": nb / n, "hbm_GBps": nb / s / 1e9}
     return roof, kernels
 
 

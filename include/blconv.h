@@ -155,9 +155,11 @@ const char* bl_status_string(bl_status_t status);
  * has been synchronised, bl_profile_count / bl_profile_get return each
  * launch's kernel name (a static string), its duration in milliseconds and
  * its algorithmic cost: the compulsory HBM bytes (every input read once, every
- * output written once) and, for the channel contraction, the real flops of
- * the complex products (8 per complex multiply-add).  Output pointers may be
- * NULL.  bl_profile_end stops recording; bl_profile_release frees the events. */
+ * output written once) and the arithmetic: for the channel contraction the
+ * real flops of the complex products (8 per complex multiply-add), for the
+ * transforms the conventional FFT count (5 N log2 N per complex N-point FFT,
+ * 2.5 N log2 N per real one) of the FFTs the kernel performs.  Output pointers
+ * may be NULL.  bl_profile_end stops recording; bl_profile_release frees the events. */
 bl_status_t bl_profile_begin(int capacity);
 bl_status_t bl_profile_end(void);
 int bl_profile_count(void);

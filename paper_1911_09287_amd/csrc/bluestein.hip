@@ -372,6 +372,12 @@ int device_cus() {
 
 template <int M, int MODE>
 bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+  // algorithmic arithmetic: two M-point complex FFTs (5 M log2 M flops each, the
+  // conventional count) per series, or per pair of series when two share an FFT
+  const double ffts = (MODE >= 2) ? (double)((a.P + 1) / 2) : (double)a.P;
+  double lg = 0;
+  for (int m = M; m > 1; m >>= 1) lg += 1;
+  const double flops = ffts * 2.0 * 5.0 * M * lg;
   // host-side seeds of the root and chirp tables, in double precision
   for (int i = 0; i < M / 64; ++i) {
     const double t = -2.0 * M_PI * 64.0 * i / M;
@@ -393,7 +399,7 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
   const long groups = (a.P + kSeriesPerGroup - 1) / kSeriesPerGroup;
   const long blocks = std::min<long>(groups, 2L * device_cus());
-  return timed_launch(name, bytes, 0.0, s, [&] {
+  return timed_launch(name, bytes, flops, s, [&] {
     hipLaunchKernelGGL((k_bluestein<M, MODE>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, in, out, a);
   });
 }

@@ -19,6 +19,7 @@
 // (M - 1) complex x real products; all twiddles are compile-time constants.
 // A block handles G planes; rows go through LDS once for the transpose.
 #include <algorithm>
+#include <cmath>
 
 #include "common.hpp"
 
@@ -339,7 +340,10 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, 
   g.G = G;
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
-  return timed_launch("spec_fwd_2d", bytes, 0.0, s, [&] {
+  // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
+  // complex LH-point column FFTs (5 LH log2 LH) per plane
+  const double flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
+  return timed_launch("spec_fwd_2d", bytes, flops, s, [&] {
     hipLaunchKernelGGL((k_fft2_fwd<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
   });
 }
@@ -365,7 +369,8 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   g.G = G;
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
-  return timed_launch("spec_inv_2d", bytes, 0.0, s, [&] {
+  const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
+  return timed_launch("spec_inv_2d", bytes, flops, s, [&] {
     hipLaunchKernelGGL((k_fft2_inv<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
   });
 }
