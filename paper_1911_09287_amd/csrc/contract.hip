@@ -35,7 +35,7 @@ struct CgemmArgs {
 };
 
 constexpr int kBN = 64;  // complex columns per block
-constexpr int kBK = 8;   // complex k per stage
+constexpr int kBK = 16;  // complex k per stage
 
 template <int BM, bool A_KC, bool B_NC, bool CONJ>
 __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
@@ -43,7 +43,8 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
   constexpr int WM = BM / 2;   // rows per wave
   constexpr int MI = WM / 32;  // 32-row MFMA blocks per wave
   constexpr int NJ = 2;        // 16-complex-column MFMA blocks per wave
-  constexpr int AV = BM / 64;  // 16-byte A loads per thread per stage
+  constexpr int AV = BM / 32;  // 16-byte A loads per thread per stage
+  constexpr int BV = 2;        // 16-byte B loads per thread per stage
   __shared__ float As[2][2][kBK][BM];
   __shared__ float Bs[2][2][kBK][kBN];
 
@@ -75,7 +76,7 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  float4 ra[AV], rb;
+  float4 ra[AV], rb[BV];
   const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
 
   auto load = [&](int k0) {
@@ -83,19 +84,21 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
     for (int q = 0; q < AV; ++q) {
       const int e = tid + 256 * q;
       int m, k;
-      if (A_KC) { m = e >> 2; k = (e & 3) * 2; }
+      if (A_KC) { m = e >> 3; k = (e & 7) * 2; }
       else { k = e / (BM / 2); m = (e - k * (BM / 2)) * 2; }
       ra[q] = zero4;
       if ((m0 + m < g.M) && (k0 + k < kend))
         ra[q] = *reinterpret_cast<const float4*>(Ab + (size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk);
     }
-    {
+#pragma unroll
+    for (int q = 0; q < BV; ++q) {
+      const int e = tid + 256 * q;
       int k, n;
-      if (B_NC) { k = tid >> 5; n = (tid & 31) * 2; }
-      else { n = tid >> 2; k = (tid & 3) * 2; }
-      rb = zero4;
+      if (B_NC) { k = e >> 5; n = (e & 31) * 2; }
+      else { n = e >> 3; k = (e & 7) * 2; }
+      rb[q] = zero4;
       if ((n0 + n < g.N) && (k0 + k < kend))
-        rb = *reinterpret_cast<const float4*>(Bb + (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
+        rb[q] = *reinterpret_cast<const float4*>(Bb + (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
     }
   };
   auto store = [&](int buf) {
@@ -103,7 +106,7 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
     for (int q = 0; q < AV; ++q) {
       const int e = tid + 256 * q;
       if (A_KC) {
-        const int m = e >> 2, k = (e & 3) * 2;
+        const int m = e >> 3, k = (e & 7) * 2;
         As[buf][0][k][m] = ra[q].x; As[buf][1][k][m] = ra[q].y;
         As[buf][0][k + 1][m] = ra[q].z; As[buf][1][k + 1][m] = ra[q].w;
       } else {
@@ -112,14 +115,18 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
         As[buf][0][k][m + 1] = ra[q].z; As[buf][1][k][m + 1] = ra[q].w;
       }
     }
-    if (B_NC) {
-      const int k = tid >> 5, n = (tid & 31) * 2;
-      Bs[buf][0][k][n] = rb.x; Bs[buf][1][k][n] = rb.y;
-      Bs[buf][0][k][n + 1] = rb.z; Bs[buf][1][k][n + 1] = rb.w;
-    } else {
-      const int n = tid >> 2, k = (tid & 3) * 2;
-      Bs[buf][0][k][n] = rb.x; Bs[buf][1][k][n] = rb.y;
-      Bs[buf][0][k + 1][n] = rb.z; Bs[buf][1][k + 1][n] = rb.w;
+#pragma unroll
+    for (int q = 0; q < BV; ++q) {
+      const int e = tid + 256 * q;
+      if (B_NC) {
+        const int k = e >> 5, n = (e & 31) * 2;
+        Bs[buf][0][k][n] = rb[q].x; Bs[buf][1][k][n] = rb[q].y;
+        Bs[buf][0][k][n + 1] = rb[q].z; Bs[buf][1][k][n + 1] = rb[q].w;
+      } else {
+        const int n = e >> 3, k = (e & 7) * 2;
+        Bs[buf][0][k][n] = rb[q].x; Bs[buf][1][k][n] = rb[q].y;
+        Bs[buf][0][k + 1][n] = rb[q].z; Bs[buf][1][k + 1][n] = rb[q].w;
+      }
     }
   };
 
@@ -130,18 +137,22 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
   for (int st = 0; st < nst; ++st) {
     const int cur = st & 1;
     if (st + 1 < nst) load(kbeg + (st + 1) * kBK);
+    // all fragments of the stage first, so the LDS reads overlap the MFMAs
+    float av[kBK][MI], bv[kBK][NJ];
 #pragma unroll
     for (int s = 0; s < kBK; ++s) {
-      float av[MI], bv[NJ];
 #pragma unroll
-      for (int i = 0; i < MI; ++i) av[i] = As[cur][a_part][s][wm + 32 * i + jcol];
+      for (int i = 0; i < MI; ++i) av[s][i] = As[cur][a_part][s][wm + 32 * i + jcol];
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) bv[j] = b_sign * Bs[cur][b_src][s][wn + 16 * j + (jcol >> 1)];
+      for (int j = 0; j < NJ; ++j) bv[s][j] = Bs[cur][b_src][s][wn + 16 * j + (jcol >> 1)];
+    }
+#pragma unroll
+    for (int s = 0; s < kBK; ++s)
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
+        for (int j = 0; j < NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[s][i], b_sign * bv[s][j], acc[i][j], 0, 0, 0);
     if (st + 1 < nst) store(cur ^ 1);
     __syncthreads();
   }

@@ -14,9 +14,10 @@
 
 // Tiling of the per-bin contraction [M x K] . [K x N] (complex) over `bins`
 // bins: tile height (64 or 128 rows, 64 complex columns) and the number of
-// k-splits, so that a launch has at least ~1024 work items (4 per CU of an
-// MI355X, enough waves to cover HBM latency) while each split keeps at least
-// 32 complex k.  Split partial tiles
+// k-splits: 64-row tiles when 128-row ones give fewer than ~512 work items
+// (2 per CU of an MI355X), and k-splits while there are still fewer than ~512,
+// each split keeping at least 64 complex k (the pass that sums the split
+// partials only pays off when the splits are long).  Split partial tiles
 // are summed in a fixed order by a separate pass (deterministic results).
 struct BlContractTiling {
   int bm, splits;
@@ -24,11 +25,11 @@ struct BlContractTiling {
 inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
   BlContractTiling t{M > 64 ? 128 : 64, 1};
   const long tiles = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
-  if (tiles < 1024 && t.bm == 128) {
+  if (tiles < 512 && t.bm == 128) {
     t.bm = 64;
   }
   const long tiles2 = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
-  while (tiles2 * t.splits < 1024 && K / (2 * t.splits) >= 32 && t.splits < 16) t.splits *= 2;
+  while (tiles2 * t.splits < 512 && K / (2 * t.splits) >= 64 && t.splits < 16) t.splits *= 2;
   return t;
 }
 
