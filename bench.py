@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--table", default=None, help="also write a per-config/per-c table (JSON lines) here")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first run a plain elementwise copy of this many MiB (fp32), the reference kernel "
+                         "for scaling hardware traffic counters")
     return ap.parse_args()
 
 
@@ -145,6 +148,27 @@ def roofline(torch, blconv, layers, steps):
     return roof, kernels
 
 
+KERNEL_SOURCES = {"spec_fwd_1d": "bluestein.hip", "spec_inv_1d": "bluestein.hip", "spec_fwd_2d": "fft2d.hip",
+                  "spec_inv_2d": "fft2d.hip", "contract_fwd": "contract.hip", "contract_dgrad": "contract.hip",
+                  "contract_wgrad": "contract.hip", "wgrad_idft": "direct.hip", "spec_filt": "direct.hip"}
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter measurement, or None if
+    there is none for this kernel and workload or the kernel source changed."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
+        return None
+    t = json.load(open(path))
+    src = os.path.join(ROOT, "paper_1911_09287_amd", "csrc", KERNEL_SOURCES[kernel])
+    if t.get("kernel") != kernel or t.get("workload") != workload or not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != t.get("source_sha256_16"):
+        return None
+    return t["traffic_bytes_per_launch"]
+
+
 def cpu_baseline(cfg, c, target_s):
     """The fp64 oracle on a bounded sample: the first n samples of the batch."""
     from oracle import bl_oracle as bo
@@ -199,6 +223,14 @@ def main():
         sys.exit(1)
     blconv.load()
     dev = torch.device("cuda:0")
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, device=dev)
+        dst = torch.empty(n, device=dev)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)  # reads 4n bytes, writes 4n bytes
+        torch.cuda.synchronize()
+        del src, dst
     cfg = synth.CONFIGS[args.config]
     arrays = [synth.layer_inputs(args.config, i) for i in range(len(cfg.layers))]
     eq_flops = sum(3 * L.direct_flops() for L in cfg.layers)
@@ -209,6 +241,10 @@ def main():
     layers = build(args.c)
     ms, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup)
     roof, kernels = roofline(torch, blconv, layers, max(1, min(args.steps, 10)))
+    workload_key = f"config {args.config} c={args.c}"
+    roof["traffic"] = measured_traffic(roof["kernel"], workload_key)
+    if roof["traffic"] is not None:
+        roof["traffic_over_algorithmic"] = roof["traffic"] / roof["per_launch_bytes"]
     value = eq_flops / (ms * 1e-3) / 1e12
 
     per_c = []
