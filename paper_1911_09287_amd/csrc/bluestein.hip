@@ -41,16 +41,10 @@ constexpr float kW32s[16] = {0.0f, -0.19509032201612825f, -0.38268343236508978f,
                              -0.83146961230254546f, -0.70710678118654757f, -0.55557023301960218f,
                              -0.38268343236508989f, -0.19509032201612861f};
 
-// a * e^{-2 pi i k / R} for a compile-time k (after unrolling), R <= 32.
-template <int R>
-__device__ __forceinline__ float2 rot(float2 a, int k) {
-  if (k == 0) return a;
-  if (4 * k == R) return make_float2(a.y, -a.x);
-  const float c = kW32c[k * (32 / R)], s = kW32s[k * (32 / R)];
-  return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.x, s, a.y * c));
-}
-
-// In-register R-point DFT (natural order in and out), radix-2 decimation in time.
+// In-register R-point DFT (natural order in and out), radix-2 decimation in
+// time, R <= 32.  A butterfly with a general twiddle w forms e + w o with four
+// fused multiply-adds and takes the difference as 2 e - (e + w o), one more
+// each (6 instructions instead of 4 for w o and 4 for the sum and difference).
 template <int R>
 struct RegFft {
   static __device__ __forceinline__ void run(float2* v) {
@@ -64,9 +58,19 @@ struct RegFft {
     RegFft<R / 2>::run(o);
 #pragma unroll
     for (int k = 0; k < R / 2; ++k) {
-      const float2 t = rot<R>(o[k], k);
-      v[k] = cadd(e[k], t);
-      v[k + R / 2] = csub(e[k], t);
+      if (k == 0) {
+        v[k] = cadd(e[k], o[k]);
+        v[k + R / 2] = csub(e[k], o[k]);
+      } else if (4 * k == R) {  // w = -i
+        v[k] = make_float2(e[k].x + o[k].y, e[k].y - o[k].x);
+        v[k + R / 2] = make_float2(e[k].x - o[k].y, e[k].y + o[k].x);
+      } else {
+        const float c = kW32c[k * (32 / R)], sn = kW32s[k * (32 / R)];
+        const float2 x = make_float2(fmaf(o[k].x, c, fmaf(-o[k].y, sn, e[k].x)),
+                                     fmaf(o[k].x, sn, fmaf(o[k].y, c, e[k].y)));
+        v[k] = x;
+        v[k + R / 2] = make_float2(fmaf(2.f, e[k].x, -x.x), fmaf(2.f, e[k].y, -x.y));
+      }
     }
   }
 };
@@ -217,7 +221,7 @@ __device__ __forceinline__ void block_fft(float2* buf, int t, const float2* root
   if (Ns < M) stockham_pass<M, 2, NT>(Ns, t, roots, nullptr, lb, sb);
 }
 
-struct BlueArgs {
+struct BlueGeom {
   int n_in, n_out;     // inputs and outputs of the chirp convolution per FFT
   int L;               // DFT length
   int V;               // kept bins per series
@@ -225,6 +229,8 @@ struct BlueArgs {
   int nyq;             // Nyquist bin (L even) or -1
   long P;              // number of series
   float out_scale;     // extra output scale (inverse: 1 / L)
+};
+struct BlueArgs : BlueGeom {
   float2 root_hi[16], root_lo[64];    // e^{-2 pi i k / M} = hi[k >> 6] * lo[k & 63]
   float2 chirp_hi[64], chirp_lo[64];  // e^{-i pi q / L} = hi[q >> 6] * lo[q & 63], q < 2L
 };
@@ -357,6 +363,266 @@ __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restric
   }
 }
 
+// ---------------------------------------------------------------------------
+// M = 1024 as 32 x 32 per half-wave: with n = l + 32 j and k' = k + 32 m,
+//   X[k + 32 m] = sum_l w32^{lm} [w1024^{lk} sum_j x[l + 32 j] w32^{jk}],
+// lane l of a half-wave runs the inner 32-point FFT over j in registers, the
+// twiddled results cross lanes once through LDS (a 32 x 33 transpose), and
+// lane k runs the outer 32-point FFT over l, ending with X[k + 32 m] in its
+// registers.  That is exactly the layout the second FFT's inner pass needs
+// (lane k holding element k + 32 m), so the pointwise product with the filter
+// spectrum needs no extra transpose: each Bluestein job costs one LDS
+// transpose per FFT instead of a pass per radix stage.
+// A block has 8 waves = 16 half-wave slots; each slot takes jobs (one series,
+// or a pair of series in the paired modes) of its block's contiguous range.
+// ---------------------------------------------------------------------------
+constexpr int kWaves1k = 8;
+constexpr int kXS = 32 * 33;  // transpose buffer of one slot (complex)
+
+// c[m] = e^{-i pi m^2 / L} from seed tables held in LDS (see chirp()).
+template <bool INV>
+__device__ __forceinline__ float2 chirp_lds(const float2* chi, const float2* clo, int L, int m) {
+  const unsigned mm = (unsigned)(m < 0 ? -m : m);
+  const int q = (int)((mm * mm) % (2u * (unsigned)L));
+  const float2 c = cmul(chi[q >> 6], clo[q & 63]);
+  return INV ? cconj(c) : c;
+}
+
+// e^{-i pi x} for x = num / den, evaluated in double precision.
+__device__ __forceinline__ float2 expmpi(double num, double den) {
+  double sn, cs;
+  sincospi(-num / den, &sn, &cs);
+  return make_float2((float)cs, (float)sn);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
+                                                               BlueGeom a, long jobs_per_block) {
+  constexpr int M = 1024;
+  constexpr bool INV = MODE & 1, PACK = MODE >= 2;
+  extern __shared__ float2 sm[];
+  float2* bufs = sm;                          // 16 slots x kXS
+  float2* pre = bufs + 2 * kWaves1k * kXS;    // n_in
+  float2* post = pre + a.n_in;                // n_out
+  float2* F = post + a.n_out;                 // spectrum of the chirp filter (M)
+  float2* TW = F + M;                         // TW[32 k + h] = w1024^{h k}
+  float2* chi = bufs;                         // chirp seeds, only during setup
+  float2* clo = bufs + 128;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int slot = lane >> 5, h = lane & 31;
+  float2* xb = bufs + (wave * 2 + slot) * kXS;
+
+  // seeds of the chirp, e^{-i pi q / L} = chi[q >> 6] * clo[q & 63] for
+  // q < 2L <= 8192, and the twiddles, all computed here (the angles of TW are
+  // exact in single precision)
+  if (tid < 64) {
+    clo[tid] = expmpi(tid, a.L);
+  } else if (tid < 64 + 128) {
+    chi[tid - 64] = expmpi(64.0 * (tid - 64), a.L);
+  }
+  for (int i = tid; i < M; i += blockDim.x) {
+    const int e = ((i >> 5) * (i & 31)) & (M - 1);
+    float sn, cs;
+    sincospif(-(float)e / (M / 2), &sn, &cs);
+    TW[i] = make_float2(cs, sn);
+  }
+  __syncthreads();
+  for (int k = tid; k < a.n_in; k += blockDim.x) {
+    float2 c = chirp_lds<INV>(chi, clo, a.L, k + a.off_in);
+    if (INV && !PACK && k != 0 && k != a.nyq) c = cscale(c, 2.f);
+    pre[k] = c;
+  }
+  const float osc = a.out_scale / (float)M * (PACK && !INV ? 0.5f : 1.0f);
+  for (int k = tid; k < a.n_out; k += blockDim.x) post[k] = cscale(chirp_lds<INV>(chi, clo, a.L, k + a.off_out), osc);
+  for (int m = tid; m < M; m += blockDim.x) {
+    const int d = m < a.n_out ? m : m - M;
+    F[m] = (d >= -(a.n_in - 1)) ? cconj(chirp_lds<INV>(chi, clo, a.L, d + a.off_out - a.off_in))
+                                : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  auto exchange = [&](float2* v) {
+#pragma unroll
+    for (int k = 0; k < 32; ++k) xb[k * 33 + h] = v[k];
+    wave_sync();
+#pragma unroll
+    for (int l = 0; l < 32; ++l) v[l] = xb[h * 33 + l];
+    wave_sync();
+  };
+  // inner FFT over j (input v[j] = element h + 32 j), twiddle, transpose, outer FFT:
+  // leaves v[m] = element h + 32 m of the transform.
+  auto fft1k = [&](float2* v) {
+    RegFft<32>::run(v);
+#pragma unroll
+    for (int k = 1; k < 32; ++k) v[k] = cmul(v[k], TW[32 * k + h]);
+    exchange(v);
+    RegFft<32>::run(v);
+  };
+
+  // spectrum of the chirp filter, in place, by wave 0 (lane h only touches
+  // the elements h + 32 j; the chirp seeds in its transpose buffers are no
+  // longer needed)
+  __syncthreads();
+  if (wave == 0) {
+    float2 v[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = F[h + 32 * j];
+    fft1k(v);
+    if (slot == 0) {
+#pragma unroll
+      for (int m = 0; m < 32; ++m) F[h + 32 * m] = v[m];
+    }
+  }
+  __syncthreads();
+
+  // Jobs go 16 at a time (one per slot).  Series data moves between HBM and
+  // the slot buffers cooperatively, so that every bin row of a bin-major
+  // spectrum is read or written as 16 (or 32 paired) consecutive series, and
+  // the slots run their transforms on LDS-resident data.
+  const float* xin = static_cast<const float*>(in_);
+  const float2* yin = static_cast<const float2*>(in_);
+  const long P = a.P;
+  const long jobs = PACK ? (P + 1) / 2 : P;
+  const long j0 = blockIdx.x * jobs_per_block;
+  const long j1 = min(jobs, j0 + jobs_per_block);
+  constexpr int NS = 2 * kWaves1k;  // slots per block
+  constexpr int NT = 64 * kWaves1k;
+  for (long base = j0; base < j1; base += NS) {
+    const int nj = (int)min((long)NS, j1 - base);  // jobs this round
+    __syncthreads();
+    // Loads are issued in batches (indices clamped into range instead of
+    // branched on) so that a thread has many in flight before it waits.
+    if constexpr (MODE == 0 || MODE == 2) {
+      for (int n = tid; n < a.n_in; n += NT) {
+        float x1[NS], x2[NS];
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) {
+          const long job = min(base + sl, j1 - 1);
+          if constexpr (MODE == 0) {
+            x1[sl] = xin[(size_t)job * a.n_in + n];
+          } else {
+            const long s1 = 2 * job;
+            const long s2 = min(s1 + 1, P - 1);
+            x1[sl] = xin[(size_t)s1 * a.n_in + n];
+            x2[sl] = xin[(size_t)s2 * a.n_in + n];
+            if (s2 == s1) x2[sl] = 0.f;
+          }
+        }
+        const float2 pn = pre[n];
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl)
+          bufs[sl * kXS + n] = MODE == 0 ? cscale(pn, x1[sl]) : cmul(make_float2(x1[sl], x2[sl]), pn);
+      }
+    } else {
+      constexpr int RB = 8;  // rows per batch
+      const int sl = tid & (NS - 1);
+      const long job = min(base + sl, j1 - 1);
+      float2* dst = bufs + sl * kXS;
+      for (int n0 = tid / NS; n0 < a.n_in; n0 += RB * (NT / NS)) {
+        float2 y1[RB], y2[RB];
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+          const int n = min(n0 + u * (NT / NS), a.n_in - 1);
+          if constexpr (MODE == 1) {
+            y1[u] = yin[(size_t)n * P + job];
+          } else {
+            // two Hermitian spectra packed into one series: Z[k] = Y1[k] + i Y2[k]
+            // for k = n - (V - 1) in (-V, V), with Y[-k] = conj(Y[k])
+            const int k = n - (a.V - 1);
+            const int kk = k < 0 ? -k : k;
+            const long s1 = 2 * job;
+            const long s2 = min(s1 + 1, P - 1);
+            y1[u] = yin[(size_t)kk * P + s1];
+            y2[u] = yin[(size_t)kk * P + s2];
+            if (s2 == s1) y2[u] = make_float2(0.f, 0.f);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+          const int n = n0 + u * (NT / NS);
+          if (n < a.n_in) {
+            float2 x;
+            if constexpr (MODE == 1) {
+              x = y1[u];
+            } else {
+              const int k = n - (a.V - 1);
+              if (k > 0) x = make_float2(y1[u].x - y2[u].y, y1[u].y + y2[u].x);
+              else if (k < 0) x = make_float2(y1[u].x + y2[u].y, y2[u].x - y1[u].y);
+              else x = make_float2(y1[u].x, y2[u].x);
+            }
+            dst[n] = cmul(x, pre[n]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (2 * wave < nj) {  // waves with no job this round skip the transforms
+      float2 v[32];
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        const int n = h + 32 * j;
+        v[j] = n < a.n_in ? xb[n] : make_float2(0.f, 0.f);
+      }
+      wave_sync();
+      fft1k(v);
+      // inverse FFT of (A * F) as conj(FFT(conj(A * F)))
+#pragma unroll
+      for (int m = 0; m < 32; ++m) v[m] = cconj(cmul(v[m], F[h + 32 * m]));
+      fft1k(v);
+#pragma unroll
+      for (int m = 0; m < 32; ++m) {
+        const int i = h + 32 * m;
+        if (i < a.n_out) xb[i] = cmul(post[i], cconj(v[m]));
+      }
+    }
+    __syncthreads();
+    if constexpr (MODE == 0) {
+      const int sl = tid & (NS - 1);
+      if (sl < nj) {
+        float2* dst = static_cast<float2*>(out_) + base + sl;
+        const float2* src = bufs + sl * kXS;
+#pragma unroll 4
+        for (int i = tid / NS; i < a.n_out; i += NT / NS) dst[(size_t)i * P] = src[i];
+      }
+    } else if constexpr (MODE == 1) {
+      float* dst = static_cast<float*>(out_) + (size_t)base * a.n_out;
+      for (int i = tid; i < a.n_out; i += NT) {
+        float r[NS];
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i].x;
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl)
+          if (sl < nj) dst[(size_t)sl * a.n_out + i] = r[sl];
+      }
+    } else if constexpr (MODE == 2) {
+      // Z[k] sits at index k + V - 1; the two series split by conjugate symmetry
+      const int q = tid & (2 * NS - 1);
+      const long s = 2 * base + q;
+      if (q < 2 * nj && s < P) {
+        float2* dst = static_cast<float2*>(out_) + s;
+        const float2* src = bufs + (q >> 1) * kXS + (a.V - 1);
+#pragma unroll 4
+        for (int k = tid / (2 * NS); k < a.V; k += NT / (2 * NS)) {
+          const float2 zp = src[k], zm = cconj(src[-k]);
+          dst[(size_t)k * P] = (q & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
+        }
+      }
+    } else {
+      float* dst = static_cast<float*>(out_) + (size_t)(2 * base) * a.n_out;
+      const long ns = min(P - 2 * base, 2L * nj);  // series of this round
+      for (int i = tid; i < a.n_out; i += NT) {
+        float2 r[NS];
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i];
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) {
+          if (2 * sl < ns) dst[(size_t)(2 * sl) * a.n_out + i] = r[sl].x;
+          if (2 * sl + 1 < ns) dst[(size_t)(2 * sl + 1) * a.n_out + i] = r[sl].y;
+        }
+      }
+    }
+  }
+}
+
 int g_cu_count[64];
 
 int device_cus() {
@@ -404,6 +670,34 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   });
 }
 
+template <int MODE>
+bl_status_t launch_1k(const BlueGeom& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+  constexpr int M = 1024;
+  const size_t lds = (size_t)(2 * kWaves1k * kXS + a.n_in + a.n_out + 2 * M) * sizeof(float2);
+  static bool attr_set[4] = {false, false, false, false};
+  if (!attr_set[MODE]) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess)
+      return BL_ERR_HIP;
+    attr_set[MODE] = true;
+  }
+  if (lds > 160 * 1024) return BL_ERR_UNSUPPORTED;
+  const long jobs = (MODE >= 2) ? (a.P + 1) / 2 : a.P;
+  // contiguous job ranges per block: one block per CU at most, in multiples of
+  // the 16 jobs a block runs at a time when there are enough, else spread
+  // over more blocks in pairs (one wave each), as a round costs the same time
+  // however few of its slots are busy
+  long per = (jobs + device_cus() - 1) / device_cus();
+  per = per >= 16 ? (per + 15) / 16 * 16 : (per + 1) / 2 * 2;
+  const long blocks = (jobs + per - 1) / per;
+  const double ffts = (double)jobs;
+  const double flops = ffts * 2.0 * 5.0 * M * 10.0;
+  return timed_launch(name, bytes, flops, s, [&] {
+    hipLaunchKernelGGL((k_bluestein1k<MODE>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, in, out, a,
+                       per);
+  });
+}
+
 int fft_size_for(int need) {
   int M = 256;
   while (M < need) M *= 2;
@@ -415,7 +709,7 @@ bl_status_t launch_mode(BlueArgs& a, int M, const void* in, void* out, const cha
                         hipStream_t s) {
   if (M == 256) return launch_m<256, MODE>(a, in, out, name, bytes, s);
   if (M == 512) return launch_m<512, MODE>(a, in, out, name, bytes, s);
-  if (M == 1024) return launch_m<1024, MODE>(a, in, out, name, bytes, s);
+  if (M == 1024) return launch_1k<MODE>(a, in, out, name, bytes, s);
   return BL_ERR_UNSUPPORTED;
 }
 
