@@ -9,12 +9,15 @@
 // in LDS; the real [M x 2N] result is the interleaved complex O.  Each
 // v_mfma_f32_32x32x2f32 step consumes one complex k.
 //
-// Block tile: BM rows x 64 complex columns, 8 complex k per stage, LDS double
-// buffered with the next stage's global loads (16-byte vectors, two complex
-// values each) in flight during the current stage's MFMAs.  4 waves in a 2x2
-// grid; a wave owns BM/2 rows x 32 complex columns.  Operands are staged in
-// LDS as separate real and imaginary planes, k-major, so that each MFMA
-// operand fetch is one conflict-free 32-bit LDS read per lane.
+// Block tile: BM rows x BN complex columns, 16 complex k per stage.  Global
+// loads (16-byte vectors, two complex values each) run two stages ahead of
+// the MFMAs through two register sets, and LDS is double buffered.  4 waves
+// in a 2x2 grid; a wave owns BM/2 rows x BN/2 complex columns.  Operands are
+// staged in LDS as separate real and imaginary planes, k-major, with rows
+// padded by 4 floats and planes offset by half the banks, so that the MFMA
+// operand fetches (one 32-bit read per lane) and the stores are free of bank
+// conflicts.  Blocks are numbered so that consecutive tiles (which share
+// operand rows) run on the same XCD and its L2.
 #include <algorithm>
 
 #include "common.hpp"
@@ -30,33 +33,46 @@ struct CgemmArgs {
   unsigned ldo;
   unsigned long long bA, bB, bO;  // per-bin strides
   unsigned long long split_stride;  // complex elements between the partial outputs of two k-splits
-  int tiles_n;
+  int tiles_n, tiles;               // tiles per bin along n, and per bin in all
   int kper;                         // complex k per split (multiple of the stage depth)
 };
 
-constexpr int kBN = 64;  // complex columns per block
 constexpr int kBK = 16;  // complex k per stage
 
-template <int BM, bool A_KC, bool B_NC, bool CONJ>
+// LDS plane of R rows of W floats: padded rows, plane size = 32 (mod 64) floats.
+template <int W>
+constexpr int plane_floats() {
+  return ((kBK * (W + 4) + 63) / 64) * 64 + 32;
+}
+
+template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ>
 __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
                                                float2* __restrict__ O, CgemmArgs g) {
   constexpr int WM = BM / 2;   // rows per wave
+  constexpr int WN = BN / 2;   // complex columns per wave
   constexpr int MI = WM / 32;  // 32-row MFMA blocks per wave
-  constexpr int NJ = 2;        // 16-complex-column MFMA blocks per wave
+  constexpr int NJ = WN / 16;  // 16-complex-column MFMA blocks per wave
   constexpr int AV = BM / 32;  // 16-byte A loads per thread per stage
-  constexpr int BV = 2;        // 16-byte B loads per thread per stage
-  __shared__ float As[2][2][kBK][BM];
-  __shared__ float Bs[2][2][kBK][kBN];
+  constexpr int BV = BN / 32;  // 16-byte B loads per thread per stage
+  constexpr int SA = BM + 4, SB = BN + 4;  // padded row lengths
+  constexpr int PA = plane_floats<BM>(), PB = plane_floats<BN>();
+  __shared__ float As[2][2 * PA];
+  __shared__ float Bs[2][2 * PB];
 
-  const int bin = blockIdx.y;
+  // XCD-aware numbering: the hardware deals blocks to the 8 XCDs in turn
+  const unsigned nb = gridDim.x * gridDim.y;
+  unsigned id = blockIdx.x + blockIdx.y * gridDim.x;
+  if (nb % 8 == 0) id = (id % 8) * (nb / 8) + id / 8;
+  const int bin = id / g.tiles;
+  const int tile = id - bin * g.tiles;
   const int kbeg = blockIdx.z * g.kper;
   const int kend = min(g.K, kbeg + g.kper);
-  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x - (blockIdx.x / g.tiles_n) * g.tiles_n;
-  const int m0 = tm * BM, n0 = tn * kBN;
+  const int tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
   const float2* Ab = A + bin * g.bA;
   const float2* Bb = Bm + bin * g.bB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * WM, wn = (wave & 1) * 32;
+  const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
 
   // B operand of this lane: real column jcol = lane % 32 of a 32-wide block is
   // complex column jcol / 2, part jcol % 2; real k row a_part = lane / 32.
@@ -76,10 +92,8 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  float4 ra[AV], rb[BV];
   const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
-
-  auto load = [&](int k0) {
+  auto load = [&](int k0, float4* ra, float4* rb) {
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
       const int e = tid + 256 * q;
@@ -94,57 +108,56 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
     for (int q = 0; q < BV; ++q) {
       const int e = tid + 256 * q;
       int k, n;
-      if (B_NC) { k = e >> 5; n = (e & 31) * 2; }
+      if (B_NC) { k = e / (BN / 2); n = (e - k * (BN / 2)) * 2; }
       else { n = e >> 3; k = (e & 7) * 2; }
       rb[q] = zero4;
       if ((n0 + n < g.N) && (k0 + k < kend))
         rb[q] = *reinterpret_cast<const float4*>(Bb + (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const float4* ra, const float4* rb) {
+    float* a0 = As[buf];
+    float* a1 = As[buf] + PA;
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
       const int e = tid + 256 * q;
       if (A_KC) {
         const int m = e >> 3, k = (e & 7) * 2;
-        As[buf][0][k][m] = ra[q].x; As[buf][1][k][m] = ra[q].y;
-        As[buf][0][k + 1][m] = ra[q].z; As[buf][1][k + 1][m] = ra[q].w;
+        a0[k * SA + m] = ra[q].x; a1[k * SA + m] = ra[q].y;
+        a0[(k + 1) * SA + m] = ra[q].z; a1[(k + 1) * SA + m] = ra[q].w;
       } else {
         const int k = e / (BM / 2), m = (e - k * (BM / 2)) * 2;
-        As[buf][0][k][m] = ra[q].x; As[buf][1][k][m] = ra[q].y;
-        As[buf][0][k][m + 1] = ra[q].z; As[buf][1][k][m + 1] = ra[q].w;
+        *reinterpret_cast<float2*>(a0 + k * SA + m) = make_float2(ra[q].x, ra[q].z);
+        *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(ra[q].y, ra[q].w);
       }
     }
+    float* b0 = Bs[buf];
+    float* b1 = Bs[buf] + PB;
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
       const int e = tid + 256 * q;
       if (B_NC) {
-        const int k = e >> 5, n = (e & 31) * 2;
-        Bs[buf][0][k][n] = rb[q].x; Bs[buf][1][k][n] = rb[q].y;
-        Bs[buf][0][k][n + 1] = rb[q].z; Bs[buf][1][k][n + 1] = rb[q].w;
+        const int k = e / (BN / 2), n = (e - k * (BN / 2)) * 2;
+        *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(rb[q].x, rb[q].z);
+        *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(rb[q].y, rb[q].w);
       } else {
         const int n = e >> 3, k = (e & 7) * 2;
-        Bs[buf][0][k][n] = rb[q].x; Bs[buf][1][k][n] = rb[q].y;
-        Bs[buf][0][k + 1][n] = rb[q].z; Bs[buf][1][k + 1][n] = rb[q].w;
+        b0[k * SB + n] = rb[q].x; b1[k * SB + n] = rb[q].y;
+        b0[(k + 1) * SB + n] = rb[q].z; b1[(k + 1) * SB + n] = rb[q].w;
       }
     }
   };
-
-  const int nst = (kend - kbeg + kBK - 1) / kBK;
-  load(kbeg);
-  store(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int cur = st & 1;
-    if (st + 1 < nst) load(kbeg + (st + 1) * kBK);
+  auto compute = [&](int buf) {
     // all fragments of the stage first, so the LDS reads overlap the MFMAs
+    const float* ap = As[buf] + a_part * PA + wm + jcol;
+    const float* bp = Bs[buf] + b_src * PB + wn + (jcol >> 1);
     float av[kBK][MI], bv[kBK][NJ];
 #pragma unroll
     for (int s = 0; s < kBK; ++s) {
 #pragma unroll
-      for (int i = 0; i < MI; ++i) av[s][i] = As[cur][a_part][s][wm + 32 * i + jcol];
+      for (int i = 0; i < MI; ++i) av[s][i] = ap[s * SA + 32 * i];
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) bv[s][j] = Bs[cur][b_src][s][wn + 16 * j + (jcol >> 1)];
+      for (int j = 0; j < NJ; ++j) bv[s][j] = bp[s * SB + 16 * j];
     }
 #pragma unroll
     for (int s = 0; s < kBK; ++s)
@@ -153,8 +166,27 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[s][i], b_sign * bv[s][j], acc[i][j], 0, 0, 0);
-    if (st + 1 < nst) store(cur ^ 1);
-    __syncthreads();
+  };
+
+  // stage st sits in LDS buffer st % 2; register set st % 2 receives stage
+  // st + 2 while stage st + 1 (in the other set) waits to be stored
+  const int nst = (kend - kbeg + kBK - 1) / kBK;
+  float4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
+  load(kbeg, ra0, rb0);
+  if (nst > 1) load(kbeg + kBK, ra1, rb1);
+  store(0, ra0, rb0);
+  __syncthreads();
+  for (int st = 0; st < nst; st += 2) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int cs = st + h;
+      if (cs < nst) {
+        if (cs + 2 < nst) load(kbeg + (cs + 2) * kBK, h ? ra1 : ra0, h ? rb1 : rb0);
+        compute(h);
+        if (cs + 1 < nst) store(h ^ 1, h ? ra0 : ra1, h ? rb0 : rb1);
+      }
+      __syncthreads();
+    }
   }
 
   // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
@@ -219,10 +251,10 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   const bool b_ok = (g.bB % 2 == 0) && (b_nc ? (g.sBk % 2 == 0 && g.N % 2 == 0) : (g.sBn % 2 == 0 && g.K % 2 == 0));
   if (!a_ok || !b_ok || B > 65535) return BL_ERR_UNSUPPORTED;
   const BlContractTiling& t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
-  const bool big = t.bm == 128;
-  const int BM = t.bm;
+  const int BM = t.bm, BN = t.bn;
   const int tiles_m = (g.M + BM - 1) / BM;
-  g.tiles_n = (g.N + kBN - 1) / kBN;
+  g.tiles_n = (g.N + BN - 1) / BN;
+  g.tiles = tiles_m * g.tiles_n;
   const unsigned long long total = B * (unsigned long long)g.M * g.N;  // complex outputs
   int splits = t.splits;
   g.kper = (g.K + splits - 1) / splits;
@@ -231,23 +263,30 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   if (total % 2 != 0) splits = 1, g.kper = g.K;  // the reduction works on pairs
   g.split_stride = total;
   float2* dst = splits > 1 ? part : O;
-  dim3 grid((unsigned)(tiles_m * g.tiles_n), (unsigned)B, (unsigned)splits);
+  // (tile, bin) pairs as a 2-D grid; the kernel renumbers them per XCD
+  dim3 grid((unsigned)g.tiles, (unsigned)B, (unsigned)splits);
   const double flops = 8.0 * B * g.M * g.N * g.K;
   const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
   const char* name = which == Contract::Forward ? "contract_fwd"
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
-  bl_status_t st;
-#define BL_GO(BMV, AK, BN_, CJ)                                                                    \
+  bl_status_t st = BL_ERR_UNSUPPORTED;
+#define BL_GO(BMV, BNV, AK, BN_, CJ)                                                               \
   st = timed_launch(name, bytes, flops, s, [&] {                                                   \
-    hipLaunchKernelGGL((k_cgemm<BMV, AK, BN_, CJ>), grid, dim3(256), 0, s, A, Bm, dst, g);          \
+    hipLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ>), grid, dim3(256), 0, s, A, Bm, dst, g);     \
   })
+#define BL_SHAPES(AK, BN_, CJ)                       \
+  if (BM == 128 && BN == 64) BL_GO(128, 64, AK, BN_, CJ); \
+  else if (BM == 64 && BN == 64) BL_GO(64, 64, AK, BN_, CJ); \
+  else if (BM == 128 && BN == 32) BL_GO(128, 32, AK, BN_, CJ); \
+  else if (BM == 64 && BN == 32) BL_GO(64, 32, AK, BN_, CJ);
   if (which == Contract::Forward) {
-    if (big) BL_GO(128, true, true, true); else BL_GO(64, true, true, true);
+    BL_SHAPES(true, true, true)
   } else if (which == Contract::GradInput) {
-    if (big) BL_GO(128, true, false, false); else BL_GO(64, true, false, false);
+    BL_SHAPES(true, false, false)
   } else {
-    if (big) BL_GO(128, false, true, true); else BL_GO(64, false, true, true);
+    BL_SHAPES(false, true, true)
   }
+#undef BL_SHAPES
 #undef BL_GO
   if (st != BL_OK || splits == 1) return st;
   const unsigned long long n4 = total / 2;

@@ -6,6 +6,7 @@
 // kernels reduce to the 1-D transform, so one set of kernels serves both.
 #pragma once
 
+#include <cmath>
 #include <cstddef>
 #include <cstdint>
 #include <vector>
@@ -13,24 +14,41 @@
 #include "../../include/blconv.h"
 
 // Tiling of the per-bin contraction [M x K] . [K x N] (complex) over `bins`
-// bins: tile height (64 or 128 rows, 64 complex columns) and the number of
-// k-splits: 64-row tiles when 128-row ones give fewer than ~512 work items
-// (2 per CU of an MI355X), and k-splits while there are still fewer than ~512,
-// each split keeping at least 64 complex k (the pass that sums the split
-// partials only pays off when the splits are long).  Split partial tiles
-// are summed in a fixed order by a separate pass (deterministic results).
+// bins: tile height bm (64 or 128 rows), tile width bn (32 or 64 complex
+// columns) and the number of k-splits.  Each candidate is priced by a model
+// of a 256-CU part: a CU runs its share of the tiles one after another on its
+// matrix cores (the busiest CU sets the time), every tile pays a fixed start
+// (operand latency before the first MFMA), and k-splits add a pass that sums
+// the partial tiles in a fixed order (deterministic results) at HBM speed.
 struct BlContractTiling {
-  int bm, splits;
+  int bm, bn, splits;
 };
 inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
-  BlContractTiling t{M > 64 ? 128 : 64, 1};
-  const long tiles = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
-  if (tiles < 512 && t.bm == 128) {
-    t.bm = 64;
+  // constants fitted to measured launches of the tiles on an MI355X: the
+  // matrix cores reach about 60% (1 or 4 MFMA chains per wave) or 50%
+  // (2 chains) of their rate inside a tile
+  const double kCUs = 256, kClock = 2.4e9, kStart = 0.3e-6, kHbm = 5.0e12, kPass = 4e-6;
+  BlContractTiling best{64, 64, 1};
+  double best_t = 1e30;
+  const int shapes[4][2] = {{128, 64}, {64, 64}, {128, 32}, {64, 32}};
+  for (const auto& sh : shapes) {
+    const int bm = sh[0], bn = sh[1];
+    if (bm == 128 && M <= 64) continue;
+    if (bn == 64 && N <= 32) continue;
+    for (int splits = 1; splits <= 16; splits *= 2) {
+      const long kper = ((K + splits - 1) / splits + 15) / 16 * 16;
+      if (splits > 1 && kper < 64) break;
+      const long tiles = bins * ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * splits;
+      const double per_cu = std::ceil(tiles / kCUs);
+      // one wave per SIMD per tile: (bm/64)(bn/32) MFMAs of 64 cycles per complex k
+      const int chains = (bm / 64) * (bn / 32);
+      const double mfma = chains * 64.0 * kper / kClock / (chains == 2 ? 0.5 : 0.6);
+      double t = per_cu * (mfma + kStart);
+      if (splits > 1) t += kPass + 8.0 * bins * M * N * (splits + 1) / kHbm;
+      if (t < best_t * 0.98) best_t = t, best = BlContractTiling{bm, bn, splits};
+    }
   }
-  const long tiles2 = bins * ((M + t.bm - 1) / t.bm) * ((N + 63) / 64);
-  while (tiles2 * t.splits < 512 && K / (2 * t.splits) >= 64 && t.splits < 16) t.splits *= 2;
-  return t;
+  return best;
 }
 
 struct bl_conv_plan_s {
