@@ -395,7 +395,7 @@ __device__ __forceinline__ float2 expmpi(double num, double den) {
   return make_float2((float)cs, (float)sn);
 }
 
-template <int MODE>
+template <int MODE, bool PREF>
 __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
                                                                BlueGeom a, long jobs_per_block) {
   constexpr int M = 1024;
@@ -458,9 +458,114 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     RegFft<32>::run(v);
   };
 
-  // spectrum of the chirp filter, in place, by wave 0 (lane h only touches
-  // the elements h + 32 j; the chirp seeds in its transpose buffers are no
-  // longer needed)
+
+  // Jobs go 16 at a time (one per slot).  Series data moves between HBM and
+  // the slot buffers cooperatively, so that every bin row of a bin-major
+  // spectrum is read or written as 16 (or 32 paired) consecutive series, and
+  // the slots run their transforms on LDS-resident data.  When a round's
+  // inputs fit in 32 floats per thread (PREF), the next round's are loaded
+  // into registers while the current round's transforms run.  Loads use
+  // clamped indices instead of branches so that all of a thread's loads are
+  // in flight together.
+  const float* xin = static_cast<const float*>(in_);
+  const float2* yin = static_cast<const float2*>(in_);
+  const long P = a.P;
+  const long jobs = PACK ? (P + 1) / 2 : P;
+  const long j0 = blockIdx.x * jobs_per_block;
+  const long j1 = min(jobs, j0 + jobs_per_block);
+  constexpr int NS = 2 * kWaves1k;  // slots per block
+  constexpr int NT = 64 * kWaves1k;
+  // a round's inputs pass through registers in chunks of 32 floats per thread
+  constexpr int PER = MODE == 0 ? NS : MODE == 2 ? 2 * NS : MODE == 1 ? 2 : 4;  // floats per index
+  constexpr int IPC = 32 / PER;  // indices per chunk
+  const int nch = MODE == 0 || MODE == 2 ? ((a.n_in + NT - 1) / NT + IPC - 1) / IPC
+                  : MODE == 1 ? ((a.n_in + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC
+                              : ((a.V + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC;
+  float pf[32];
+  auto prefetch = [&](long base, int c) {
+    if constexpr (MODE == 0 || MODE == 2) {
+#pragma unroll
+      for (int r = 0; r < IPC; ++r) {
+        const int n = min(tid + NT * (c * IPC + r), a.n_in - 1);
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) {
+          const long job = min(base + sl, j1 - 1);
+          if constexpr (MODE == 0) {
+            pf[r * PER + sl] = xin[(size_t)job * a.n_in + n];
+          } else {
+            const long s1 = 2 * job;
+            const long s2 = min(s1 + 1, P - 1);
+            pf[r * PER + 2 * sl] = xin[(size_t)s1 * a.n_in + n];
+            pf[r * PER + 2 * sl + 1] = s2 == s1 ? 0.f : xin[(size_t)s2 * a.n_in + n];
+          }
+        }
+      }
+    } else {
+      const long job = min(base + (tid & (NS - 1)), j1 - 1);
+      const int rows = MODE == 1 ? a.n_in : a.V;
+#pragma unroll
+      for (int u = 0; u < IPC; ++u) {
+        const int n = min(tid / NS + (NT / NS) * (c * IPC + u), rows - 1);
+        if constexpr (MODE == 1) {
+          const float2 y = yin[(size_t)n * P + job];
+          pf[PER * u] = y.x;
+          pf[PER * u + 1] = y.y;
+        } else {
+          const long s1 = 2 * job;
+          const long s2 = min(s1 + 1, P - 1);
+          const float2 y1 = yin[(size_t)n * P + s1];
+          const float2 y2 = s2 == s1 ? make_float2(0.f, 0.f) : yin[(size_t)n * P + s2];
+          pf[PER * u] = y1.x;
+          pf[PER * u + 1] = y1.y;
+          pf[PER * u + 2] = y2.x;
+          pf[PER * u + 3] = y2.y;
+        }
+      }
+    }
+  };
+  // registers -> slot buffers, times the pre-chirp
+  auto commit = [&](int c) {
+    if constexpr (MODE == 0 || MODE == 2) {
+#pragma unroll
+      for (int r = 0; r < IPC; ++r) {
+        const int n = tid + NT * (c * IPC + r);
+        if (n < a.n_in) {
+          const float2 pn = pre[n];
+#pragma unroll
+          for (int sl = 0; sl < NS; ++sl)
+            bufs[sl * kXS + n] = MODE == 0 ? cscale(pn, pf[r * PER + sl])
+                                           : cmul(make_float2(pf[r * PER + 2 * sl], pf[r * PER + 2 * sl + 1]), pn);
+        }
+      }
+    } else {
+      float2* dst = bufs + (tid & (NS - 1)) * kXS;
+#pragma unroll
+      for (int u = 0; u < IPC; ++u) {
+        const int n = tid / NS + (NT / NS) * (c * IPC + u);
+        if constexpr (MODE == 1) {
+          if (n < a.n_in) dst[n] = cmul(make_float2(pf[PER * u], pf[PER * u + 1]), pre[n]);
+        } else if (n < a.V) {
+          // two Hermitian spectra packed into one series: Z[k] = Y1[k] + i Y2[k]
+          // at index k + V - 1 for |k| < V, with Y[-k] = conj(Y[k])
+          const float2 y1 = make_float2(pf[PER * u], pf[PER * u + 1]);
+          const float2 y2 = make_float2(pf[PER * u + 2], pf[PER * u + 3]);
+          const int ip = a.V - 1 + n, im = a.V - 1 - n;
+          if (n == 0) {
+            dst[ip] = cmul(make_float2(y1.x, y2.x), pre[ip]);
+          } else {
+            dst[ip] = cmul(make_float2(y1.x - y2.y, y1.y + y2.x), pre[ip]);
+            dst[im] = cmul(make_float2(y1.x + y2.y, y2.x - y1.y), pre[im]);
+          }
+        }
+      }
+    }
+  };
+
+  // the first round's loads go out before the set-up's last step: the
+  // spectrum of the chirp filter, computed in place by wave 0 (lane h only
+  // touches the elements h + 32 j; the chirp seeds in its transpose buffers
+  // are no longer needed)
+  if (PREF && j0 < j1) prefetch(j0, 0);
   __syncthreads();
   if (wave == 0) {
     float2 v[32];
@@ -473,88 +578,18 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     }
   }
   __syncthreads();
-
-  // Jobs go 16 at a time (one per slot).  Series data moves between HBM and
-  // the slot buffers cooperatively, so that every bin row of a bin-major
-  // spectrum is read or written as 16 (or 32 paired) consecutive series, and
-  // the slots run their transforms on LDS-resident data.
-  const float* xin = static_cast<const float*>(in_);
-  const float2* yin = static_cast<const float2*>(in_);
-  const long P = a.P;
-  const long jobs = PACK ? (P + 1) / 2 : P;
-  const long j0 = blockIdx.x * jobs_per_block;
-  const long j1 = min(jobs, j0 + jobs_per_block);
-  constexpr int NS = 2 * kWaves1k;  // slots per block
-  constexpr int NT = 64 * kWaves1k;
   for (long base = j0; base < j1; base += NS) {
     const int nj = (int)min((long)NS, j1 - base);  // jobs this round
-    __syncthreads();
-    // Loads are issued in batches (indices clamped into range instead of
-    // branched on) so that a thread has many in flight before it waits.
-    if constexpr (MODE == 0 || MODE == 2) {
-      for (int n = tid; n < a.n_in; n += NT) {
-        float x1[NS], x2[NS];
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl) {
-          const long job = min(base + sl, j1 - 1);
-          if constexpr (MODE == 0) {
-            x1[sl] = xin[(size_t)job * a.n_in + n];
-          } else {
-            const long s1 = 2 * job;
-            const long s2 = min(s1 + 1, P - 1);
-            x1[sl] = xin[(size_t)s1 * a.n_in + n];
-            x2[sl] = xin[(size_t)s2 * a.n_in + n];
-            if (s2 == s1) x2[sl] = 0.f;
-          }
-        }
-        const float2 pn = pre[n];
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl)
-          bufs[sl * kXS + n] = MODE == 0 ? cscale(pn, x1[sl]) : cmul(make_float2(x1[sl], x2[sl]), pn);
-      }
+    if constexpr (PREF) {
+      commit(0);
     } else {
-      constexpr int RB = 8;  // rows per batch
-      const int sl = tid & (NS - 1);
-      const long job = min(base + sl, j1 - 1);
-      float2* dst = bufs + sl * kXS;
-      for (int n0 = tid / NS; n0 < a.n_in; n0 += RB * (NT / NS)) {
-        float2 y1[RB], y2[RB];
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          const int n = min(n0 + u * (NT / NS), a.n_in - 1);
-          if constexpr (MODE == 1) {
-            y1[u] = yin[(size_t)n * P + job];
-          } else {
-            // two Hermitian spectra packed into one series: Z[k] = Y1[k] + i Y2[k]
-            // for k = n - (V - 1) in (-V, V), with Y[-k] = conj(Y[k])
-            const int k = n - (a.V - 1);
-            const int kk = k < 0 ? -k : k;
-            const long s1 = 2 * job;
-            const long s2 = min(s1 + 1, P - 1);
-            y1[u] = yin[(size_t)kk * P + s1];
-            y2[u] = yin[(size_t)kk * P + s2];
-            if (s2 == s1) y2[u] = make_float2(0.f, 0.f);
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          const int n = n0 + u * (NT / NS);
-          if (n < a.n_in) {
-            float2 x;
-            if constexpr (MODE == 1) {
-              x = y1[u];
-            } else {
-              const int k = n - (a.V - 1);
-              if (k > 0) x = make_float2(y1[u].x - y2[u].y, y1[u].y + y2[u].x);
-              else if (k < 0) x = make_float2(y1[u].x + y2[u].y, y2[u].x - y1[u].y);
-              else x = make_float2(y1[u].x, y2[u].x);
-            }
-            dst[n] = cmul(x, pre[n]);
-          }
-        }
+      for (int c = 0; c < nch; ++c) {
+        prefetch(base, c);
+        commit(c);
       }
     }
     __syncthreads();
+    if (PREF && base + NS < j1) prefetch(base + NS, 0);
     if (2 * wave < nj) {  // waves with no job this round skip the transforms
       float2 v[32];
 #pragma unroll
@@ -620,6 +655,7 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
         }
       }
     }
+    __syncthreads();  // slot buffers free for the next round
   }
 }
 
@@ -670,18 +706,19 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   });
 }
 
-template <int MODE>
-bl_status_t launch_1k(const BlueGeom& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+template <int MODE, bool PREF>
+bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const char* name, double bytes,
+                          hipStream_t s) {
   constexpr int M = 1024;
   const size_t lds = (size_t)(2 * kWaves1k * kXS + a.n_in + a.n_out + 2 * M) * sizeof(float2);
-  static bool attr_set[4] = {false, false, false, false};
-  if (!attr_set[MODE]) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE>),
+  if (lds > 160 * 1024) return BL_ERR_UNSUPPORTED;
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, PREF>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess)
       return BL_ERR_HIP;
-    attr_set[MODE] = true;
+    attr_set = true;
   }
-  if (lds > 160 * 1024) return BL_ERR_UNSUPPORTED;
   const long jobs = (MODE >= 2) ? (a.P + 1) / 2 : a.P;
   // contiguous job ranges per block: one block per CU at most, in multiples of
   // the 16 jobs a block runs at a time when there are enough, else spread
@@ -693,9 +730,20 @@ bl_status_t launch_1k(const BlueGeom& a, const void* in, void* out, const char* 
   const double ffts = (double)jobs;
   const double flops = ffts * 2.0 * 5.0 * M * 10.0;
   return timed_launch(name, bytes, flops, s, [&] {
-    hipLaunchKernelGGL((k_bluestein1k<MODE>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, in, out, a,
-                       per);
+    hipLaunchKernelGGL((k_bluestein1k<MODE, PREF>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, in, out,
+                       a, per);
   });
+}
+
+// Rounds are prefetched when one round's inputs fit in 32 floats per thread.
+template <int MODE>
+bl_status_t launch_1k(const BlueGeom& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+  const int need = MODE == 0 ? 16 * ((a.n_in + 511) / 512)
+                   : MODE == 2 ? 32 * ((a.n_in + 511) / 512)
+                   : MODE == 1 ? 2 * ((a.n_in + 31) / 32)
+                               : 4 * ((a.V + 31) / 32);
+  if (need <= 32) return launch_1k_cap<MODE, true>(a, in, out, name, bytes, s);
+  return launch_1k_cap<MODE, false>(a, in, out, name, bytes, s);
 }
 
 int fft_size_for(int need) {

@@ -188,6 +188,26 @@ def test_1d_long_sequences(torch):
         assert max(errs) <= TOL
 
 
+def test_1d_many_series(torch):
+    """1-D layers with thousands of series, so that each block of the chirp-z
+    kernel runs several rounds of 16 jobs: inputs longer than 512 (rounds
+    staged in chunks) and shorter ones (next round loaded during the current
+    one), forward and inverse, paired and single series."""
+    cases = [
+        (synth.Layer("rounds_long", 1, 64, 160, 4, 600, 1, 3, (1, 1), "walk"), 0.5),
+        (synth.Layer("rounds_short", 1, 64, 160, 4, 300, 1, 5, (2, 2), "walk"), 0.5),
+        (synth.Layer("rounds_single", 1, 40, 130, 3, 510, 1, 3, (1, 1), "walk"), 0.0),
+    ]
+    for i, (layer, c) in enumerate(cases):
+        say(f"[many series] {layer.name} c={c}")
+        x, w, dy = synth.random_inputs(layer, 1300 + i)
+        y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
+        ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        say(f"    rel err {errs}")
+        assert max(errs) <= TOL
+
+
 def test_2d_fast_grids(torch):
     """Grids 6, 10, 18, 34, 58 (2 x odd: the mixed-radix 2-D path) reached with
     other filter sizes, asymmetric padding, non-square inputs and grid
