@@ -216,9 +216,18 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
   const int B = g.R * g.V;
   const int b0 = blockIdx.y * g.bins_per_block;
   const int b1 = min(B, b0 + g.bins_per_block);
-  for (int bin = b0; bin < b1; ++bin) {
-    const int r = bin / g.V, v = bin % g.V;
+  // twiddle indices (u a) mod Lh and (v b) mod Lw, advanced bin by bin
+  int r = b0 / g.V, v = b0 - (b0 / g.V) * g.V;
+  int ih[KH], iw[KW];
+  auto row_start = [&]() {
     const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
+#pragma unroll
+    for (int a = 0; a < KH; ++a) ih[a] = (int)(((long)u * a) % g.Lh);
+  };
+  row_start();
+#pragma unroll
+  for (int b = 0; b < KW; ++b) iw[b] = (int)(((long)v * b) % g.Lw);
+  for (int bin = b0; bin < b1; ++bin) {
     float re = 0.f, im = 0.f;
 #pragma unroll
     for (int a = 0; a < KH; ++a) {
@@ -226,15 +235,28 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
       float rr = 0.f, ri = 0.f;
 #pragma unroll
       for (int b = 0; b < KW; ++b) {
-        const float2 t = tww[(v * b) % g.Lw];
+        const float2 t = tww[iw[b]];
         rr = fmaf(tap[a][b], t.x, rr);
         ri = fmaf(tap[a][b], t.y, ri);
       }
-      const float2 t = twh[(u * a) % g.Lh];
+      const float2 t = twh[ih[a]];
       re = fmaf(rr, t.x, fmaf(-ri, t.y, re));
       im = fmaf(rr, t.y, fmaf(ri, t.x, im));
     }
     out[(size_t)bin * CF + q] = make_float2(re, im);
+    if (++v == g.V) {
+      v = 0;
+      ++r;
+      row_start();
+#pragma unroll
+      for (int b = 0; b < KW; ++b) iw[b] = 0;
+    } else {
+#pragma unroll
+      for (int b = 0; b < KW; ++b) {
+        iw[b] += b;
+        if (iw[b] >= g.Lw) iw[b] -= g.Lw;
+      }
+    }
   }
 }
 
@@ -284,6 +306,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
   const float2* src = DW + (size_t)b0 * Q + q;
+#pragma unroll 8
   for (int bb = 0; bb < nb; ++bb) {
     const float2 d = src[(size_t)bb * Q];
     const float2* Eb = E + bb * g.T;
