@@ -160,7 +160,7 @@ def measured_traffic(kernel, workload):
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
         return None
-    t = json.load(open(path))
+    t = json.load(open(path)).get(kernel, {})
     src = os.path.join(ROOT, "paper_1911_09287_amd", "csrc", KERNEL_SOURCES[kernel])
     if t.get("kernel") != kernel or t.get("workload") != workload or not os.path.exists(src):
         return None

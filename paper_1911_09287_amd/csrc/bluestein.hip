@@ -701,8 +701,8 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
   const long groups = (a.P + kSeriesPerGroup - 1) / kSeriesPerGroup;
   const long blocks = std::min<long>(groups, 2L * device_cus());
-  return timed_launch(name, bytes, flops, s, [&] {
-    hipLaunchKernelGGL((k_bluestein<M, MODE>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, in, out, a);
+  return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL((k_bluestein<M, MODE>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, e0, e1, 0, in, out, a);
   });
 }
 
@@ -729,8 +729,8 @@ bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const ch
   const long blocks = (jobs + per - 1) / per;
   const double ffts = (double)jobs;
   const double flops = ffts * 2.0 * 5.0 * M * 10.0;
-  return timed_launch(name, bytes, flops, s, [&] {
-    hipLaunchKernelGGL((k_bluestein1k<MODE, PREF>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, in, out,
+  return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL((k_bluestein1k<MODE, PREF>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, e0, e1, 0, in, out,
                        a, per);
   });
 }

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include "plan.hpp"
 
@@ -18,13 +19,15 @@ hipEvent_t prof_event(int slot, int end);
 // Launch with optional event timing.  `bytes` and `flops` are the launch's
 // algorithmic HBM traffic (compulsory reads + writes) and arithmetic, reported
 // with the timing so that measurement tools can place it on a roofline.
+// The launch takes a start and a stop event (null when not profiling), which
+// hipExtLaunchKernelGGL stamps at the kernel's own start and end, so the
+// timing is the kernel's execution time without the gaps around it.
 template <typename Launch>
 bl_status_t timed_launch(const char* name, double bytes, double flops, hipStream_t s, Launch&& launch) {
   const int slot = prof_slot(name, bytes, flops);
-  if (slot >= 0 && hipEventRecord(prof_event(slot, 0), s) != hipSuccess) return BL_ERR_HIP;
-  launch();
+  (void)s;
+  launch(slot >= 0 ? prof_event(slot, 0) : nullptr, slot >= 0 ? prof_event(slot, 1) : nullptr);
   if (hipGetLastError() != hipSuccess) return BL_ERR_HIP;
-  if (slot >= 0 && hipEventRecord(prof_event(slot, 1), s) != hipSuccess) return BL_ERR_HIP;
   return BL_OK;
 }
 

@@ -271,8 +271,8 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
   bl_status_t st = BL_ERR_UNSUPPORTED;
 #define BL_GO(BMV, BNV, AK, BN_, CJ)                                                               \
-  st = timed_launch(name, bytes, flops, s, [&] {                                                   \
-    hipLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ>), grid, dim3(256), 0, s, A, Bm, dst, g);     \
+  st = timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                      \
+    hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g);     \
   })
 #define BL_SHAPES(AK, BN_, CJ)                       \
   if (BM == 128 && BN == 64) BL_GO(128, 64, AK, BN_, CJ); \
@@ -291,8 +291,8 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   if (st != BL_OK || splits == 1) return st;
   const unsigned long long n4 = total / 2;
   const unsigned long long blocks = (n4 + 255) / 256;
-  return timed_launch("contract_reduce", 8.0 * total * (splits + 1), 0.0, s, [&] {
-    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)blocks), dim3(256), 0, s,
+  return timed_launch("contract_reduce", 8.0 * total * (splits + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_split_reduce, dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0,
                        reinterpret_cast<const float4*>(part), reinterpret_cast<float4*>(O), n4, splits);
   });
 }

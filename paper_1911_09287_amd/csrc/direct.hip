@@ -472,8 +472,8 @@ bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, flo
   const size_t lds = fixed + g.TP * per;
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
-  return timed_launch("spec_fwd_direct", bytes, 0.0, s, [&] {
-    hipLaunchKernelGGL(k_spec_fwd, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
+  return timed_launch("spec_fwd_direct", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_spec_fwd, dim3((unsigned)blocks), dim3(kThreads), lds, s, e0, e1, 0, in, out, g);
   });
 }
 
@@ -487,8 +487,8 @@ bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, fl
   const size_t lds = fixed + g.TP * per;
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
-  return timed_launch("spec_inv_direct", bytes, 0.0, s, [&] {
-    hipLaunchKernelGGL(k_spec_inv, dim3((unsigned)blocks), dim3(kThreads), lds, s, in, out, g);
+  return timed_launch("spec_inv_direct", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_spec_inv, dim3((unsigned)blocks), dim3(kThreads), lds, s, e0, e1, 0, in, out, g);
   });
 }
 
@@ -510,8 +510,8 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* ou
   const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * 8;
 #define X(a, b)                                                                                 \
   if (p->Kh == a && p->Kw == b)                                                                 \
-    return timed_launch("spec_filt", bytes, 0.0, s, [&] {                                      \
-      hipLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, w, out, g);        \
+    return timed_launch("spec_filt", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {        \
+      hipExtLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, out, g);        \
     });
   BL_FILT_CASES(X)
 #undef X
@@ -532,8 +532,8 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
   bl_status_t st;
   auto go = [&](auto kern) {
-    return timed_launch("wgrad_idft", bytes, 0.0, s, [&] {
-      hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, DW, dw, part, g);
+    return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+      hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, dw, part, g);
     });
   };
   if (g.T <= 8) st = go(k_wgrad_idft<8>);
@@ -542,8 +542,8 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   else st = go(k_wgrad_idft<64>);
   if (st != BL_OK || g.chunks == 1) return st;
   const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
-  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&] {
-    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, part, dw, g);
+  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, e0, e1, 0, part, dw, g);
   });
 }
 
@@ -577,16 +577,16 @@ bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, con
   const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
   switch (which) {
     case Contract::Forward:
-      return timed_launch("contract_fwd", bytes, flops, s, [&] {
-        hipLaunchKernelGGL((k_contract<true, true, true>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      return timed_launch("contract_fwd", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+        hipExtLaunchKernelGGL((k_contract<true, true, true>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
       });
     case Contract::GradInput:
-      return timed_launch("contract_dgrad", bytes, flops, s, [&] {
-        hipLaunchKernelGGL((k_contract<true, false, false>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      return timed_launch("contract_dgrad", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+        hipExtLaunchKernelGGL((k_contract<true, false, false>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
       });
     case Contract::GradWeight:
-      return timed_launch("contract_wgrad", bytes, flops, s, [&] {
-        hipLaunchKernelGGL((k_contract<false, true, true>), grid, dim3(kThreads), 0, s, A, Bm, O, g);
+      return timed_launch("contract_wgrad", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+        hipExtLaunchKernelGGL((k_contract<false, true, true>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
       });
   }
   return BL_ERR_INVALID_ARG;

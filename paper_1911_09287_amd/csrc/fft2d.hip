@@ -343,8 +343,8 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, 
   // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
   // complex LH-point column FFTs (5 LH log2 LH) per plane
   const double flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
-  return timed_launch("spec_fwd_2d", bytes, flops, s, [&] {
-    hipLaunchKernelGGL((k_fft2_fwd<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
+  return timed_launch("spec_fwd_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0, e1, 0, in, out, g);
   });
 }
 
@@ -370,8 +370,8 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
   const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
-  return timed_launch("spec_inv_2d", bytes, flops, s, [&] {
-    hipLaunchKernelGGL((k_fft2_inv<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, in, out, g);
+  return timed_launch("spec_inv_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL((k_fft2_inv<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0, e1, 0, in, out, g);
   });
 }
 

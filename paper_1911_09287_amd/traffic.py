@@ -8,7 +8,8 @@ The copy's readings give the scale from counter kilobytes to bytes for reads
 and for writes; the kernel's average per-dispatch readings times those scales
 are its measured traffic.  The result is written as JSON together with a hash
 of the kernel's source file, so that a later run can tell whether the kernel
-has changed since the counters were taken.
+has changed since the counters were taken; the output file keeps one entry
+per kernel name.
 
     python -m paper_1911_09287_amd.traffic --fetch F.csv --write W.csv \\
         --kernel k_bluestein --match "<1024, 2>" --name spec_fwd_1d \\
@@ -74,8 +75,13 @@ def main():
            "read_scale": read_scale, "write_scale": write_scale,
            "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
            "traffic_bytes_per_launch": fetch + write}
+    # the file holds one entry per kernel name; other kernels' entries are kept
     os.makedirs(os.path.dirname(os.path.abspath(a.out)), exist_ok=True)
-    json.dump(out, open(a.out, "w"), indent=1)
+    table = json.load(open(a.out)) if os.path.exists(a.out) else {}
+    if "kernel" in table:  # a single-entry file
+        table = {table["kernel"]: table}
+    table[a.name] = out
+    json.dump(table, open(a.out, "w"), indent=1, sort_keys=True)
     print(json.dumps(out))
 
 
