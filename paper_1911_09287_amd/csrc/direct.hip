@@ -188,6 +188,13 @@ __global__ __launch_bounds__(kThreads) void k_spec_inv(const float2* __restrict_
 // spec_filt: w [F][C][Kh][Kw] -> W[b][c][f] at the kept bins (origin placement).
 // One thread per (c, f) pair; blockIdx.y strides over chunks of bins.
 // ---------------------------------------------------------------------------
+// Channel tile of the weight-gradient inverse DFT: TC input x 256 / TC output
+// channels.  Rows wider than 256 output channels take 32-channel spans of 8
+// input channels, so that the gradient rows dw[f][c0 .. c0 + 8][taps] are
+// written 8 x taps floats at a time; otherwise a block spans whole rows of
+// one input channel.
+inline int chan_tile(int taps, int F) { return (taps <= 16 && F > 256) ? 8 : 1; }
+
 struct FiltGeom {
   int F, C, Kh, Kw;
   int Lh, Lw, r_h, R, V;
@@ -266,9 +273,11 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
 //   E[b][t] = h_v e^{+2 pi i (u a / Lh + v b' / Lw)} / (Lh Lw)
 // (the c2r inverse restricted to the filter support).  The bins are split
 // into `chunks` slices (blockIdx.y); each block tabulates E for its slice in
-// LDS and every thread reduces one q over the slice.  With more than one
-// slice the partial sums go to part[chunk][t][q] and k_wgrad_reduce adds
-// them in a fixed order, so results do not depend on scheduling.
+// LDS and reduces a tile of TC x TF (c, f) pairs over it.  With more than one
+// slice the partial sums go to part[chunk][t][q] (contiguous in q) and
+// k_wgrad_reduce adds them in a fixed order, so results do not depend on
+// scheduling; with one slice and TC > 1 the results go through LDS so that
+// each row dw[f][c0 .. c0 + TC][:] is written contiguously.
 // ---------------------------------------------------------------------------
 struct WgradGeom {
   int F, C, Kh, Kw, T;
@@ -276,10 +285,12 @@ struct WgradGeom {
   int bins_per_chunk, chunks;
 };
 
-template <int TMAX>
+template <int TMAX, int TC>
 __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, float* __restrict__ dw,
                                                          float* __restrict__ part, WgradGeom g) {
+  constexpr int TF = kThreads / TC;
   extern __shared__ float2 E[];  // bins_per_chunk x T
+  __shared__ float res[TC > 1 ? TF * TC * TMAX : 1];
   const int B = g.R * g.V;
   const int b0 = blockIdx.y * g.bins_per_chunk;
   const int nb = min(g.bins_per_chunk, B - b0);
@@ -300,12 +311,15 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
   }
   __syncthreads();
   const long Q = (long)g.C * g.F;
-  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= Q) return;
+  const int tiles_f = (g.F + TF - 1) / TF;
+  const int c0 = (blockIdx.x / tiles_f) * TC, f0 = (blockIdx.x % tiles_f) * TF;
+  const int tc = threadIdx.x / TF, tf = threadIdx.x - (threadIdx.x / TF) * TF;
+  const int c = c0 + tc, f = f0 + tf;
+  const bool valid = c < g.C && f < g.F;
   float acc[TMAX];
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
-  const float2* src = DW + (size_t)b0 * Q + q;
+  const float2* src = DW + (size_t)b0 * Q + (valid ? (long)c * g.F + f : 0);
 #pragma unroll 8
   for (int bb = 0; bb < nb; ++bb) {
     const float2 d = src[(size_t)bb * Q];
@@ -314,16 +328,34 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
     for (int t = 0; t < TMAX; ++t)
       if (t < g.T) acc[t] = fmaf(d.x, Eb[t].x, fmaf(-d.y, Eb[t].y, acc[t]));
   }
-  if (g.chunks == 1) {
-    const int c = (int)(q / g.F), f = (int)(q % g.F);
-    float* o = dw + ((size_t)f * g.C + c) * g.T;
+  if (g.chunks > 1) {
+    if (valid) {
 #pragma unroll
-    for (int t = 0; t < TMAX; ++t)
-      if (t < g.T) o[t] = acc[t];
-  } else {
+      for (int t = 0; t < TMAX; ++t)
+        if (t < g.T) part[((size_t)blockIdx.y * g.T + t) * Q + (size_t)c * g.F + f] = acc[t];
+    }
+    return;
+  }
+  if (TC == 1) {
+    if (valid) {
+      float* o = dw + ((size_t)f * g.C + c) * g.T;
 #pragma unroll
-    for (int t = 0; t < TMAX; ++t)
-      if (t < g.T) part[((size_t)blockIdx.y * g.T + t) * Q + q] = acc[t];
+      for (int t = 0; t < TMAX; ++t)
+        if (t < g.T) o[t] = acc[t];
+    }
+    return;
+  }
+  // transpose through LDS: res[tf][tc][t], then each output row f gets its
+  // TC x T contiguous floats
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t)
+    if (t < g.T) res[(tf * TC + tc) * g.T + t] = acc[t];
+  __syncthreads();
+  const int seg = TC * g.T;
+  for (int e = threadIdx.x; e < TF * seg; e += kThreads) {
+    const int ef = e / seg, r = e - ef * seg;
+    const int oc = c0 + r / g.T, of = f0 + ef;
+    if (oc < g.C && of < g.F) dw[((size_t)of * g.C + c0) * g.T + r] = res[e];
   }
 }
 
@@ -527,8 +559,8 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   if (g.T > 64 || g.chunks > 65535) return BL_ERR_UNSUPPORTED;
   const size_t lds = (size_t)g.bins_per_chunk * g.T * sizeof(float2);
   if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
-  const long xblocks = (Q + kThreads - 1) / kThreads;
-  dim3 grid((unsigned)xblocks, (unsigned)g.chunks);
+  const int TC = chan_tile(g.T, p->Cout), TF = kThreads / TC;
+  dim3 grid((unsigned)((long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF)), (unsigned)g.chunks);
   const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
   bl_status_t st;
   auto go = [&](auto kern) {
@@ -536,10 +568,10 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
       hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, dw, part, g);
     });
   };
-  if (g.T <= 8) st = go(k_wgrad_idft<8>);
-  else if (g.T <= 16) st = go(k_wgrad_idft<16>);
-  else if (g.T <= 32) st = go(k_wgrad_idft<32>);
-  else st = go(k_wgrad_idft<64>);
+  if (g.T <= 8) st = TC == 8 ? go(k_wgrad_idft<8, 8>) : go(k_wgrad_idft<8, 1>);
+  else if (g.T <= 16) st = TC == 8 ? go(k_wgrad_idft<16, 8>) : go(k_wgrad_idft<16, 1>);
+  else if (g.T <= 32) st = go(k_wgrad_idft<32, 1>);
+  else st = go(k_wgrad_idft<64, 1>);
   if (st != BL_OK || g.chunks == 1) return st;
   const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
   return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
