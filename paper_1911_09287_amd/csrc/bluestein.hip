@@ -377,7 +377,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restric
 // or a pair of series in the paired modes) of its block's contiguous range.
 // ---------------------------------------------------------------------------
 constexpr int kWaves1k = 8;
-constexpr int kXS = 32 * 33;  // transpose buffer of one slot (complex)
+// Slot stride (complex): the 32 x 33 transpose tile plus 4 elements, so that
+// the same element of the 16 slots falls in different LDS banks when the
+// block moves series between HBM and the slots (one lane per slot).
+constexpr int kXS = 32 * 33 + 4;
 
 // c[m] = e^{-i pi m^2 / L} from seed tables held in LDS (see chirp()).
 template <bool INV>
