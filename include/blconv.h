@@ -45,18 +45,25 @@
  *   no dilation, no groups, no bias.
  *
  * Ownership: the caller owns every device buffer (x, w, y, dy, dx, dw and the
- * workspace ws).  A plan is host memory only; creating, querying and destroying
- * it makes no HIP call.  The compute calls allocate nothing, make no host
- * synchronisation and enqueue their kernels on `stream` (a hipStream_t, passed
- * as void*; NULL = the default stream).
+ * workspace ws).  Creating and querying a plan makes no HIP call.  The plan
+ * also owns small device tables of its 1-D transforms (chirps, the chirp
+ * filter's spectrum and twiddles: under 100 KB per device), built in double
+ * precision on the host and uploaded by the first 1-D compute call of the plan
+ * on each device; that first call allocates and copies synchronously, so make
+ * it outside stream capture.  Every other compute call allocates nothing,
+ * makes no host synchronisation and enqueues its kernels on `stream` (a
+ * hipStream_t, passed as void*; NULL = the default stream).
+ * bl_conv_plan_destroy frees the tables (no kernel of the plan may still be
+ * running).
  *
  * Errors: every call returns a bl_status_t.  Arguments are validated on the host
  * before anything is enqueued; a call that returns an error has enqueued no
  * kernel, except BL_ERR_HIP, which reports a failed launch (work enqueued before
  * it by the same call may have run).
  *
- * Threading: a plan is immutable after creation; calls with distinct
- * workspaces may run concurrently from several threads and streams.
+ * Threading: a plan's geometry is immutable after creation (the device tables
+ * are built under a lock); calls with distinct workspaces may run
+ * concurrently from several threads and streams.
  */
 #ifndef BLCONV_H
 #define BLCONV_H
@@ -73,7 +80,7 @@ typedef enum {
   BL_ERR_UNSUPPORTED = 2,         /* valid but outside what this library implements (e.g. K > 8) */
   BL_ERR_WORKSPACE_TOO_SMALL = 3, /* reserved for callers that check bl_conv_workspace_size */
   BL_ERR_HIP = 4,                 /* a HIP launch or runtime call failed */
-  BL_ERR_OOM = 5                  /* host allocation failed */
+  BL_ERR_OOM = 5                  /* host or device allocation failed */
 } bl_status_t;
 
 typedef struct {

@@ -23,6 +23,9 @@
 // computed once per block by all its threads.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
+#include <new>
+#include <vector>
 
 #include "common.hpp"
 
@@ -229,6 +232,7 @@ struct BlueGeom {
   int nyq;             // Nyquist bin (L even) or -1
   long P;              // number of series
   float out_scale;     // extra output scale (inverse: 1 / L)
+  const float2* tab;   // 1024-point kernel: [pre n_in][post n_out][F 1024][TW 1024]
 };
 struct BlueArgs : BlueGeom {
   float2 root_hi[16], root_lo[64];    // e^{-2 pi i k / M} = hi[k >> 6] * lo[k & 63]
@@ -382,22 +386,6 @@ constexpr int kWaves1k = 8;
 // block moves series between HBM and the slots (one lane per slot).
 constexpr int kXS = 32 * 33 + 4;
 
-// c[m] = e^{-i pi m^2 / L} from seed tables held in LDS (see chirp()).
-template <bool INV>
-__device__ __forceinline__ float2 chirp_lds(const float2* chi, const float2* clo, int L, int m) {
-  const unsigned mm = (unsigned)(m < 0 ? -m : m);
-  const int q = (int)((mm * mm) % (2u * (unsigned)L));
-  const float2 c = cmul(chi[q >> 6], clo[q & 63]);
-  return INV ? cconj(c) : c;
-}
-
-// e^{-i pi x} for x = num / den, evaluated in double precision.
-__device__ __forceinline__ float2 expmpi(double num, double den) {
-  double sn, cs;
-  sincospi(-num / den, &sn, &cs);
-  return make_float2((float)cs, (float)sn);
-}
-
 template <int MODE, bool PREF>
 __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
                                                                BlueGeom a, long jobs_per_block) {
@@ -409,40 +397,13 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
   float2* post = pre + a.n_in;                // n_out
   float2* F = post + a.n_out;                 // spectrum of the chirp filter (M)
   float2* TW = F + M;                         // TW[32 k + h] = w1024^{h k}
-  float2* chi = bufs;                         // chirp seeds, only during setup
-  float2* clo = bufs + 128;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int slot = lane >> 5, h = lane & 31;
   float2* xb = bufs + (wave * 2 + slot) * kXS;
 
-  // seeds of the chirp, e^{-i pi q / L} = chi[q >> 6] * clo[q & 63] for
-  // q < 2L <= 8192, and the twiddles, all computed here (the angles of TW are
-  // exact in single precision)
-  if (tid < 64) {
-    clo[tid] = expmpi(tid, a.L);
-  } else if (tid < 64 + 128) {
-    chi[tid - 64] = expmpi(64.0 * (tid - 64), a.L);
-  }
-  for (int i = tid; i < M; i += blockDim.x) {
-    const int e = ((i >> 5) * (i & 31)) & (M - 1);
-    float sn, cs;
-    sincospif(-(float)e / (M / 2), &sn, &cs);
-    TW[i] = make_float2(cs, sn);
-  }
-  __syncthreads();
-  for (int k = tid; k < a.n_in; k += blockDim.x) {
-    float2 c = chirp_lds<INV>(chi, clo, a.L, k + a.off_in);
-    if (INV && !PACK && k != 0 && k != a.nyq) c = cscale(c, 2.f);
-    pre[k] = c;
-  }
-  const float osc = a.out_scale / (float)M * (PACK && !INV ? 0.5f : 1.0f);
-  for (int k = tid; k < a.n_out; k += blockDim.x) post[k] = cscale(chirp_lds<INV>(chi, clo, a.L, k + a.off_out), osc);
-  for (int m = tid; m < M; m += blockDim.x) {
-    const int d = m < a.n_out ? m : m - M;
-    F[m] = (d >= -(a.n_in - 1)) ? cconj(chirp_lds<INV>(chi, clo, a.L, d + a.off_out - a.off_in))
-                                : make_float2(0.f, 0.f);
-  }
-  __syncthreads();
+  // the chirps, the filter's spectrum and the twiddles, built once per plan
+  // in double precision on the host, are laid out in the table as in LDS
+  for (int i = tid; i < a.n_in + a.n_out + 2 * M; i += blockDim.x) pre[i] = a.tab[i];
   auto exchange = [&](float2* v) {
 #pragma unroll
     for (int k = 0; k < 32; ++k) xb[k * 33 + h] = v[k];
@@ -564,23 +525,8 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     }
   };
 
-  // the first round's loads go out before the set-up's last step: the
-  // spectrum of the chirp filter, computed in place by wave 0 (lane h only
-  // touches the elements h + 32 j; the chirp seeds in its transpose buffers
-  // are no longer needed)
   if (PREF && j0 < j1) prefetch(j0, 0);
-  __syncthreads();
-  if (wave == 0) {
-    float2 v[32];
-#pragma unroll
-    for (int j = 0; j < 32; ++j) v[j] = F[h + 32 * j];
-    fft1k(v);
-    if (slot == 0) {
-#pragma unroll
-      for (int m = 0; m < 32; ++m) F[h + 32 * m] = v[m];
-    }
-  }
-  __syncthreads();
+  __syncthreads();  // tables in LDS
   for (long base = j0; base < j1; base += NS) {
     const int nj = (int)min((long)NS, j1 - base);  // jobs this round
     if constexpr (PREF) {
@@ -709,6 +655,105 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   });
 }
 
+// ---- tables of the 1024-point kernel, built on the host in double precision ----
+// For one transform geometry: pre[n] (n < n_in), post[k] (k < n_out), the
+// spectrum F of the chirp filter, and the twiddles TW[32 k + h] = w^{h k}, in
+// that order, as the kernel lays them out in LDS.
+void host_tables_1k(const BlueGeom& a, int mode, std::vector<float2>& out) {
+  constexpr int M = 1024;
+  const bool inv = mode & 1, pack = mode >= 2;
+  const double pi = 3.141592653589793238462643383279502884;
+  auto chirp = [&](long m, double& re, double& im) {  // e^{-i pi m^2 / L}, conjugated for the inverse
+    const long mm = m < 0 ? -m : m;
+    const long q = (mm * mm) % (2L * a.L);
+    re = std::cos(pi * (double)q / a.L);
+    im = -std::sin(pi * (double)q / a.L);
+    if (inv) im = -im;
+  };
+  out.assign((size_t)a.n_in + a.n_out + 2 * M, make_float2(0.f, 0.f));
+  double re, im;
+  for (int k = 0; k < a.n_in; ++k) {
+    chirp(k + a.off_in, re, im);
+    const double w = (inv && !pack && k != 0 && k != a.nyq) ? 2.0 : 1.0;
+    out[k] = make_float2((float)(w * re), (float)(w * im));
+  }
+  const double osc = (double)a.out_scale / M * (pack && !inv ? 0.5 : 1.0);
+  for (int k = 0; k < a.n_out; ++k) {
+    chirp(k + a.off_out, re, im);
+    out[a.n_in + k] = make_float2((float)(osc * re), (float)(osc * im));
+  }
+  // filter b[m] = conj(c[d + off_out - off_in]) for lags d in (-n_in, n_out),
+  // d = m or m - M; its M-point DFT by iterative radix-2 in double
+  std::vector<double> br(M, 0.0), bi(M, 0.0);
+  for (int m = 0; m < M; ++m) {
+    const int d = m < a.n_out ? m : m - M;
+    if (d >= -(a.n_in - 1)) {
+      chirp((long)d + a.off_out - a.off_in, re, im);
+      br[m] = re;
+      bi[m] = -im;
+    }
+  }
+  for (int i = 1, j = 0; i < M; ++i) {  // bit reversal
+    int bit = M >> 1;
+    for (; j & bit; bit >>= 1) j ^= bit;
+    j ^= bit;
+    if (i < j) std::swap(br[i], br[j]), std::swap(bi[i], bi[j]);
+  }
+  for (int len = 2; len <= M; len <<= 1) {
+    for (int i = 0; i < M; i += len) {
+      for (int k = 0; k < len / 2; ++k) {
+        const double t = -2.0 * pi * k / len, wr = std::cos(t), wi = std::sin(t);
+        const int u = i + k, v = i + k + len / 2;
+        const double xr = br[v] * wr - bi[v] * wi, xi = br[v] * wi + bi[v] * wr;
+        br[v] = br[u] - xr; bi[v] = bi[u] - xi;
+        br[u] += xr; bi[u] += xi;
+      }
+    }
+  }
+  float2* F = out.data() + a.n_in + a.n_out;
+  for (int m = 0; m < M; ++m) F[m] = make_float2((float)br[m], (float)bi[m]);
+  float2* TW = F + M;
+  for (int i = 0; i < M; ++i) {
+    const int e = ((i >> 5) * (i & 31)) & (M - 1);
+    TW[i] = make_float2((float)std::cos(2.0 * pi * e / M), (float)-std::sin(2.0 * pi * e / M));
+  }
+}
+
+struct BlueTabEntry {
+  int dev, mode, n_in, n_out, off_in, off_out, L, nyq;
+  float out_scale;
+  float2* d;
+};
+std::mutex g_blue_mu;
+
+// Device copy of the tables for this geometry on the current device, built
+// and uploaded on first use (the plan owns it).
+bl_status_t blue_tables(const bl_conv_plan_s* p, const BlueGeom& a, int mode, const float2** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BL_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_blue_mu);
+  if (!p->blue_cache) p->blue_cache = new (std::nothrow) std::vector<BlueTabEntry>();
+  auto* cache = static_cast<std::vector<BlueTabEntry>*>(p->blue_cache);
+  if (!cache) return BL_ERR_OOM;
+  for (const BlueTabEntry& e : *cache)
+    if (e.dev == dev && e.mode == mode && e.n_in == a.n_in && e.n_out == a.n_out && e.off_in == a.off_in &&
+        e.off_out == a.off_out && e.L == a.L && e.nyq == a.nyq && e.out_scale == a.out_scale) {
+      *out = e.d;
+      return BL_OK;
+    }
+  std::vector<float2> host;
+  host_tables_1k(a, mode, host);
+  float2* d = nullptr;
+  if (hipMalloc(&d, host.size() * sizeof(float2)) != hipSuccess) return BL_ERR_OOM;
+  if (hipMemcpy(d, host.data(), host.size() * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(d);
+    return BL_ERR_HIP;
+  }
+  cache->push_back(BlueTabEntry{dev, mode, a.n_in, a.n_out, a.off_in, a.off_out, a.L, a.nyq, a.out_scale, d});
+  *out = d;
+  return BL_OK;
+}
+
 template <int MODE, bool PREF>
 bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const char* name, double bytes,
                           hipStream_t s) {
@@ -740,7 +785,11 @@ bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const ch
 
 // Rounds are prefetched when one round's inputs fit in 32 floats per thread.
 template <int MODE>
-bl_status_t launch_1k(const BlueGeom& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
+bl_status_t launch_1k(const bl_conv_plan_s* p, const BlueGeom& a0, const void* in, void* out, const char* name,
+                      double bytes, hipStream_t s) {
+  BlueGeom a = a0;
+  const bl_status_t ts = blue_tables(p, a, MODE, &a.tab);
+  if (ts != BL_OK) return ts;
   const int need = MODE == 0 ? 16 * ((a.n_in + 511) / 512)
                    : MODE == 2 ? 32 * ((a.n_in + 511) / 512)
                    : MODE == 1 ? 2 * ((a.n_in + 31) / 32)
@@ -756,18 +805,18 @@ int fft_size_for(int need) {
 }
 
 template <int MODE>
-bl_status_t launch_mode(BlueArgs& a, int M, const void* in, void* out, const char* name, double bytes,
-                        hipStream_t s) {
+bl_status_t launch_mode(const bl_conv_plan_s* p, BlueArgs& a, int M, const void* in, void* out, const char* name,
+                        double bytes, hipStream_t s) {
   if (M == 256) return launch_m<256, MODE>(a, in, out, name, bytes, s);
   if (M == 512) return launch_m<512, MODE>(a, in, out, name, bytes, s);
-  if (M == 1024) return launch_1k<MODE>(a, in, out, name, bytes, s);
+  if (M == 1024) return launch_1k<MODE>(p, a, in, out, name, bytes, s);
   return BL_ERR_UNSUPPORTED;
 }
 
 // Chooses between one series per FFT and two (when the conjugate-symmetric
 // output or input range fits the same FFT size).
-bl_status_t launch_any(BlueArgs& a, bool inv, int other, const void* in, void* out, const char* name,
-                       double bytes, hipStream_t s) {
+bl_status_t launch_any(const bl_conv_plan_s* p, BlueArgs& a, bool inv, int other, const void* in, void* out,
+                       const char* name, double bytes, hipStream_t s) {
   if (2 * a.L > 64 * 64) return BL_ERR_UNSUPPORTED;
   if ((long)a.V * other < 2048) return BL_ERR_UNSUPPORTED;  // the direct DFT is as cheap
   const int M1 = fft_size_for(a.V + other - 1);
@@ -779,21 +828,21 @@ bl_status_t launch_any(BlueArgs& a, bool inv, int other, const void* in, void* o
     if (pack) {
       a.n_out = 2 * a.V - 1;
       a.off_out = -(a.V - 1);
-      return launch_mode<2>(a, M2, in, out, name, bytes, s);
+      return launch_mode<2>(p, a, M2, in, out, name, bytes, s);
     }
     a.n_out = a.V;
     a.off_out = 0;
-    return launch_mode<0>(a, M1, in, out, name, bytes, s);
+    return launch_mode<0>(p, a, M1, in, out, name, bytes, s);
   }
   a.n_out = other;
   if (pack) {
     a.n_in = 2 * a.V - 1;
     a.off_in = -(a.V - 1);
-    return launch_mode<3>(a, M2, in, out, name, bytes, s);
+    return launch_mode<3>(p, a, M2, in, out, name, bytes, s);
   }
   a.n_in = a.V;
   a.off_in = 0;
-  return launch_mode<1>(a, M1, in, out, name, bytes, s);
+  return launch_mode<1>(p, a, M1, in, out, name, bytes, s);
 }
 
 }  // namespace
@@ -808,7 +857,7 @@ bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float
   a.P = P;
   a.out_scale = 1.0f;
   const double bytes = (double)P * Win * 4 + (double)P * p->V * 8;
-  return launch_any(a, false, Win, in, out, "spec_fwd_1d", bytes, s);
+  return launch_any(p, a, false, Win, in, out, "spec_fwd_1d", bytes, s);
 }
 
 bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
@@ -821,7 +870,20 @@ bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, floa
   a.P = P;
   a.out_scale = 1.0f / (float)p->Lw;
   const double bytes = (double)P * p->V * 8 + (double)P * OW * 4;
-  return launch_any(a, true, OW, in, out, "spec_inv_1d", bytes, s);
+  return launch_any(p, a, true, OW, in, out, "spec_inv_1d", bytes, s);
 }
 
 }  // namespace blc
+
+void bl_blue_cache_free(void* cache) {
+  if (!cache) return;
+  auto* c = static_cast<std::vector<blc::BlueTabEntry>*>(cache);
+  int cur = 0;
+  const bool have = hipGetDevice(&cur) == hipSuccess;
+  for (const blc::BlueTabEntry& e : *c) {
+    if (hipSetDevice(e.dev) == hipSuccess) (void)hipFree(e.d);
+  }
+  if (have) (void)hipSetDevice(cur);
+  delete c;
+}
+
