@@ -433,10 +433,11 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
   // in flight together.
   const float* xin = static_cast<const float*>(in_);
   const float2* yin = static_cast<const float2*>(in_);
-  const long P = a.P;
-  const long jobs = PACK ? (P + 1) / 2 : P;
-  const long j0 = blockIdx.x * jobs_per_block;
-  const long j1 = min(jobs, j0 + jobs_per_block);
+  // element indices fit in 32 bits (checked on the host)
+  const unsigned P = (unsigned)a.P;
+  const unsigned jobs = PACK ? (P + 1) / 2 : P;
+  const unsigned j0 = blockIdx.x * (unsigned)jobs_per_block;
+  const unsigned j1 = min(jobs, j0 + (unsigned)jobs_per_block);
   constexpr int NS = 2 * kWaves1k;  // slots per block
   constexpr int NT = 64 * kWaves1k;
   // a round's inputs pass through registers in chunks of 32 floats per thread
@@ -446,39 +447,39 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
                   : MODE == 1 ? ((a.n_in + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC
                               : ((a.V + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC;
   float pf[32];
-  auto prefetch = [&](long base, int c) {
+  auto prefetch = [&](unsigned base, int c) {
     if constexpr (MODE == 0 || MODE == 2) {
 #pragma unroll
       for (int r = 0; r < IPC; ++r) {
         const int n = min(tid + NT * (c * IPC + r), a.n_in - 1);
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) {
-          const long job = min(base + sl, j1 - 1);
+          const unsigned job = min(base + sl, j1 - 1);
           if constexpr (MODE == 0) {
-            pf[r * PER + sl] = xin[(size_t)job * a.n_in + n];
+            pf[r * PER + sl] = xin[job * (unsigned)a.n_in + n];
           } else {
-            const long s1 = 2 * job;
-            const long s2 = min(s1 + 1, P - 1);
-            pf[r * PER + 2 * sl] = xin[(size_t)s1 * a.n_in + n];
-            pf[r * PER + 2 * sl + 1] = s2 == s1 ? 0.f : xin[(size_t)s2 * a.n_in + n];
+            const unsigned s1 = 2 * job;
+            const unsigned s2 = min(s1 + 1, P - 1);
+            pf[r * PER + 2 * sl] = xin[s1 * (unsigned)a.n_in + n];
+            pf[r * PER + 2 * sl + 1] = s2 == s1 ? 0.f : xin[s2 * (unsigned)a.n_in + n];
           }
         }
       }
     } else {
-      const long job = min(base + (tid & (NS - 1)), j1 - 1);
+      const unsigned job = min(base + (tid & (NS - 1)), j1 - 1);
       const int rows = MODE == 1 ? a.n_in : a.V;
 #pragma unroll
       for (int u = 0; u < IPC; ++u) {
         const int n = min(tid / NS + (NT / NS) * (c * IPC + u), rows - 1);
         if constexpr (MODE == 1) {
-          const float2 y = yin[(size_t)n * P + job];
+          const float2 y = yin[n * P + job];
           pf[PER * u] = y.x;
           pf[PER * u + 1] = y.y;
         } else {
-          const long s1 = 2 * job;
-          const long s2 = min(s1 + 1, P - 1);
-          const float2 y1 = yin[(size_t)n * P + s1];
-          const float2 y2 = s2 == s1 ? make_float2(0.f, 0.f) : yin[(size_t)n * P + s2];
+          const unsigned s1 = 2 * job;
+          const unsigned s2 = min(s1 + 1, P - 1);
+          const float2 y1 = yin[n * P + s1];
+          const float2 y2 = s2 == s1 ? make_float2(0.f, 0.f) : yin[n * P + s2];
           pf[PER * u] = y1.x;
           pf[PER * u + 1] = y1.y;
           pf[PER * u + 2] = y2.x;
@@ -527,8 +528,8 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
 
   if (PREF && j0 < j1) prefetch(j0, 0);
   __syncthreads();  // tables in LDS
-  for (long base = j0; base < j1; base += NS) {
-    const int nj = (int)min((long)NS, j1 - base);  // jobs this round
+  for (unsigned base = j0; base < j1; base += NS) {
+    const int nj = (int)min((unsigned)NS, j1 - base);  // jobs this round
     if constexpr (PREF) {
       commit(0);
     } else {
@@ -565,42 +566,42 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
         float2* dst = static_cast<float2*>(out_) + base + sl;
         const float2* src = bufs + sl * kXS;
 #pragma unroll 4
-        for (int i = tid / NS; i < a.n_out; i += NT / NS) dst[(size_t)i * P] = src[i];
+        for (int i = tid / NS; i < a.n_out; i += NT / NS) dst[i * P] = src[i];
       }
     } else if constexpr (MODE == 1) {
-      float* dst = static_cast<float*>(out_) + (size_t)base * a.n_out;
+      float* dst = static_cast<float*>(out_) + base * (unsigned)a.n_out;
       for (int i = tid; i < a.n_out; i += NT) {
         float r[NS];
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i].x;
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl)
-          if (sl < nj) dst[(size_t)sl * a.n_out + i] = r[sl];
+          if (sl < nj) dst[sl * (unsigned)a.n_out + i] = r[sl];
       }
     } else if constexpr (MODE == 2) {
       // Z[k] sits at index k + V - 1; the two series split by conjugate symmetry
       const int q = tid & (2 * NS - 1);
-      const long s = 2 * base + q;
+      const unsigned s = 2 * base + q;
       if (q < 2 * nj && s < P) {
         float2* dst = static_cast<float2*>(out_) + s;
         const float2* src = bufs + (q >> 1) * kXS + (a.V - 1);
 #pragma unroll 4
         for (int k = tid / (2 * NS); k < a.V; k += NT / (2 * NS)) {
           const float2 zp = src[k], zm = cconj(src[-k]);
-          dst[(size_t)k * P] = (q & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
+          dst[k * P] = (q & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
         }
       }
     } else {
-      float* dst = static_cast<float*>(out_) + (size_t)(2 * base) * a.n_out;
-      const long ns = min(P - 2 * base, 2L * nj);  // series of this round
+      float* dst = static_cast<float*>(out_) + 2 * base * (unsigned)a.n_out;
+      const unsigned ns = min(P - 2 * base, 2u * nj);  // series of this round
       for (int i = tid; i < a.n_out; i += NT) {
         float2 r[NS];
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i];
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) {
-          if (2 * sl < ns) dst[(size_t)(2 * sl) * a.n_out + i] = r[sl].x;
-          if (2 * sl + 1 < ns) dst[(size_t)(2 * sl + 1) * a.n_out + i] = r[sl].y;
+          if (2u * sl < ns) dst[2 * sl * (unsigned)a.n_out + i] = r[sl].x;
+          if (2u * sl + 1 < ns) dst[(2 * sl + 1) * (unsigned)a.n_out + i] = r[sl].y;
         }
       }
     }
@@ -787,6 +788,9 @@ bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const ch
 template <int MODE>
 bl_status_t launch_1k(const bl_conv_plan_s* p, const BlueGeom& a0, const void* in, void* out, const char* name,
                       double bytes, hipStream_t s) {
+  // the kernel indexes its input and output with 32-bit element offsets
+  const long rows = std::max<long>({(long)a0.n_in, (long)a0.n_out, 2L * a0.V});
+  if (a0.P * rows >= 2147483647L || a0.P * rows < 0) return BL_ERR_UNSUPPORTED;
   BlueGeom a = a0;
   const bl_status_t ts = blue_tables(p, a, MODE, &a.tab);
   if (ts != BL_OK) return ts;
