@@ -27,6 +27,8 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// Offsets inside one bin's matrices are 32-bit (a bin's matrices hold far
+// fewer than 2^31 elements); the per-bin bases are 64-bit.
 struct CgemmArgs {
   int M, N, K;                   // complex sizes
   unsigned sAm, sAk, sBk, sBn;   // element strides (complex units); one of each pair is 1
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
       else { k = e / (BM / 2); m = (e - k * (BM / 2)) * 2; }
       ra[q] = zero4;
       if ((m0 + m < g.M) && (k0 + k < kend))
-        ra[q] = *reinterpret_cast<const float4*>(Ab + (size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk);
+        ra[q] = *reinterpret_cast<const float4*>(Ab + ((unsigned)(m0 + m) * g.sAm + (unsigned)(k0 + k) * g.sAk));
     }
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
@@ -112,7 +114,7 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
       else { n = e >> 3; k = (e & 7) * 2; }
       rb[q] = zero4;
       if ((n0 + n < g.N) && (k0 + k < kend))
-        rb[q] = *reinterpret_cast<const float4*>(Bb + (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
+        rb[q] = *reinterpret_cast<const float4*>(Bb + ((unsigned)(k0 + k) * g.sBk + (unsigned)(n0 + n) * g.sBn));
     }
   };
   auto store = [&](int buf, const float4* ra, const float4* rb) {
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int m = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (m < g.M && n < g.N) Of[((size_t)m * g.ldo + n) * 2 + bcol] = acc[i][j][v];
+        if (m < g.M && n < g.N) Of[((unsigned)m * g.ldo + n) * 2 + bcol] = acc[i][j][v];
       }
     }
 }
@@ -250,6 +252,8 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   const bool a_ok = (g.bA % 2 == 0) && (a_kc ? (g.sAm % 2 == 0 && g.K % 2 == 0) : (g.sAk % 2 == 0 && g.M % 2 == 0));
   const bool b_ok = (g.bB % 2 == 0) && (b_nc ? (g.sBk % 2 == 0 && g.N % 2 == 0) : (g.sBn % 2 == 0 && g.K % 2 == 0));
   if (!a_ok || !b_ok || B > 65535) return BL_ERR_UNSUPPORTED;
+  const long most = std::max<long>({(long)g.M * g.K, (long)g.K * g.N, (long)g.M * g.N});
+  if (2 * most >= 2147483647L) return BL_ERR_UNSUPPORTED;  // 32-bit offsets within a bin
   const BlContractTiling& t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
   const int BM = t.bm, BN = t.bn;
   const int tiles_m = (g.M + BM - 1) / BM;
