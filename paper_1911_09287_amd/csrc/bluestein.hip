@@ -403,7 +403,17 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
 
   // the chirps, the filter's spectrum and the twiddles, built once per plan
   // in double precision on the host, are laid out in the table as in LDS
-  for (int i = tid; i < a.n_in + a.n_out + 2 * M; i += blockDim.x) pre[i] = a.tab[i];
+  // (all of a thread's table loads in flight together: n_in + n_out <= M + 1)
+  {
+    constexpr int NT = 64 * kWaves1k, NTAB = (3 * M + 1 + NT - 1) / NT;
+    const int ntab = a.n_in + a.n_out + 2 * M;
+    float2 tv[NTAB];
+#pragma unroll
+    for (int u = 0; u < NTAB; ++u) tv[u] = a.tab[min(tid + NT * u, ntab - 1)];
+#pragma unroll
+    for (int u = 0; u < NTAB; ++u)
+      if (tid + NT * u < ntab) pre[tid + NT * u] = tv[u];
+  }
   auto exchange = [&](float2* v) {
 #pragma unroll
     for (int k = 0; k < 32; ++k) xb[k * 33 + h] = v[k];
