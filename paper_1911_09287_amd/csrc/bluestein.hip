@@ -730,39 +730,10 @@ void host_tables_1k(const BlueGeom& a, int mode, std::vector<float2>& out) {
   }
 }
 
-struct BlueTabEntry {
-  int dev, mode, n_in, n_out, off_in, off_out, L, nyq;
-  float out_scale;
-  float2* d;
-};
-std::mutex g_blue_mu;
-
-// Device copy of the tables for this geometry on the current device, built
-// and uploaded on first use (the plan owns it).
+// Device copy of the tables for this geometry (built and uploaded on first use).
 bl_status_t blue_tables(const bl_conv_plan_s* p, const BlueGeom& a, int mode, const float2** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return BL_ERR_HIP;
-  std::lock_guard<std::mutex> lk(g_blue_mu);
-  if (!p->blue_cache) p->blue_cache = new (std::nothrow) std::vector<BlueTabEntry>();
-  auto* cache = static_cast<std::vector<BlueTabEntry>*>(p->blue_cache);
-  if (!cache) return BL_ERR_OOM;
-  for (const BlueTabEntry& e : *cache)
-    if (e.dev == dev && e.mode == mode && e.n_in == a.n_in && e.n_out == a.n_out && e.off_in == a.off_in &&
-        e.off_out == a.off_out && e.L == a.L && e.nyq == a.nyq && e.out_scale == a.out_scale) {
-      *out = e.d;
-      return BL_OK;
-    }
-  std::vector<float2> host;
-  host_tables_1k(a, mode, host);
-  float2* d = nullptr;
-  if (hipMalloc(&d, host.size() * sizeof(float2)) != hipSuccess) return BL_ERR_OOM;
-  if (hipMemcpy(d, host.data(), host.size() * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
-    (void)hipFree(d);
-    return BL_ERR_HIP;
-  }
-  cache->push_back(BlueTabEntry{dev, mode, a.n_in, a.n_out, a.off_in, a.off_out, a.L, a.nyq, a.out_scale, d});
-  *out = d;
-  return BL_OK;
+  const std::vector<long> key{1, mode, a.n_in, a.n_out, a.off_in, a.off_out, a.L, a.nyq, float_key(a.out_scale)};
+  return plan_table(p, key, [&](std::vector<float2>& host) { host_tables_1k(a, mode, host); }, out);
 }
 
 template <int MODE, bool PREF>
@@ -889,15 +860,4 @@ bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, floa
 
 }  // namespace blc
 
-void bl_blue_cache_free(void* cache) {
-  if (!cache) return;
-  auto* c = static_cast<std::vector<blc::BlueTabEntry>*>(cache);
-  int cur = 0;
-  const bool have = hipGetDevice(&cur) == hipSuccess;
-  for (const blc::BlueTabEntry& e : *c) {
-    if (hipSetDevice(e.dev) == hipSuccess) (void)hipFree(e.d);
-  }
-  if (have) (void)hipSetDevice(cur);
-  delete c;
-}
 

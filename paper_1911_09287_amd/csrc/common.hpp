@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
+#include <functional>
+#include <vector>
+
 #include "plan.hpp"
 
 namespace blc {
@@ -42,6 +45,13 @@ __device__ inline float2 cscale(float2 a, float s) { return make_float2(a.x * s,
 
 // FFT row index of the r-th kept row.
 __device__ inline int kept_row_d(int r, int r_h, int Lh, int R) { return r <= r_h ? r : r + (Lh - R); }
+
+// ---- plan-owned device tables (tables.hip) ----------------------------------
+// Returns the device copy, on the current device, of the table identified by
+// `key`, building it with `build` (on the host) and uploading it on first use.
+bl_status_t plan_table(const bl_conv_plan_s* p, const std::vector<long>& key,
+                       const std::function<void(std::vector<float2>&)>& build, const float2** out);
+long float_key(float x);  // bit pattern of x, for keys
 
 // ---- stage launchers --------------------------------------------------------
 // Real planes [P][Hin][Win] placed at (oi, oj) of the grid -> kept spectrum

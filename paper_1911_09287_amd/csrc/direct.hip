@@ -289,7 +289,7 @@ template <int TMAX, int TC>
 __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, float* __restrict__ dw,
                                                          float* __restrict__ part, WgradGeom g) {
   constexpr int TF = kThreads / TC;
-  extern __shared__ float2 E[];  // bins_per_chunk x T
+  extern __shared__ float2 E[];  // bins_per_chunk x TMAX, zero beyond T (no branches in the bin loop)
   __shared__ float res[TC > 1 ? TF * TC * TMAX : 1];
   const int B = g.R * g.V;
   const int b0 = blockIdx.y * g.bins_per_chunk;
@@ -297,8 +297,12 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
   const int LL = g.Lh * g.Lw;
   const int nyq = (g.Lw % 2 == 0) ? g.Lw / 2 : -1;
   const double inv = 1.0 / (double)LL;
-  for (int e = threadIdx.x; e < nb * g.T; e += blockDim.x) {
-    const int bb = e / g.T, t = e % g.T;
+  for (int e = threadIdx.x; e < nb * TMAX; e += blockDim.x) {
+    const int bb = e / TMAX, t = e % TMAX;
+    if (t >= g.T) {
+      E[e] = make_float2(0.f, 0.f);
+      continue;
+    }
     const int bin = b0 + bb;
     const int r = bin / g.V, v = bin % g.V;
     const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
@@ -320,13 +324,19 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
   const float2* src = DW + (size_t)b0 * Q + (valid ? (long)c * g.F + f : 0);
-#pragma unroll 8
-  for (int bb = 0; bb < nb; ++bb) {
-    const float2 d = src[(size_t)bb * Q];
-    const float2* Eb = E + bb * g.T;
+  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
+  for (int bb = 0; bb < nb; bb += 8) {
+    float2 d[8];
 #pragma unroll
-    for (int t = 0; t < TMAX; ++t)
-      if (t < g.T) acc[t] = fmaf(d.x, Eb[t].x, fmaf(-d.y, Eb[t].y, acc[t]));
+    for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, nb - 1) * Q];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = bb + j < nb;
+      const float2 dj = in ? d[j] : make_float2(0.f, 0.f);
+      const float2* Eb = E + min(bb + j, nb - 1) * TMAX;
+#pragma unroll
+      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
+    }
   }
   if (g.chunks > 1) {
     if (valid) {
@@ -380,6 +390,76 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restri
   const float tot = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
   const int c = (int)(q / g.F), f = (int)(q % g.F);
   dw[((size_t)f * g.C + c) * g.T + t] = tot;
+}
+
+// Wide layers (many (c, f) pairs): one block per 64 consecutive pairs and all
+// bins, its four waves each reducing a quarter of the bins; the quarters are
+// added in a fixed order through LDS and written straight to dw, so no
+// partial sums leave the block.  E comes from a table built once per plan.
+template <int TMAX>
+__global__ __launch_bounds__(kThreads) void k_wgrad_wide(const float2* __restrict__ DW, const float2* __restrict__ Et,
+                                                         float* __restrict__ dw, WgradGeom g) {
+  extern __shared__ float2 E[];  // [kept][TMAX], zero beyond T: the bin loop has no branches
+  __shared__ float red[4][64][TMAX];
+  const int B = g.R * g.V;
+  for (int e = threadIdx.x; e < B * TMAX; e += blockDim.x) {
+    const int bb = e / TMAX, t = e - bb * TMAX;
+    E[e] = t < g.T ? Et[bb * g.T + t] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  const unsigned Q = (unsigned)g.C * g.F;
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const unsigned q = blockIdx.x * 64u + lane;
+  const bool valid = q < Q;
+  const int bb0 = grp * B / 4, bb1 = (grp + 1) * B / 4;
+  float acc[TMAX];
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
+  const float2* src = DW + (valid ? q : 0u);
+  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
+  for (int bb = bb0; bb < bb1; bb += 8) {
+    float2 d[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, bb1 - 1) * Q];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = bb + j < bb1;
+      const float2 dj = in ? d[j] : make_float2(0.f, 0.f);
+      const float2* Eb = E + min(bb + j, bb1 - 1) * TMAX;
+#pragma unroll
+      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) red[grp][lane][t] = acc[t];
+  __syncthreads();
+  if (grp == 0 && valid) {
+    const int c = (int)(q / g.F), f = (int)(q % g.F);
+    float* o = dw + ((size_t)f * g.C + c) * g.T;
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t)
+      if (t < g.T) o[t] = ((red[0][lane][t] + red[1][lane][t]) + red[2][lane][t]) + red[3][lane][t];
+  }
+}
+
+// Inverse-DFT weights E[bin][t] of the weight gradient, in double precision.
+void host_wgrad_weights(const bl_conv_plan_s* p, std::vector<float2>& out) {
+  const int T = p->Kh * p->Kw, B = (int)p->kept;
+  const long LL = (long)p->Lh * p->Lw;
+  const int nyq = (p->Lw % 2 == 0) ? p->Lw / 2 : -1;
+  const double pi = 3.141592653589793238462643383279502884;
+  out.assign((size_t)B * T, make_float2(0.f, 0.f));
+  for (int bin = 0; bin < B; ++bin) {
+    const int r = bin / p->V, v = bin % p->V;
+    const int u = bl_kept_row(r, p->r_h, p->Lh, p->R);
+    const double h = ((v == 0 || v == nyq) ? 1.0 : 2.0) / (double)LL;
+    for (int t = 0; t < T; ++t) {
+      const int ta = t / p->Kw, tb = t % p->Kw;
+      const long idx = ((long)u * ta * p->Lw + (long)v * tb * p->Lh) % LL;
+      const double ang = 2.0 * pi * (double)idx / (double)LL;
+      out[(size_t)bin * T + t] = make_float2((float)(h * std::cos(ang)), (float)(h * std::sin(ang)));
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -554,10 +634,43 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept;
+  // wide layers: at least 256 blocks of 64 pairs, taps and table that fit
+  // (rows of at most 256 output channels: wider rows write dw better from
+  // the tiled kernel below)
+  const int tmax_w = g.T <= 9 ? g.T : 16;
+  if (Q / 64 >= 256 && p->Cout <= 256 && g.T <= 16 && (size_t)B * tmax_w * sizeof(float2) <= 48 * 1024 &&
+      Q < 2147483647L) {
+    const float2* Et = nullptr;
+    const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
+    const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
+    if (ts != BL_OK) return ts;
+    const size_t lds = (size_t)B * tmax_w * sizeof(float2);
+    const dim3 grid((unsigned)((Q + 63) / 64));
+    const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
+    auto go = [&](auto kern) {
+      return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+        hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, Et, dw, g);
+      });
+    };
+    switch (g.T) {
+      case 1: return go(k_wgrad_wide<1>);
+      case 2: return go(k_wgrad_wide<2>);
+      case 3: return go(k_wgrad_wide<3>);
+      case 4: return go(k_wgrad_wide<4>);
+      case 5: return go(k_wgrad_wide<5>);
+      case 6: return go(k_wgrad_wide<6>);
+      case 7: return go(k_wgrad_wide<7>);
+      case 8: return go(k_wgrad_wide<8>);
+      case 9: return go(k_wgrad_wide<9>);
+      default: return go(k_wgrad_wide<16>);
+    }
+  }
   g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices
-  g.bins_per_chunk = (B + g.chunks - 1) / g.chunks;
+  g.bins_per_chunk = ((B + g.chunks - 1) / g.chunks + 7) / 8 * 8;  // whole batches of 8 loads
+  g.chunks = (B + g.bins_per_chunk - 1) / g.bins_per_chunk;         // at most the workspace's slices
   if (g.T > 64 || g.chunks > 65535) return BL_ERR_UNSUPPORTED;
-  const size_t lds = (size_t)g.bins_per_chunk * g.T * sizeof(float2);
+  const int tmax = g.T <= 9 ? g.T : g.T <= 16 ? 16 : g.T <= 32 ? 32 : 64;  // as instantiated below
+  const size_t lds = (size_t)g.bins_per_chunk * tmax * sizeof(float2);
   if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
   const int TC = chan_tile(g.T, p->Cout), TF = kThreads / TC;
   dim3 grid((unsigned)((long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF)), (unsigned)g.chunks);
@@ -568,10 +681,17 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
       hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, dw, part, g);
     });
   };
-  if (g.T <= 8) st = TC == 8 ? go(k_wgrad_idft<8, 8>) : go(k_wgrad_idft<8, 1>);
-  else if (g.T <= 16) st = TC == 8 ? go(k_wgrad_idft<16, 8>) : go(k_wgrad_idft<16, 1>);
-  else if (g.T <= 32) st = go(k_wgrad_idft<32, 1>);
-  else st = go(k_wgrad_idft<64, 1>);
+  auto go2 = [&](auto k8, auto k1) { return TC == 8 ? go(k8) : go(k1); };
+  switch (g.T) {
+#define BL_WG_T(n) \
+  case n: st = go2(k_wgrad_idft<n, 8>, k_wgrad_idft<n, 1>); break;
+    BL_WG_T(1) BL_WG_T(2) BL_WG_T(3) BL_WG_T(4) BL_WG_T(5) BL_WG_T(6) BL_WG_T(7) BL_WG_T(8) BL_WG_T(9)
+#undef BL_WG_T
+    default:
+      if (g.T <= 16) st = go2(k_wgrad_idft<16, 8>, k_wgrad_idft<16, 1>);
+      else if (g.T <= 32) st = go(k_wgrad_idft<32, 1>);
+      else st = go(k_wgrad_idft<64, 1>);
+  }
   if (st != BL_OK || g.chunks == 1) return st;
   const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
   return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {

@@ -134,7 +134,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
 
 extern "C" bl_status_t bl_conv_plan_destroy(bl_conv_plan_t p) {
   if (!p) return BL_ERR_INVALID_ARG;
-  bl_blue_cache_free(p->blue_cache);
+  bl_plan_tables_free(p->tables);
   delete p;
   return BL_OK;
 }

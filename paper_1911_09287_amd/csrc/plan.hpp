@@ -72,13 +72,14 @@ struct bl_conv_plan_s {
   int wg_chunks;        // bin slices of the weight-gradient inverse DFT
   BlContractTiling ct[3];  // contraction tiling: forward, grad-input, grad-weight
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
-  // device tables of the 1-D transforms (chirps and filter spectra), built
-  // on a plan's first 1-D call on each device; freed with the plan
-  mutable void* blue_cache;
+  // small device tables (1-D chirps and filter spectra, weight-gradient
+  // inverse-DFT weights), built on a plan's first call that needs them on
+  // each device; freed with the plan
+  mutable void* tables;
 };
 
-// Frees the device tables a plan's 1-D transforms built (null is a no-op).
-void bl_blue_cache_free(void* cache);
+// Frees a plan's device tables (null is a no-op).
+void bl_plan_tables_free(void* tables);
 
 // FFT row index of the r-th kept row: the top-left corner (u = 0..r_h) first,
 // then the bottom-left corner (u = Lh - r_h .. Lh - 1).
