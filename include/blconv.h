@@ -46,11 +46,13 @@
  *
  * Ownership: the caller owns every device buffer (x, w, y, dy, dx, dw and the
  * workspace ws).  Creating and querying a plan makes no HIP call.  The plan
- * also owns small device tables of its 1-D transforms (chirps, the chirp
- * filter's spectrum and twiddles: under 100 KB per device), built in double
- * precision on the host and uploaded by the first 1-D compute call of the plan
- * on each device; that first call allocates and copies synchronously, so make
- * it outside stream capture.  Every other compute call allocates nothing,
+ * also owns small device tables, built in double precision on the host: those
+ * of its 1-D transforms (chirps, the chirp filter's spectrum and twiddles:
+ * under 100 KB) and the inverse-DFT weights of the weight gradient (8 K^2
+ * bytes per kept bin, K^2 -> K in 1-D).  The first compute call of
+ * the plan that needs a table on a device uploads it there; that call
+ * allocates and copies synchronously, so make each kind of call once outside
+ * stream capture before capturing it.  Every other compute call allocates nothing,
  * makes no host synchronisation and enqueues its kernels on `stream` (a
  * hipStream_t, passed as void*; NULL = the default stream).
  * bl_conv_plan_destroy frees the tables (no kernel of the plan may still be

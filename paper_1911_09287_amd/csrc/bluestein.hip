@@ -144,15 +144,11 @@ __device__ __forceinline__ void stockham_pass(int Ns, int t, const float2* roots
   if constexpr (NT == 64) wave_sync(); else __syncthreads();
 }
 
-// Radix sequence of the per-wave FFTs: M = 1024: 16, 16, 4; 512: 8, 8, 8;
-// 256: 4, 4, 4, 4.  Pass p has span Ns_p = product of the earlier radices.
+// Radix sequence of the per-wave FFTs: M = 512: 8, 8, 8; 256: 4, 4, 4, 4.
+// Pass p has span Ns_p = product of the earlier radices.  (M = 1024 has a
+// kernel of its own.)
 template <int M>
 struct WavePlan;
-template <>
-struct WavePlan<1024> {
-  static constexpr int n = 3;
-  static constexpr int R[3] = {16, 16, 4};
-};
 template <>
 struct WavePlan<512> {
   static constexpr int n = 3;
@@ -390,7 +386,7 @@ template <int MODE, bool PREF>
 __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
                                                                BlueGeom a, long jobs_per_block) {
   constexpr int M = 1024;
-  constexpr bool INV = MODE & 1, PACK = MODE >= 2;
+  constexpr bool PACK = MODE >= 2;
   extern __shared__ float2 sm[];
   float2* bufs = sm;                          // 16 slots x kXS
   float2* pre = bufs + 2 * kWaves1k * kXS;    // n_in

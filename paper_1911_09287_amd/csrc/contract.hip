@@ -227,25 +227,25 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
                                   float2* O, float2* part, hipStream_t s) {
   CgemmArgs g{};
   const unsigned long long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
-  bool a_kc = true, b_nc = true, conj = true;
+  bool a_kc = true, b_nc = true;
   switch (which) {
     case Contract::Forward:  // Y[n][f] = sum_c X[n][c] conj(W[c][f])
       g.M = (int)N; g.N = (int)Co; g.K = (int)Ci;
       g.sAm = (unsigned)Ci; g.sAk = 1; g.sBk = (unsigned)Co; g.sBn = 1; g.ldo = (unsigned)Co;
       g.bA = N * Ci; g.bB = Ci * Co; g.bO = N * Co;
-      a_kc = true; b_nc = true; conj = true;
+      a_kc = true; b_nc = true;
       break;
     case Contract::GradInput:  // DX[n][c] = sum_f DY[n][f] W[c][f]
       g.M = (int)N; g.N = (int)Ci; g.K = (int)Co;
       g.sAm = (unsigned)Co; g.sAk = 1; g.sBk = 1; g.sBn = (unsigned)Co; g.ldo = (unsigned)Ci;
       g.bA = N * Co; g.bB = Ci * Co; g.bO = N * Ci;
-      a_kc = true; b_nc = false; conj = false;
+      a_kc = true; b_nc = false;
       break;
     case Contract::GradWeight:  // DW[c][f] = sum_n X[n][c] conj(DY[n][f])
       g.M = (int)Ci; g.N = (int)Co; g.K = (int)N;
       g.sAm = 1; g.sAk = (unsigned)Ci; g.sBk = (unsigned)Co; g.sBn = 1; g.ldo = (unsigned)Co;
       g.bA = N * Ci; g.bB = N * Co; g.bO = Ci * Co;
-      a_kc = false; b_nc = true; conj = true;
+      a_kc = false; b_nc = true;
       break;
   }
   // alignment of every 2-complex vector: even strides, even sizes along the vector

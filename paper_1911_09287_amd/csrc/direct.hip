@@ -272,8 +272,9 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
 //   dw = sum over kept bins (u, v) of Re(DW[u, v] * E[b][t]),
 //   E[b][t] = h_v e^{+2 pi i (u a / Lh + v b' / Lw)} / (Lh Lw)
 // (the c2r inverse restricted to the filter support).  The bins are split
-// into `chunks` slices (blockIdx.y); each block tabulates E for its slice in
-// LDS and reduces a tile of TC x TF (c, f) pairs over it.  With more than one
+// into `chunks` slices (blockIdx.y); each block copies E for its slice from a
+// table built once per plan into LDS and reduces 256 (c, f) pairs over it:
+// consecutive q when TC = 1, a TC x TF tile otherwise.  With more than one
 // slice the partial sums go to part[chunk][t][q] (contiguous in q) and
 // k_wgrad_reduce adds them in a fixed order, so results do not depend on
 // scheduling; with one slice and TC > 1 the results go through LDS so that
@@ -286,40 +287,37 @@ struct WgradGeom {
 };
 
 template <int TMAX, int TC>
-__global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, float* __restrict__ dw,
-                                                         float* __restrict__ part, WgradGeom g) {
+__global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, const float2* __restrict__ Et,
+                                                         float* __restrict__ dw, float* __restrict__ part,
+                                                         WgradGeom g) {
   constexpr int TF = kThreads / TC;
   extern __shared__ float2 E[];  // bins_per_chunk x TMAX, zero beyond T (no branches in the bin loop)
   __shared__ float res[TC > 1 ? TF * TC * TMAX : 1];
   const int B = g.R * g.V;
   const int b0 = blockIdx.y * g.bins_per_chunk;
   const int nb = min(g.bins_per_chunk, B - b0);
-  const int LL = g.Lh * g.Lw;
-  const int nyq = (g.Lw % 2 == 0) ? g.Lw / 2 : -1;
-  const double inv = 1.0 / (double)LL;
-  for (int e = threadIdx.x; e < nb * TMAX; e += blockDim.x) {
-    const int bb = e / TMAX, t = e % TMAX;
-    if (t >= g.T) {
-      E[e] = make_float2(0.f, 0.f);
-      continue;
+  // copy this slice of the table, four loads of a thread in flight together
+  const float2* Es = Et + (size_t)b0 * g.T;
+  for (int e0 = threadIdx.x; e0 < nb * TMAX; e0 += 4 * kThreads) {
+    float2 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int e = e0 + k * kThreads, bb = e / TMAX, t = e - bb * TMAX;
+      v[k] = (e < nb * TMAX && t < g.T) ? Es[bb * g.T + t] : make_float2(0.f, 0.f);
     }
-    const int bin = b0 + bb;
-    const int r = bin / g.V, v = bin % g.V;
-    const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
-    const int ta = t / g.Kw, tb = t % g.Kw;
-    const long idx = ((long)u * ta * g.Lw + (long)v * tb * g.Lh) % LL;
-    double sn, cs;
-    sincospi(2.0 * (double)idx / (double)LL, &sn, &cs);
-    const double h = (v == 0 || v == nyq) ? inv : 2.0 * inv;
-    E[e] = make_float2((float)(h * cs), (float)(h * sn));
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (e0 + k * kThreads < nb * TMAX) E[e0 + k * kThreads] = v[k];
   }
   __syncthreads();
   const long Q = (long)g.C * g.F;
+  // TC == 1: 256 consecutive pairs q = c F + f per block; else a TC x TF tile
   const int tiles_f = (g.F + TF - 1) / TF;
   const int c0 = (blockIdx.x / tiles_f) * TC, f0 = (blockIdx.x % tiles_f) * TF;
   const int tc = threadIdx.x / TF, tf = threadIdx.x - (threadIdx.x / TF) * TF;
-  const int c = c0 + tc, f = f0 + tf;
-  const bool valid = c < g.C && f < g.F;
+  const long q1 = (long)blockIdx.x * kThreads + threadIdx.x;
+  const int c = TC == 1 ? (int)(q1 / g.F) : c0 + tc, f = TC == 1 ? (int)(q1 % g.F) : f0 + tf;
+  const bool valid = TC == 1 ? q1 < Q : (c < g.C && f < g.F);
   float acc[TMAX];
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
@@ -637,13 +635,14 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   // wide layers: at least 256 blocks of 64 pairs, taps and table that fit
   // (rows of at most 256 output channels: wider rows write dw better from
   // the tiled kernel below)
+  if (g.T > 64) return BL_ERR_UNSUPPORTED;
+  const float2* Et = nullptr;  // E[bin][t], built once per plan
+  const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
+  const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
+  if (ts != BL_OK) return ts;
   const int tmax_w = g.T <= 9 ? g.T : 16;
-  if (Q / 64 >= 256 && p->Cout <= 256 && g.T <= 16 && (size_t)B * tmax_w * sizeof(float2) <= 48 * 1024 &&
+  if (Q / 64 >= 256 && p->Cout <= 256 && g.T <= 16 && (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&
       Q < 2147483647L) {
-    const float2* Et = nullptr;
-    const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
-    const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
-    if (ts != BL_OK) return ts;
     const size_t lds = (size_t)B * tmax_w * sizeof(float2);
     const dim3 grid((unsigned)((Q + 63) / 64));
     const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
@@ -666,19 +665,19 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
     }
   }
   g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices
-  g.bins_per_chunk = ((B + g.chunks - 1) / g.chunks + 7) / 8 * 8;  // whole batches of 8 loads
-  g.chunks = (B + g.bins_per_chunk - 1) / g.bins_per_chunk;         // at most the workspace's slices
-  if (g.T > 64 || g.chunks > 65535) return BL_ERR_UNSUPPORTED;
+  g.bins_per_chunk = p->wg_bins;
+  if (g.chunks > 65535) return BL_ERR_UNSUPPORTED;
   const int tmax = g.T <= 9 ? g.T : g.T <= 16 ? 16 : g.T <= 32 ? 32 : 64;  // as instantiated below
   const size_t lds = (size_t)g.bins_per_chunk * tmax * sizeof(float2);
-  if (lds > kMaxLds) return BL_ERR_UNSUPPORTED;
+  if ((long)lds > kWgradSliceLds) return BL_ERR_UNSUPPORTED;
   const int TC = chan_tile(g.T, p->Cout), TF = kThreads / TC;
-  dim3 grid((unsigned)((long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF)), (unsigned)g.chunks);
+  const long xblocks = TC == 1 ? (Q + kThreads - 1) / kThreads : (long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF);
+  dim3 grid((unsigned)xblocks, (unsigned)g.chunks);
   const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
   bl_status_t st;
   auto go = [&](auto kern) {
     return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
-      hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, dw, part, g);
+      hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, Et, dw, part, g);
     });
   };
   auto go2 = [&](auto k8, auto k1) { return TC == 8 ? go(k8) : go(k1); };

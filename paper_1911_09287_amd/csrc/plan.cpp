@@ -101,15 +101,20 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   p->off_T = o;  o = align_up(o + B * p->N * (size_t)std::max(p->Cin, p->Cout) * cb, 256);
   p->off_DW = o; o = align_up(o + B * p->Cin * p->Cout * cb, 256);
   // partial sums of the weight-gradient inverse DFT over bin slices: enough
-  // slices for ~1024 blocks, at least 16 bins per slice
+  // slices for ~1024 blocks of 256 (c, f) pairs, at least 16 bins per slice,
+  // whole batches of 8 bins, and a slice's weights [bins][taps, padded as the
+  // kernels are instantiated] within kWgradSliceLds
   {
     const long Q = (long)p->Cin * p->Cout;
+    const int T = p->Kh * p->Kw;
+    const long tmax = T <= 9 ? T : T <= 16 ? 16 : T <= 32 ? 32 : 64;
     const long xblocks = (Q + 255) / 256;
     const long want = (1024 + xblocks - 1) / xblocks;
-    const long maxc = std::max<long>(1, p->kept / 16);
-    long chunks = std::max<long>(1, std::min(want, maxc));
-    const long per = (p->kept + chunks - 1) / chunks;
-    chunks = (p->kept + per - 1) / per;
+    long per = std::max<long>(16, (p->kept + want - 1) / want);
+    const long cap = std::max<long>(8, kWgradSliceLds / (tmax * 8) / 8 * 8);
+    per = std::min((per + 7) / 8 * 8, cap);
+    const long chunks = (p->kept + per - 1) / per;
+    p->wg_bins = (int)per;
     p->wg_chunks = (int)chunks;
     p->off_Part = o;
     o = align_up(o + (chunks > 1 ? (size_t)chunks * Q * p->Kh * p->Kw * sizeof(float) : 0), 256);

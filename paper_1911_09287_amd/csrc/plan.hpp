@@ -20,6 +20,10 @@
 // matrix cores (the busiest CU sets the time), every tile pays a fixed start
 // (operand latency before the first MFMA), and k-splits add a pass that sums
 // the partial tiles in a fixed order (deterministic results) at HBM speed.
+// Dynamic LDS of one weight-gradient slice (its inverse-DFT weights): with
+// the kernel's static LDS (at most 16 KB) a block stays within 64 KB.
+constexpr long kWgradSliceLds = 48 * 1024;
+
 struct BlContractTiling {
   int bm, bn, splits;
 };
@@ -70,6 +74,7 @@ struct bl_conv_plan_s {
   std::vector<uint8_t> mask;  // [Lh][Wh]
   // workspace layout (bytes)
   int wg_chunks;        // bin slices of the weight-gradient inverse DFT
+  int wg_bins;          // bins per slice (a multiple of 8)
   BlContractTiling ct[3];  // contraction tiling: forward, grad-input, grad-weight
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
   // small device tables (1-D chirps and filter spectra, weight-gradient

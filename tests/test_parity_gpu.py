@@ -233,3 +233,30 @@ def test_2d_fast_grids(torch):
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
             errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
             assert max(errs) <= TOL, errs
+
+
+def test_wgrad_paths(torch):
+    """Each route of the weight-gradient inverse DFT: one pass over all bins
+    for wide layers (taps padded to 16 or exact), bin slices whose weights fill
+    the LDS cap (8 x 8 taps), channel-tiled slices for more than 256 output
+    channels, and a single slice written without partial sums."""
+    cases = [
+        synth.Layer("wg_wide_k3", 2, 2, 128, 128, 8, 8, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("wg_wide_k4", 2, 2, 128, 128, 8, 8, 4, (2, 1, 2, 1), "blur"),
+        synth.Layer("wg_lds_cap_k8", 2, 1, 256, 256, 32, 32, 8, (0, 0, 0, 0), "blur"),
+        synth.Layer("wg_tiled_f384", 2, 2, 16, 384, 12, 12, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("wg_single_slice", 1, 2, 4, 300, 20, 1, 3, (1, 1), "walk"),
+    ]
+    for i, layer in enumerate(cases):
+        for c in (0.0, 0.5):
+            say(f"[wgrad] {layer.name} c={c}")
+            x, w, dy = synth.random_inputs(layer, 1500 + i)
+            y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
+            # the oracle's forward of the 65536-filter case takes a minute: dw only there
+            rdw = bo.backward_weight(x, dy, layer.K, layer.pad, c, None)
+            errs = [rel(dw, rdw)]
+            if layer.C_in * layer.C_out < 65536:
+                ry, rdx, _ = oracle_passes(layer, c, x, w, dy)
+                errs += [rel(y, ry), rel(dx, rdx)]
+            say(f"    rel err {errs}")
+            assert max(errs) <= TOL, errs
