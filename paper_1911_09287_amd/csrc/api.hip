@@ -49,7 +49,10 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* ou
 
 bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
                             float2* part, hipStream_t s) {
-  bl_status_t st = launch_contract_tiled(p, which, A, Bm, O, part, s);
+  bl_status_t st = BL_ERR_UNSUPPORTED;
+  if (contract_is_thin(p, which)) st = launch_contract_thin(p, which, A, Bm, O, s);
+  if (st != BL_ERR_UNSUPPORTED) return st;
+  st = launch_contract_tiled(p, which, A, Bm, O, part, s);
   if (st != BL_ERR_UNSUPPORTED) return st;
   return launch_contract_generic(p, which, A, Bm, O, s);
 }

@@ -399,17 +399,13 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
 
   // the chirps, the filter's spectrum and the twiddles, built once per plan
   // in double precision on the host, are laid out in the table as in LDS
-  // (all of a thread's table loads in flight together: n_in + n_out <= M + 1)
-  {
-    constexpr int NT = 64 * kWaves1k, NTAB = (3 * M + 1 + NT - 1) / NT;
-    const int ntab = a.n_in + a.n_out + 2 * M;
-    float2 tv[NTAB];
+  // (all of a thread's table loads in flight together, and with the first
+  // round's input loads: n_in + n_out <= M + 1)
+  constexpr int NTAB = (3 * M + 1 + 64 * kWaves1k - 1) / (64 * kWaves1k);
+  const int ntab = a.n_in + a.n_out + 2 * M;
+  float2 tv[NTAB];
 #pragma unroll
-    for (int u = 0; u < NTAB; ++u) tv[u] = a.tab[min(tid + NT * u, ntab - 1)];
-#pragma unroll
-    for (int u = 0; u < NTAB; ++u)
-      if (tid + NT * u < ntab) pre[tid + NT * u] = tv[u];
-  }
+  for (int u = 0; u < NTAB; ++u) tv[u] = a.tab[min(tid + 64 * kWaves1k * u, ntab - 1)];
   auto exchange = [&](float2* v) {
 #pragma unroll
     for (int k = 0; k < 32; ++k) xb[k * 33 + h] = v[k];
@@ -532,7 +528,11 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     }
   };
 
-  if (PREF && j0 < j1) prefetch(j0, 0);
+  if constexpr (PREF) prefetch(j0, 0);  // every block has a job: j0 < j1
+  // (indices past the table are clamped like the loads: those threads store
+  // the last entry's own value again, so the stores need no branch)
+#pragma unroll
+  for (int u = 0; u < NTAB; ++u) pre[min(tid + NT * u, ntab - 1)] = tv[u];
   __syncthreads();  // tables in LDS
   for (unsigned base = j0; base < j1; base += NS) {
     const int nj = (int)min((unsigned)NS, j1 - base);  // jobs this round

@@ -70,6 +70,10 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
 enum class Contract { Forward, GradInput, GradWeight };
 bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
                             float2* part, hipStream_t s);
+// One of M, N, K at most 8: memory-bound, on the vector ALUs (thin.hip).
+bool contract_is_thin(const bl_conv_plan_s* p, Contract which);
+bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+                                 float2* O, hipStream_t s);
 // Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
 // generic one (any strides and sizes).
 bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,

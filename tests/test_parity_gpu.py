@@ -260,3 +260,26 @@ def test_wgrad_paths(torch):
                 errs += [rel(y, ry), rel(dx, rdx)]
             say(f"    rel err {errs}")
             assert max(errs) <= TOL, errs
+
+
+def test_thin_contractions(torch):
+    """Layers where a contraction size (batch, input or output channels) is at
+    most 8, which run the memory-bound vector-ALU contraction: lanes over
+    output columns with k split over a block's waves or not, strided and
+    contiguous operands, and one output row per wave with a cross-lane sum."""
+    cases = [
+        synth.Layer("thin_c1_1d", 1, 64, 1, 128, 200, 1, 8, (3, 4), "walk"),
+        synth.Layer("thin_c3_2d", 2, 4, 3, 64, 12, 12, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("thin_f2_2d", 2, 16, 64, 2, 10, 10, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("thin_n1_2d", 2, 1, 96, 80, 9, 9, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("thin_f5_1d", 1, 70, 100, 5, 90, 1, 5, (2, 2), "walk"),
+    ]
+    for i, layer in enumerate(cases):
+        for c in (0.0, 0.5):
+            say(f"[thin] {layer.name} c={c}")
+            x, w, dy = synth.random_inputs(layer, 1700 + i)
+            y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
+            ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            say(f"    rel err {errs}")
+            assert max(errs) <= TOL, errs
