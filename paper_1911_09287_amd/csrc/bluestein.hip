@@ -373,20 +373,43 @@ __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restric
 // (lane k holding element k + 32 m), so the pointwise product with the filter
 // spectrum needs no extra transpose: each Bluestein job costs one LDS
 // transpose per FFT instead of a pass per radix stage.
-// A block has 8 waves = 16 half-wave slots; each slot takes jobs (one series,
-// or a pair of series in the paired modes) of its block's contiguous range.
+//
+// Every wave runs its own jobs, with no block barrier once the tables are in
+// LDS: half-wave q of the wave with grid-wide index p takes job 2 p + q, then
+// job 2 (p + W) + q for W waves in the grid, and so on.  A wave's jobs are two
+// consecutive series (four in the paired modes), and the waves of a block
+// hold consecutive jobs, so the rows of a bin-major spectrum are read and
+// written in runs of consecutive series that meet in the L2.  A wave loads its
+// inputs (the next round's while it transforms the current one, when they fit
+// in 32 registers per lane), transforms and stores, and the waves of a CU fall
+// into different phases, overlapping memory traffic with arithmetic.
+// Inputs and outputs that run along the series (real samples) move straight
+// between HBM and registers; bin-major spectra pass through the wave's slot
+// buffers in LDS, where the conjugate-symmetric pairs of the paired modes are
+// formed or split.
 // ---------------------------------------------------------------------------
 constexpr int kWaves1k = 8;
-// Slot stride (complex): the 32 x 33 transpose tile plus 4 elements, so that
-// the same element of the 16 slots falls in different LDS banks when the
-// block moves series between HBM and the slots (one lane per slot).
+// Slot stride (complex): the 32 x 33 transpose tile plus 4 elements.
 constexpr int kXS = 32 * 33 + 4;
 
-template <int MODE, bool PREF>
+// Rows of input one lane loads per round (NR, a compile-time bound; loads past
+// the data are clamped to its last row and their values unused):
+//   MODE 0, 2: rows j of the series, element h + 32 j;
+//   MODE 1, 3: bins k = lane / 2 + 32 t, t < NR.
+// Floats per row: 1 (MODE 0), 2 (MODE 1, 2), 4 (MODE 3).  The next round is
+// prefetched when NR rows take at most 32 floats.
+template <int MODE>
+constexpr int floats_per_row() {
+  return MODE == 0 ? 1 : MODE == 3 ? 4 : 2;
+}
+
+template <int MODE, int NR>
 __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
-                                                               BlueGeom a, long jobs_per_block) {
+                                                               BlueGeom a, int wpb) {
   constexpr int M = 1024;
   constexpr bool PACK = MODE >= 2;
+  constexpr int FPR = floats_per_row<MODE>();
+  constexpr bool PREF = NR * FPR <= 32;
   extern __shared__ float2 sm[];
   float2* bufs = sm;                          // 16 slots x kXS
   float2* pre = bufs + 2 * kWaves1k * kXS;    // n_in
@@ -394,18 +417,21 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
   float2* F = post + a.n_out;                 // spectrum of the chirp filter (M)
   float2* TW = F + M;                         // TW[32 k + h] = w1024^{h k}
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int slot = lane >> 5, h = lane & 31;
-  float2* xb = bufs + (wave * 2 + slot) * kXS;
+  const int q = lane >> 5, h = lane & 31;
+  float2* xw = bufs + wave * 2 * kXS;  // the wave's two slot buffers
+  float2* xb = xw + q * kXS;           // this half-wave's
 
   // the chirps, the filter's spectrum and the twiddles, built once per plan
   // in double precision on the host, are laid out in the table as in LDS
   // (all of a thread's table loads in flight together, and with the first
   // round's input loads: n_in + n_out <= M + 1)
-  constexpr int NTAB = (3 * M + 1 + 64 * kWaves1k - 1) / (64 * kWaves1k);
+  constexpr int NT = 64 * kWaves1k;
+  constexpr int NTAB = (3 * M + 1 + NT - 1) / NT;
   const int ntab = a.n_in + a.n_out + 2 * M;
   float2 tv[NTAB];
 #pragma unroll
-  for (int u = 0; u < NTAB; ++u) tv[u] = a.tab[min(tid + 64 * kWaves1k * u, ntab - 1)];
+  for (int u = 0; u < NTAB; ++u) tv[u] = a.tab[min(tid + NT * u, ntab - 1)];
+
   auto exchange = [&](float2* v) {
 #pragma unroll
     for (int k = 0; k < 32; ++k) xb[k * 33 + h] = v[k];
@@ -424,194 +450,175 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     RegFft<32>::run(v);
   };
 
-
-  // Jobs go 16 at a time (one per slot).  Series data moves between HBM and
-  // the slot buffers cooperatively, so that every bin row of a bin-major
-  // spectrum is read or written as 16 (or 32 paired) consecutive series, and
-  // the slots run their transforms on LDS-resident data.  When a round's
-  // inputs fit in 32 floats per thread (PREF), the next round's are loaded
-  // into registers while the current round's transforms run.  Loads use
-  // clamped indices instead of branches so that all of a thread's loads are
-  // in flight together.
+  // element indices fit in 32 bits (checked on the host)
   const float* xin = static_cast<const float*>(in_);
   const float2* yin = static_cast<const float2*>(in_);
-  // element indices fit in 32 bits (checked on the host)
   const unsigned P = (unsigned)a.P;
   const unsigned jobs = PACK ? (P + 1) / 2 : P;
-  const unsigned j0 = blockIdx.x * (unsigned)jobs_per_block;
-  const unsigned j1 = min(jobs, j0 + (unsigned)jobs_per_block);
-  constexpr int NS = 2 * kWaves1k;  // slots per block
-  constexpr int NT = 64 * kWaves1k;
-  // a round's inputs pass through registers in chunks of 32 floats per thread
-  constexpr int PER = MODE == 0 ? NS : MODE == 2 ? 2 * NS : MODE == 1 ? 2 : 4;  // floats per index
-  constexpr int IPC = 32 / PER;  // indices per chunk
-  const int nch = MODE == 0 || MODE == 2 ? ((a.n_in + NT - 1) / NT + IPC - 1) / IPC
-                  : MODE == 1 ? ((a.n_in + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC
-                              : ((a.V + NT / NS - 1) / (NT / NS) + IPC - 1) / IPC;
-  float pf[32];
-  auto prefetch = [&](unsigned base, int c) {
-    if constexpr (MODE == 0 || MODE == 2) {
+  const unsigned pairs = (jobs + 1) / 2;  // rounds of the grid's waves: one job pair each
+  // waves past the first wpb of a block only help with the tables
+  const unsigned nw = gridDim.x * (unsigned)wpb;
+  const unsigned p0 = wave < wpb ? blockIdx.x * (unsigned)wpb + wave : pairs;
+  // series of the wave in round p: MODE 0/1: 2p + q; MODE 2/3: 4p .. 4p + 3
+  float pf[PREF ? NR * FPR : 1];
+  float2 v[32];
+  auto load = [&](unsigned p, float* dst) {
+    if constexpr (MODE == 0) {
+      const unsigned s = min(2 * p + q, P - 1);
 #pragma unroll
-      for (int r = 0; r < IPC; ++r) {
-        const int n = min(tid + NT * (c * IPC + r), a.n_in - 1);
+      for (int j = 0; j < NR; ++j) dst[j] = xin[s * (unsigned)a.n_in + min(h + 32 * j, a.n_in - 1)];
+    } else if constexpr (MODE == 2) {
+      const unsigned s1 = min(4 * p + 2 * q, P - 1), s2 = min(4 * p + 2 * q + 1, P - 1);
 #pragma unroll
-        for (int sl = 0; sl < NS; ++sl) {
-          const unsigned job = min(base + sl, j1 - 1);
-          if constexpr (MODE == 0) {
-            pf[r * PER + sl] = xin[job * (unsigned)a.n_in + n];
-          } else {
-            const unsigned s1 = 2 * job;
-            const unsigned s2 = min(s1 + 1, P - 1);
-            pf[r * PER + 2 * sl] = xin[s1 * (unsigned)a.n_in + n];
-            pf[r * PER + 2 * sl + 1] = s2 == s1 ? 0.f : xin[s2 * (unsigned)a.n_in + n];
-          }
-        }
+      for (int j = 0; j < NR; ++j) {
+        const int n = min(h + 32 * j, a.n_in - 1);
+        dst[2 * j] = xin[s1 * (unsigned)a.n_in + n];
+        dst[2 * j + 1] = xin[s2 * (unsigned)a.n_in + n];
+      }
+    } else if constexpr (MODE == 1) {
+      const unsigned s = min(2 * p + (lane & 1), P - 1);
+#pragma unroll
+      for (int t = 0; t < NR; ++t) {
+        const float2 y = yin[(unsigned)min((lane >> 1) + 32 * t, a.V - 1) * P + s];
+        dst[2 * t] = y.x;
+        dst[2 * t + 1] = y.y;
       }
     } else {
-      const unsigned job = min(base + (tid & (NS - 1)), j1 - 1);
-      const int rows = MODE == 1 ? a.n_in : a.V;
+      const unsigned s1 = min(4 * p + 2 * (lane & 1), P - 1), s2 = min(4 * p + 2 * (lane & 1) + 1, P - 1);
 #pragma unroll
-      for (int u = 0; u < IPC; ++u) {
-        const int n = min(tid / NS + (NT / NS) * (c * IPC + u), rows - 1);
-        if constexpr (MODE == 1) {
-          const float2 y = yin[n * P + job];
-          pf[PER * u] = y.x;
-          pf[PER * u + 1] = y.y;
-        } else {
-          const unsigned s1 = 2 * job;
-          const unsigned s2 = min(s1 + 1, P - 1);
-          const float2 y1 = yin[n * P + s1];
-          const float2 y2 = s2 == s1 ? make_float2(0.f, 0.f) : yin[n * P + s2];
-          pf[PER * u] = y1.x;
-          pf[PER * u + 1] = y1.y;
-          pf[PER * u + 2] = y2.x;
-          pf[PER * u + 3] = y2.y;
-        }
+      for (int t = 0; t < NR; ++t) {
+        const unsigned k = (unsigned)min((lane >> 1) + 32 * t, a.V - 1);
+        const float2 y1 = yin[k * P + s1], y2 = yin[k * P + s2];
+        dst[4 * t] = y1.x;
+        dst[4 * t + 1] = y1.y;
+        dst[4 * t + 2] = y2.x;
+        dst[4 * t + 3] = y2.y;
       }
     }
   };
-  // registers -> slot buffers, times the pre-chirp
-  auto commit = [&](int c) {
+  // loaded rows -> v (element h + 32 j of this half-wave's job), times the pre-chirp
+  auto stage = [&](unsigned p, const float* src) {
     if constexpr (MODE == 0 || MODE == 2) {
+      const bool two = MODE == 2 && 4 * p + 2 * q + 1 < P;
 #pragma unroll
-      for (int r = 0; r < IPC; ++r) {
-        const int n = tid + NT * (c * IPC + r);
-        if (n < a.n_in) {
-          const float2 pn = pre[n];
-#pragma unroll
-          for (int sl = 0; sl < NS; ++sl)
-            bufs[sl * kXS + n] = MODE == 0 ? cscale(pn, pf[r * PER + sl])
-                                           : cmul(make_float2(pf[r * PER + 2 * sl], pf[r * PER + 2 * sl + 1]), pn);
+      for (int j = 0; j < 32; ++j) {
+        const int n = h + 32 * j;
+        v[j] = make_float2(0.f, 0.f);
+        if (j < NR && n < a.n_in) {
+          const float2 z = MODE == 0 ? make_float2(src[j], 0.f) : make_float2(src[2 * j], two ? src[2 * j + 1] : 0.f);
+          v[j] = cmul(z, pre[n]);
         }
       }
     } else {
-      float2* dst = bufs + (tid & (NS - 1)) * kXS;
+      float2* dst = xw + (lane & 1) * kXS;
 #pragma unroll
-      for (int u = 0; u < IPC; ++u) {
-        const int n = tid / NS + (NT / NS) * (c * IPC + u);
-        if constexpr (MODE == 1) {
-          if (n < a.n_in) dst[n] = cmul(make_float2(pf[PER * u], pf[PER * u + 1]), pre[n]);
-        } else if (n < a.V) {
-          // two Hermitian spectra packed into one series: Z[k] = Y1[k] + i Y2[k]
-          // at index k + V - 1 for |k| < V, with Y[-k] = conj(Y[k])
-          const float2 y1 = make_float2(pf[PER * u], pf[PER * u + 1]);
-          const float2 y2 = make_float2(pf[PER * u + 2], pf[PER * u + 3]);
-          const int ip = a.V - 1 + n, im = a.V - 1 - n;
-          if (n == 0) {
-            dst[ip] = cmul(make_float2(y1.x, y2.x), pre[ip]);
+      for (int t = 0; t < NR; ++t) {
+        const int k = (lane >> 1) + 32 * t;
+        if (k < a.V) {
+          if constexpr (MODE == 1) {
+            dst[k] = cmul(make_float2(src[2 * t], src[2 * t + 1]), pre[k]);
           } else {
-            dst[ip] = cmul(make_float2(y1.x - y2.y, y1.y + y2.x), pre[ip]);
-            dst[im] = cmul(make_float2(y1.x + y2.y, y2.x - y1.y), pre[im]);
+            // two Hermitian spectra packed into one series: Z[k] = Y1[k] + i Y2[k]
+            // at index k + V - 1 for |k| < V, with Y[-k] = conj(Y[k])
+            const bool two = 4 * p + 2 * (lane & 1) + 1 < P;
+            const float2 y1 = make_float2(src[4 * t], src[4 * t + 1]);
+            const float2 y2 = two ? make_float2(src[4 * t + 2], src[4 * t + 3]) : make_float2(0.f, 0.f);
+            const int ip = a.V - 1 + k, im = a.V - 1 - k;
+            if (k == 0) {
+              dst[ip] = cmul(make_float2(y1.x, y2.x), pre[ip]);
+            } else {
+              dst[ip] = cmul(make_float2(y1.x - y2.y, y1.y + y2.x), pre[ip]);
+              dst[im] = cmul(make_float2(y1.x + y2.y, y2.x - y1.y), pre[im]);
+            }
           }
         }
       }
-    }
-  };
-
-  if constexpr (PREF) prefetch(j0, 0);  // every block has a job: j0 < j1
-  // (indices past the table are clamped like the loads: those threads store
-  // the last entry's own value again, so the stores need no branch)
-#pragma unroll
-  for (int u = 0; u < NTAB; ++u) pre[min(tid + NT * u, ntab - 1)] = tv[u];
-  __syncthreads();  // tables in LDS
-  for (unsigned base = j0; base < j1; base += NS) {
-    const int nj = (int)min((unsigned)NS, j1 - base);  // jobs this round
-    if constexpr (PREF) {
-      commit(0);
-    } else {
-      for (int c = 0; c < nch; ++c) {
-        prefetch(base, c);
-        commit(c);
-      }
-    }
-    __syncthreads();
-    if (PREF && base + NS < j1) prefetch(base + NS, 0);
-    if (2 * wave < nj) {  // waves with no job this round skip the transforms
-      float2 v[32];
+      wave_sync();
 #pragma unroll
       for (int j = 0; j < 32; ++j) {
         const int n = h + 32 * j;
         v[j] = n < a.n_in ? xb[n] : make_float2(0.f, 0.f);
       }
       wave_sync();
-      fft1k(v);
-      // inverse FFT of (A * F) as conj(FFT(conj(A * F)))
+    }
+  };
+
+  if constexpr (PREF) load(min(p0, pairs - 1), pf);  // clamped: no branch between these loads and the table's
+  // (indices past the table are clamped like the loads: those threads store
+  // the last entry's own value again, so the stores need no branch)
 #pragma unroll
-      for (int m = 0; m < 32; ++m) v[m] = cconj(cmul(v[m], F[h + 32 * m]));
-      fft1k(v);
+  for (int u = 0; u < NTAB; ++u) pre[min(tid + NT * u, ntab - 1)] = tv[u];
+  __syncthreads();  // tables in LDS; no block barrier follows
+
+  for (unsigned p = p0; p < pairs; p += nw) {
+    if constexpr (PREF) {
+      stage(p, pf);
+      load(p + nw < pairs ? p + nw : p, pf);  // the last round reloads its own rows (cache hits)
+    } else {
+      float ld[NR * FPR];
+      load(p, ld);
+      stage(p, ld);
+    }
+    fft1k(v);
+    // inverse FFT of (A * F) as conj(FFT(conj(A * F)))
+#pragma unroll
+    for (int m = 0; m < 32; ++m) v[m] = cconj(cmul(v[m], F[h + 32 * m]));
+    fft1k(v);
+    // v[m] -> output element i = h + 32 m: post[i] conj(v[m])
+    if constexpr (MODE == 1) {
+      const unsigned s = 2 * p + q;
+      if (s < P) {
+        float* dst = static_cast<float*>(out_) + s * (unsigned)a.n_out;
+#pragma unroll
+        for (int m = 0; m < 32; ++m) {
+          const int i = h + 32 * m;
+          if (i < a.n_out) dst[i] = cmul(post[i], cconj(v[m])).x;
+        }
+      }
+    } else if constexpr (MODE == 3) {
+      const unsigned s1 = 4 * p + 2 * q, s2 = s1 + 1;
+      if (s1 < P) {
+        float* d1 = static_cast<float*>(out_) + s1 * (unsigned)a.n_out;
+        float* d2 = d1 + a.n_out;
+#pragma unroll
+        for (int m = 0; m < 32; ++m) {
+          const int i = h + 32 * m;
+          if (i < a.n_out) {
+            const float2 r = cmul(post[i], cconj(v[m]));
+            d1[i] = r.x;
+            if (s2 < P) d2[i] = r.y;
+          }
+        }
+      }
+    } else {
 #pragma unroll
       for (int m = 0; m < 32; ++m) {
         const int i = h + 32 * m;
         if (i < a.n_out) xb[i] = cmul(post[i], cconj(v[m]));
       }
-    }
-    __syncthreads();
-    if constexpr (MODE == 0) {
-      const int sl = tid & (NS - 1);
-      if (sl < nj) {
-        float2* dst = static_cast<float2*>(out_) + base + sl;
-        const float2* src = bufs + sl * kXS;
-#pragma unroll 4
-        for (int i = tid / NS; i < a.n_out; i += NT / NS) dst[i * P] = src[i];
-      }
-    } else if constexpr (MODE == 1) {
-      float* dst = static_cast<float*>(out_) + base * (unsigned)a.n_out;
-      for (int i = tid; i < a.n_out; i += NT) {
-        float r[NS];
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i].x;
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl)
-          if (sl < nj) dst[sl * (unsigned)a.n_out + i] = r[sl];
-      }
-    } else if constexpr (MODE == 2) {
-      // Z[k] sits at index k + V - 1; the two series split by conjugate symmetry
-      const int q = tid & (2 * NS - 1);
-      const unsigned s = 2 * base + q;
-      if (q < 2 * nj && s < P) {
-        float2* dst = static_cast<float2*>(out_) + s;
-        const float2* src = bufs + (q >> 1) * kXS + (a.V - 1);
-#pragma unroll 4
-        for (int k = tid / (2 * NS); k < a.V; k += NT / (2 * NS)) {
-          const float2 zp = src[k], zm = cconj(src[-k]);
-          dst[k * P] = (q & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
+      wave_sync();
+      float2* X = static_cast<float2*>(out_);
+      if constexpr (MODE == 0) {
+        // bins i of the wave's two series, two consecutive series per bin row
+        const unsigned s = 2 * p + (lane & 1);
+        const float2* src = xw + (lane & 1) * kXS;
+        if (s < P) {
+          for (int i = lane >> 1; i < a.n_out; i += 32) X[(unsigned)i * P + s] = src[i];
+        }
+      } else {
+        // Z[k] sits at index k + V - 1; the two series of a job split by
+        // conjugate symmetry; four consecutive series per bin row
+        const unsigned s = 4 * p + (lane & 3);
+        const float2* src = xw + ((lane >> 1) & 1) * kXS + (a.V - 1);
+        if (s < P) {
+          for (int k = lane >> 2; k < a.V; k += 16) {
+            const float2 zp = src[k], zm = cconj(src[-k]);
+            X[(unsigned)k * P + s] = (lane & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
+          }
         }
       }
-    } else {
-      float* dst = static_cast<float*>(out_) + 2 * base * (unsigned)a.n_out;
-      const unsigned ns = min(P - 2 * base, 2u * nj);  // series of this round
-      for (int i = tid; i < a.n_out; i += NT) {
-        float2 r[NS];
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl) r[sl] = bufs[sl * kXS + i];
-#pragma unroll
-        for (int sl = 0; sl < NS; ++sl) {
-          if (2u * sl < ns) dst[2 * sl * (unsigned)a.n_out + i] = r[sl].x;
-          if (2u * sl + 1 < ns) dst[(2 * sl + 1) * (unsigned)a.n_out + i] = r[sl].y;
-        }
-      }
+      wave_sync();  // slot buffers free for the next round's transposes
     }
-    __syncthreads();  // slot buffers free for the next round
   }
 }
 
@@ -732,51 +739,58 @@ bl_status_t blue_tables(const bl_conv_plan_s* p, const BlueGeom& a, int mode, co
   return plan_table(p, key, [&](std::vector<float2>& host) { host_tables_1k(a, mode, host); }, out);
 }
 
-template <int MODE, bool PREF>
-bl_status_t launch_1k_cap(const BlueGeom& a, const void* in, void* out, const char* name, double bytes,
-                          hipStream_t s) {
+template <int MODE, int NR>
+bl_status_t launch_1k_nr(const BlueGeom& a, const void* in, void* out, const char* name, double bytes,
+                         hipStream_t s) {
   constexpr int M = 1024;
   const size_t lds = (size_t)(2 * kWaves1k * kXS + a.n_in + a.n_out + 2 * M) * sizeof(float2);
   if (lds > 160 * 1024) return BL_ERR_UNSUPPORTED;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, PREF>),
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return BL_ERR_HIP;
+  static bool attr_set[64] = {};
+  if (!attr_set[dev]) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, NR>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess)
       return BL_ERR_HIP;
-    attr_set = true;
+    attr_set[dev] = true;
   }
   const long jobs = (MODE >= 2) ? (a.P + 1) / 2 : a.P;
-  // contiguous job ranges per block: one block per CU at most, in multiples of
-  // the 16 jobs a block runs at a time when there are enough, else spread
-  // over more blocks in pairs (one wave each), as a round costs the same time
-  // however few of its slots are busy
-  long per = (jobs + device_cus() - 1) / device_cus();
-  per = per >= 16 ? (per + 15) / 16 * 16 : (per + 1) / 2 * 2;
-  const long blocks = (jobs + per - 1) / per;
-  const double ffts = (double)jobs;
-  const double flops = ffts * 2.0 * 5.0 * M * 10.0;
+  const long pairs = (jobs + 1) / 2;  // one job per half-wave
+  // one block per CU at most; when there is less than a full block of work
+  // per CU, fewer waves per block, so that the SIMDs are shared by fewer waves
+  const long cus = device_cus();
+  const int wpb = (int)std::min<long>(kWaves1k, (pairs + cus - 1) / cus);
+  const long blocks = std::min<long>(cus, (pairs + wpb - 1) / wpb);
+  const double flops = (double)jobs * 2.0 * 5.0 * M * 10.0;
   return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL((k_bluestein1k<MODE, PREF>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, e0, e1, 0, in, out,
-                       a, per);
+    hipExtLaunchKernelGGL((k_bluestein1k<MODE, NR>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, e0, e1, 0,
+                          in, out, a, wpb);
   });
 }
 
-// Rounds are prefetched when one round's inputs fit in 32 floats per thread.
+// NR: rows of input per lane as instantiated (the smallest that covers the
+// data); the kernel prefetches the next round when they fit in 32 floats.
 template <int MODE>
 bl_status_t launch_1k(const bl_conv_plan_s* p, const BlueGeom& a0, const void* in, void* out, const char* name,
                       double bytes, hipStream_t s) {
   // the kernel indexes its input and output with 32-bit element offsets
   const long rows = std::max<long>({(long)a0.n_in, (long)a0.n_out, 2L * a0.V});
-  if (a0.P * rows >= 2147483647L || a0.P * rows < 0) return BL_ERR_UNSUPPORTED;
+  if (a0.P < 1 || a0.P * rows >= 2147483647L || a0.P * rows < 0) return BL_ERR_UNSUPPORTED;
   BlueGeom a = a0;
   const bl_status_t ts = blue_tables(p, a, MODE, &a.tab);
   if (ts != BL_OK) return ts;
-  const int need = MODE == 0 ? 16 * ((a.n_in + 511) / 512)
-                   : MODE == 2 ? 32 * ((a.n_in + 511) / 512)
-                   : MODE == 1 ? 2 * ((a.n_in + 31) / 32)
-                               : 4 * ((a.V + 31) / 32);
-  if (need <= 32) return launch_1k_cap<MODE, true>(a, in, out, name, bytes, s);
-  return launch_1k_cap<MODE, false>(a, in, out, name, bytes, s);
+  if constexpr (MODE == 0 || MODE == 2) {
+    const int nr = (a.n_in + 31) / 32;
+    if (nr <= 16) return launch_1k_nr<MODE, 16>(a, in, out, name, bytes, s);
+    return launch_1k_nr<MODE, 32>(a, in, out, name, bytes, s);
+  } else {
+    const int nr = (a.V + 31) / 32;
+    if (nr <= 4) return launch_1k_nr<MODE, 4>(a, in, out, name, bytes, s);
+    if (nr <= 8) return launch_1k_nr<MODE, 8>(a, in, out, name, bytes, s);
+    if (nr <= 16) return launch_1k_nr<MODE, 16>(a, in, out, name, bytes, s);
+    if constexpr (MODE == 1) return launch_1k_nr<MODE, 32>(a, in, out, name, bytes, s);
+    return BL_ERR_UNSUPPORTED;
+  }
 }
 
 int fft_size_for(int need) {

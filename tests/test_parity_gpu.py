@@ -189,10 +189,10 @@ def test_1d_long_sequences(torch):
 
 
 def test_1d_many_series(torch):
-    """1-D layers with thousands of series, so that each block of the chirp-z
-    kernel runs several rounds of 16 jobs: inputs longer than 512 (rounds
-    staged in chunks) and shorter ones (next round loaded during the current
-    one), forward and inverse, paired and single series."""
+    """1-D layers with thousands of series, so that waves of the chirp-z kernel
+    run more than one round: inputs longer than 512 (each round loaded when it
+    starts) and shorter ones (the next round loaded during the current one),
+    forward and inverse, paired and single series."""
     cases = [
         (synth.Layer("rounds_long", 1, 64, 160, 4, 600, 1, 3, (1, 1), "walk"), 0.5),
         (synth.Layer("rounds_short", 1, 64, 160, 4, 300, 1, 5, (2, 2), "walk"), 0.5),
