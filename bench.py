@@ -5,6 +5,10 @@ of the workload at compression rate c, on synthetic inputs already resident
 in HBM.  Default workload: the 3-layer FCN time-series stack (batch 64,
 length 512; channels 1->128->256->128, filters 8/5/3, 'same' padding), c = 0.5.
 
+Kernels are launched from the host every step; with --graph each layer's
+three passes are captured once in a HIP graph and replayed instead (on this
+stack the replays measured slower than the direct launches).
+
 Prints ONE JSON line: value = TFLOP-equiv/s, where the equivalent work of a
 layer is that of the direct convolution, 3 passes x 2 N C_in C_out Lo K^d
 flops.  Also reported: ms per layer for every c of the workload, the
@@ -51,6 +55,8 @@ def parse():
     ap.add_argument("--config", type=int, default=2, help="workload index (1..5)")
     ap.add_argument("--c", type=float, default=0.5, help="compression rate of the headline value")
     ap.add_argument("--no-sweep", action="store_true", help="skip the per-c sweep")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay per-layer HIP graphs instead of launching every kernel from the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--table", default=None, help="also write a per-config/per-c table (JSON lines) here")
@@ -81,11 +87,27 @@ class Layer:
         self.plan.backward_weight(self.x, self.dy, self.dw, self.ws, flags=b.BL_REUSE_X | b.BL_REUSE_DY)
 
 
-def time_steps(torch, layers, steps, warmup):
-    """Median-free whole-loop timing: ms per step and ms per layer (events between layers)."""
-    for _ in range(warmup):
-        for L in layers:
+def capture(torch, layers):
+    """One HIP graph per layer holding its three passes.  The layers must have
+    run eagerly once (the plans' device tables are uploaded then)."""
+    graphs = []
+    for L in layers:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
             L.step()
+        graphs.append(g)
+    torch.cuda.synchronize()
+    return graphs
+
+
+def time_steps(torch, layers, steps, warmup, graphs=None):
+    """Median-free whole-loop timing: ms per step and ms per layer (events between
+    layers).  With `graphs` (from capture) each layer's passes are replayed from
+    its graph instead of launched one by one."""
+    run = [g.replay for g in graphs] if graphs else [L.step for L in layers]
+    for _ in range(warmup):
+        for r in run:
+            r()
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(layers) + 1)] for _ in range(steps)]
     t0 = torch.cuda.Event(enable_timing=True)
@@ -94,9 +116,9 @@ def time_steps(torch, layers, steps, warmup):
     wall0 = time.perf_counter()
     t0.record()
     for s in range(steps):
-        for i, L in enumerate(layers):
+        for i, r in enumerate(run):
             ev[s][i].record()
-            L.step()
+            r()
         ev[s][-1].record()
     t1.record()
     torch.cuda.synchronize()
@@ -238,8 +260,17 @@ def main():
     def build(c):
         return [Layer(torch, blconv, L, a, c, dev) for L, a in zip(cfg.layers, arrays)]
 
+    def graphs_for(Ls):
+        if not args.graph:
+            return None
+        for L in Ls:  # eager once: uploads the plans' device tables before capture
+            L.step()
+        torch.cuda.synchronize()
+        return capture(torch, Ls)
+
     layers = build(args.c)
-    ms, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup)
+    graphs = graphs_for(layers)
+    ms, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup, graphs)
     roof, kernels = roofline(torch, blconv, layers, max(1, min(args.steps, 10)))
     workload_key = f"config {args.config} c={args.c}"
     roof["traffic"] = measured_traffic(roof["kernel"], workload_key)
@@ -251,7 +282,7 @@ def main():
     if not args.no_sweep:
         for c in cfg.rates:
             Ls = layers if c == args.c else build(c)
-            m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup)
+            m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs if c == args.c else graphs_for(Ls))
             per_c.append({"c": c, "c_eff": [L.plan.c_eff for L in Ls], "ms_per_step": m,
                           "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12})
             del Ls
@@ -282,6 +313,7 @@ def main():
         "kernels": kernels,
         "per_c": per_c,
         "wall_s_timed": wall,
+        "launch": "hip_graph per layer" if args.graph else "eager",
     }
     print(json.dumps(out), flush=True)
 
