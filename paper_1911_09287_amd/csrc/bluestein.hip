@@ -500,13 +500,14 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
   auto stage = [&](unsigned p, const float* src) {
     if constexpr (MODE == 0 || MODE == 2) {
       const bool two = MODE == 2 && 4 * p + 2 * q + 1 < P;
+      const int jfull = a.n_in >> 5;  // rows complete for every lane (uniform branch)
+      const bool tail = h < (a.n_in & 31);
 #pragma unroll
       for (int j = 0; j < 32; ++j) {
-        const int n = h + 32 * j;
         v[j] = make_float2(0.f, 0.f);
-        if (j < NR && n < a.n_in) {
+        if (j < NR && (j < jfull || (j == jfull && tail))) {
           const float2 z = MODE == 0 ? make_float2(src[j], 0.f) : make_float2(src[2 * j], two ? src[2 * j + 1] : 0.f);
-          v[j] = cmul(z, pre[n]);
+          v[j] = cmul(z, pre[h + 32 * j]);
         }
       }
     } else {
@@ -565,36 +566,43 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
     for (int m = 0; m < 32; ++m) v[m] = cconj(cmul(v[m], F[h + 32 * m]));
     fft1k(v);
     // v[m] -> output element i = h + 32 m: post[i] conj(v[m])
+    // rows m < nfull are complete for every lane (a uniform branch); row
+    // nfull is partial
+    const int nfull = a.n_out >> 5;
+    const bool tail = h < (a.n_out & 31);
     if constexpr (MODE == 1) {
       const unsigned s = 2 * p + q;
       if (s < P) {
-        float* dst = static_cast<float*>(out_) + s * (unsigned)a.n_out;
+        float* dst = static_cast<float*>(out_) + s * (unsigned)a.n_out + h;
 #pragma unroll
         for (int m = 0; m < 32; ++m) {
-          const int i = h + 32 * m;
-          if (i < a.n_out) dst[i] = cmul(post[i], cconj(v[m])).x;
+          if (m < nfull || (m == nfull && tail)) dst[32 * m] = cmul(post[h + 32 * m], cconj(v[m])).x;
         }
       }
     } else if constexpr (MODE == 3) {
-      const unsigned s1 = 4 * p + 2 * q, s2 = s1 + 1;
-      if (s1 < P) {
-        float* d1 = static_cast<float*>(out_) + s1 * (unsigned)a.n_out;
-        float* d2 = d1 + a.n_out;
+      const unsigned s1 = 4 * p + 2 * q;
+      const bool two = s1 + 1 < P;
+      float* d1 = static_cast<float*>(out_) + s1 * (unsigned)a.n_out + h;
+      float* d2 = d1 + a.n_out;
+      if (two) {
 #pragma unroll
         for (int m = 0; m < 32; ++m) {
-          const int i = h + 32 * m;
-          if (i < a.n_out) {
-            const float2 r = cmul(post[i], cconj(v[m]));
-            d1[i] = r.x;
-            if (s2 < P) d2[i] = r.y;
+          if (m < nfull || (m == nfull && tail)) {
+            const float2 r = cmul(post[h + 32 * m], cconj(v[m]));
+            d1[32 * m] = r.x;
+            d2[32 * m] = r.y;
           }
+        }
+      } else if (s1 < P) {  // a lone last series
+#pragma unroll
+        for (int m = 0; m < 32; ++m) {
+          if (m < nfull || (m == nfull && tail)) d1[32 * m] = cmul(post[h + 32 * m], cconj(v[m])).x;
         }
       }
     } else {
 #pragma unroll
       for (int m = 0; m < 32; ++m) {
-        const int i = h + 32 * m;
-        if (i < a.n_out) xb[i] = cmul(post[i], cconj(v[m]));
+        if (m < nfull || (m == nfull && tail)) xb[h + 32 * m] = cmul(post[h + 32 * m], cconj(v[m]));
       }
       wave_sync();
       float2* X = static_cast<float2*>(out_);
