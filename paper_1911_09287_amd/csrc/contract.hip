@@ -48,7 +48,7 @@ constexpr int plane_floats() {
 }
 
 template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ>
-__global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
+__global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
                                                float2* __restrict__ O, CgemmArgs g) {
   constexpr int WM = BM / 2;   // rows per wave
   constexpr int WN = BN / 2;   // complex columns per wave
@@ -95,57 +95,68 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  // Operand positions of this thread's 16-byte vectors in a stage, and whether
+  // they lie inside the matrices.  Loads are unconditional (a vector outside
+  // reads the bin's first one, which always exists) and the zero fill happens
+  // when the registers are stored to LDS, so no branch separates a prefetch
+  // from the loads after it and the loads stay in flight across the stage.
+  auto a_pos = [&](int q, int& m, int& k) {
+    const int e = tid + 256 * q;
+    if (A_KC) { m = e >> 3; k = (e & 7) * 2; }
+    else { k = e / (BM / 2); m = (e - k * (BM / 2)) * 2; }
+  };
+  auto b_pos = [&](int q, int& k, int& n) {
+    const int e = tid + 256 * q;
+    if (B_NC) { k = e / (BN / 2); n = (e - k * (BN / 2)) * 2; }
+    else { n = e >> 3; k = (e & 7) * 2; }
+  };
   auto load = [&](int k0, float4* ra, float4* rb) {
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
-      const int e = tid + 256 * q;
       int m, k;
-      if (A_KC) { m = e >> 3; k = (e & 7) * 2; }
-      else { k = e / (BM / 2); m = (e - k * (BM / 2)) * 2; }
-      ra[q] = zero4;
-      if ((m0 + m < g.M) && (k0 + k < kend))
-        ra[q] = *reinterpret_cast<const float4*>(Ab + ((unsigned)(m0 + m) * g.sAm + (unsigned)(k0 + k) * g.sAk));
+      a_pos(q, m, k);
+      const bool in = (m0 + m < g.M) && (k0 + k < kend);
+      const unsigned off = in ? (unsigned)(m0 + m) * g.sAm + (unsigned)(k0 + k) * g.sAk : 0u;
+      ra[q] = *reinterpret_cast<const float4*>(Ab + off);
     }
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
-      const int e = tid + 256 * q;
       int k, n;
-      if (B_NC) { k = e / (BN / 2); n = (e - k * (BN / 2)) * 2; }
-      else { n = e >> 3; k = (e & 7) * 2; }
-      rb[q] = zero4;
-      if ((n0 + n < g.N) && (k0 + k < kend))
-        rb[q] = *reinterpret_cast<const float4*>(Bb + ((unsigned)(k0 + k) * g.sBk + (unsigned)(n0 + n) * g.sBn));
+      b_pos(q, k, n);
+      const bool in = (n0 + n < g.N) && (k0 + k < kend);
+      const unsigned off = in ? (unsigned)(k0 + k) * g.sBk + (unsigned)(n0 + n) * g.sBn : 0u;
+      rb[q] = *reinterpret_cast<const float4*>(Bb + off);
     }
   };
-  auto store = [&](int buf, const float4* ra, const float4* rb) {
+  auto store = [&](int buf, int k0, const float4* ra, const float4* rb) {
     float* a0 = As[buf];
     float* a1 = As[buf] + PA;
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
-      const int e = tid + 256 * q;
+      int m, k;
+      a_pos(q, m, k);
+      const float4 r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
       if (A_KC) {
-        const int m = e >> 3, k = (e & 7) * 2;
-        a0[k * SA + m] = ra[q].x; a1[k * SA + m] = ra[q].y;
-        a0[(k + 1) * SA + m] = ra[q].z; a1[(k + 1) * SA + m] = ra[q].w;
+        a0[k * SA + m] = r.x; a1[k * SA + m] = r.y;
+        a0[(k + 1) * SA + m] = r.z; a1[(k + 1) * SA + m] = r.w;
       } else {
-        const int k = e / (BM / 2), m = (e - k * (BM / 2)) * 2;
-        *reinterpret_cast<float2*>(a0 + k * SA + m) = make_float2(ra[q].x, ra[q].z);
-        *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(ra[q].y, ra[q].w);
+        *reinterpret_cast<float2*>(a0 + k * SA + m) = make_float2(r.x, r.z);
+        *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(r.y, r.w);
       }
     }
     float* b0 = Bs[buf];
     float* b1 = Bs[buf] + PB;
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
-      const int e = tid + 256 * q;
+      int k, n;
+      b_pos(q, k, n);
+      const float4 r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
       if (B_NC) {
-        const int k = e / (BN / 2), n = (e - k * (BN / 2)) * 2;
-        *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(rb[q].x, rb[q].z);
-        *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(rb[q].y, rb[q].w);
+        *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(r.x, r.z);
+        *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(r.y, r.w);
       } else {
-        const int n = e >> 3, k = (e & 7) * 2;
-        b0[k * SB + n] = rb[q].x; b1[k * SB + n] = rb[q].y;
-        b0[(k + 1) * SB + n] = rb[q].z; b1[(k + 1) * SB + n] = rb[q].w;
+        b0[k * SB + n] = r.x; b1[k * SB + n] = r.y;
+        b0[(k + 1) * SB + n] = r.z; b1[(k + 1) * SB + n] = r.w;
       }
     }
   };
@@ -171,24 +182,28 @@ __global__ __launch_bounds__(256) void k_cgemm(const float2* __restrict__ A, con
   };
 
   // stage st sits in LDS buffer st % 2; register set st % 2 receives stage
-  // st + 2 while stage st + 1 (in the other set) waits to be stored
+  // st + 2 while stage st + 1 (in the other set) waits to be stored.  The loop
+  // body has no branch, so the compiler's wait before each store covers only
+  // the loads of the stage being stored: a stage index past the last is
+  // clamped for the load (a repeated, cached read) and zero-filled by the
+  // store; with an odd number of stages the last pair's second stage is such
+  // an all-zero stage (its MFMAs add nothing).
   const int nst = (kend - kbeg + kBK - 1) / kBK;
+  auto kof = [&](int st) { return kbeg + min(st, nst - 1) * kBK; };
   float4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
-  load(kbeg, ra0, rb0);
-  if (nst > 1) load(kbeg + kBK, ra1, rb1);
-  store(0, ra0, rb0);
+  load(kof(0), ra0, rb0);
+  load(kof(1), ra1, rb1);
+  store(0, kbeg, ra0, rb0);
   __syncthreads();
-  for (int st = 0; st < nst; st += 2) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int cs = st + h;
-      if (cs < nst) {
-        if (cs + 2 < nst) load(kbeg + (cs + 2) * kBK, h ? ra1 : ra0, h ? rb1 : rb0);
-        compute(h);
-        if (cs + 1 < nst) store(h ^ 1, h ? ra0 : ra1, h ? rb0 : rb1);
-      }
-      __syncthreads();
-    }
+  for (int cs = 0; cs < nst; cs += 2) {
+    load(kof(cs + 2), ra0, rb0);
+    compute(0);
+    store(1, kbeg + (cs + 1) * kBK, ra1, rb1);
+    __syncthreads();
+    load(kof(cs + 3), ra1, rb1);
+    compute(1);
+    store(0, kbeg + (cs + 2) * kBK, ra0, rb0);
+    __syncthreads();
   }
 
   // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
