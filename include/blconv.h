@@ -48,8 +48,9 @@
  * workspace ws).  Creating and querying a plan makes no HIP call.  The plan
  * also owns small device tables, built in double precision on the host: those
  * of its 1-D transforms (chirps, the chirp filter's spectrum and twiddles:
- * under 100 KB) and the inverse-DFT weights of the weight gradient (8 K^2
- * bytes per kept bin, K^2 -> K in 1-D).  The first compute call of
+ * under 100 KB), the roots of unity of the filter DFT (8 (L_h + L_w) bytes)
+ * and the inverse-DFT weights of the weight gradient (8 K^2 bytes per kept
+ * bin, K^2 -> K in 1-D).  The first compute call of
  * the plan that needs a table on a device uploads it there; that call
  * allocates and copies synchronously, so make each kind of call once outside
  * stream capture before capturing it.  Every other compute call allocates nothing,

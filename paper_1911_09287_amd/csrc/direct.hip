@@ -14,6 +14,7 @@
 //   contract         per kept bin, a complex matrix product over channels (the
 //                    Hadamard product fused with the channel sum, Sec. 3.3).
 #include <algorithm>
+#include <cmath>
 
 #include "common.hpp"
 
@@ -202,13 +203,14 @@ struct FiltGeom {
 };
 
 template <int KH, int KW>
-__global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, float2* __restrict__ out,
-                                                        FiltGeom g) {
+__global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, const float2* __restrict__ roots,
+                                                        float2* __restrict__ out, FiltGeom g) {
+  // roots: e^{-2 pi i k / Lh} (k < Lh) then e^{-2 pi i k / Lw} (k < Lw), from
+  // a table built once per plan
   extern __shared__ float2 smem[];
   float2* twh = smem;
   float2* tww = twh + g.Lh;
-  fill_roots(twh, g.Lh, -1.0);
-  fill_roots(tww, g.Lw, -1.0);
+  for (int k = threadIdx.x; k < g.Lh + g.Lw; k += blockDim.x) smem[k] = roots[k];
   __syncthreads();
   const long CF = (long)g.C * g.F;
   const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;  // q = c * F + f
@@ -394,11 +396,11 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restri
 // bins, its four waves each reducing a quarter of the bins; the quarters are
 // added in a fixed order through LDS and written straight to dw, so no
 // partial sums leave the block.  E comes from a table built once per plan.
-template <int TMAX>
-__global__ __launch_bounds__(kThreads) void k_wgrad_wide(const float2* __restrict__ DW, const float2* __restrict__ Et,
-                                                         float* __restrict__ dw, WgradGeom g) {
+template <int TMAX, int NW>
+__global__ __launch_bounds__(64 * NW) void k_wgrad_wide(const float2* __restrict__ DW, const float2* __restrict__ Et,
+                                                        float* __restrict__ dw, WgradGeom g) {
   extern __shared__ float2 E[];  // [kept][TMAX], zero beyond T: the bin loop has no branches
-  __shared__ float red[4][64][TMAX];
+  __shared__ float red[NW][64][TMAX];
   const int B = g.R * g.V;
   for (int e = threadIdx.x; e < B * TMAX; e += blockDim.x) {
     const int bb = e / TMAX, t = e - bb * TMAX;
@@ -409,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_wide(const float2* __restric
   const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
   const unsigned q = blockIdx.x * 64u + lane;
   const bool valid = q < Q;
-  const int bb0 = grp * B / 4, bb1 = (grp + 1) * B / 4;
+  const int bb0 = grp * B / NW, bb1 = (grp + 1) * B / NW;
   float acc[TMAX];
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
@@ -435,8 +437,12 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_wide(const float2* __restric
     const int c = (int)(q / g.F), f = (int)(q % g.F);
     float* o = dw + ((size_t)f * g.C + c) * g.T;
 #pragma unroll
-    for (int t = 0; t < TMAX; ++t)
-      if (t < g.T) o[t] = ((red[0][lane][t] + red[1][lane][t]) + red[2][lane][t]) + red[3][lane][t];
+    for (int t = 0; t < TMAX; ++t) {
+      float sum = red[0][lane][t];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sum += red[w][lane][t];
+      if (t < g.T) o[t] = sum;
+    }
   }
 }
 
@@ -606,8 +612,23 @@ bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, fl
   X(1, 1) X(1, 2) X(1, 3) X(1, 4) X(1, 5) X(1, 6) X(1, 7) X(1, 8) \
   X(2, 2) X(3, 3) X(4, 4) X(5, 5) X(6, 6) X(7, 7) X(8, 8)
 
+// e^{-2 pi i k / Lh} for k < Lh, then e^{-2 pi i k / Lw} for k < Lw, in double precision.
+void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
+  const double pi = 3.141592653589793238462643383279502884;
+  out.clear();
+  for (int L : {p->Lh, p->Lw})
+    for (int k = 0; k < L; ++k) {
+      const double a = 2.0 * pi * (double)k / (double)L;
+      out.push_back(make_float2((float)std::cos(a), (float)(-std::sin(a))));
+    }
+}
+
 bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* out, hipStream_t s) {
   FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
+  const float2* roots = nullptr;
+  const std::vector<long> key{3, p->Lh, p->Lw};
+  const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_filt_roots(p, h); }, &roots);
+  if (ts != BL_OK) return ts;
   const long CF = (long)p->Cin * p->Cout;
   const int B = p->R * p->V;
   const long xblocks = (CF + kThreads - 1) / kThreads;
@@ -621,7 +642,7 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* ou
 #define X(a, b)                                                                                 \
   if (p->Kh == a && p->Kw == b)                                                                 \
     return timed_launch("spec_filt", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {        \
-      hipExtLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, out, g);        \
+      hipExtLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, roots, out, g); \
     });
   BL_FILT_CASES(X)
 #undef X
@@ -644,25 +665,35 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   if (Q / 64 >= 256 && p->Cout <= 256 && g.T <= 16 && (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&
       Q < 2147483647L) {
     const size_t lds = (size_t)B * tmax_w * sizeof(float2);
-    const dim3 grid((unsigned)((Q + 63) / 64));
+    const long blocks = (Q + 63) / 64;
+    // at most one block per CU: 16 waves per block, each over a sixteenth of
+    // the bins, so that every SIMD still holds several waves (measured: with
+    // 512 blocks, 4 waves per block are faster)
+    const bool many = blocks <= 256;
     const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
-    auto go = [&](auto kern) {
+    auto go = [&](auto kern, int nw) {
+      // the static reduction buffer plus up to kWgradSliceLds of weights can
+      // pass 64 KB of LDS: allow that once per kernel and device
+      static bool allowed[64] = {};
+      int dev = 0;
+      if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return BL_ERR_HIP;
+      if (!allowed[dev]) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)kWgradSliceLds) != hipSuccess)
+          return BL_ERR_HIP;
+        allowed[dev] = true;
+      }
       return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, e0, e1, 0, DW, Et, dw, g);
+        hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * nw), lds, s, e0, e1, 0, DW, Et, dw, g);
       });
     };
+#define BL_WIDE(t) \
+  case t: return many ? go(k_wgrad_wide<t, 16>, 16) : go(k_wgrad_wide<t, 4>, 4);
     switch (g.T) {
-      case 1: return go(k_wgrad_wide<1>);
-      case 2: return go(k_wgrad_wide<2>);
-      case 3: return go(k_wgrad_wide<3>);
-      case 4: return go(k_wgrad_wide<4>);
-      case 5: return go(k_wgrad_wide<5>);
-      case 6: return go(k_wgrad_wide<6>);
-      case 7: return go(k_wgrad_wide<7>);
-      case 8: return go(k_wgrad_wide<8>);
-      case 9: return go(k_wgrad_wide<9>);
-      default: return go(k_wgrad_wide<16>);
+      BL_WIDE(1) BL_WIDE(2) BL_WIDE(3) BL_WIDE(4) BL_WIDE(5) BL_WIDE(6) BL_WIDE(7) BL_WIDE(8) BL_WIDE(9)
+      default: return many ? go(k_wgrad_wide<16, 16>, 16) : go(k_wgrad_wide<16, 4>, 4);
     }
+#undef BL_WIDE
   }
   g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices
   g.bins_per_chunk = p->wg_bins;

@@ -1,5 +1,6 @@
 // Small device tables owned by a plan (chirps and filter spectra of the 1-D
-// transforms, inverse-DFT weights of the weight gradient).  Each is built on
+// transforms, roots of unity of the filter DFT, inverse-DFT weights of the
+// weight gradient).  Each is built on
 // the host in double precision and uploaded by the plan's first call that
 // needs it on a device; the plan frees them when it is destroyed.
 #include <cstring>
