@@ -653,16 +653,18 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept;
-  // wide layers: at least 256 blocks of 64 pairs, taps and table that fit
-  // (rows of at most 256 output channels: wider rows write dw better from
-  // the tiled kernel below)
+  // one pass over all bins when there are at least 256 blocks of 64 pairs,
+  // or few bins (at most 256: a sixteenth per wave), and taps and table fit
+  // (rows of at most 256 output channels: wider rows write dw better from the
+  // tiled kernel below); otherwise bin slices and a fixed-order sum
   if (g.T > 64) return BL_ERR_UNSUPPORTED;
   const float2* Et = nullptr;  // E[bin][t], built once per plan
   const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
   const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
   if (ts != BL_OK) return ts;
   const int tmax_w = g.T <= 9 ? g.T : 16;
-  if (Q / 64 >= 256 && p->Cout <= 256 && g.T <= 16 && (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&
+  if ((Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && g.T <= 16 &&
+      (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&
       Q < 2147483647L) {
     const size_t lds = (size_t)B * tmax_w * sizeof(float2);
     const long blocks = (Q + 63) / 64;
