@@ -321,3 +321,96 @@ def plan_info(ndim, L, c):
     m, t, r_h, r_w = mask_2d(L[0], L[1], c)
     kept, total = int(m.sum()), m.size
     return r_h, r_w, kept, total, 1.0 - kept / total
+
+
+# ----------------------------------------------------------------------------
+# Energy-based (adaptive) compression, coarse-grained (Sec. 4.1 and the
+# supplementary section "Compression Based on Preserved Energy")
+# ----------------------------------------------------------------------------
+#
+# The paper's second compression scheme chooses how much of the band to keep
+# from the energy the band preserves, instead of from a fixed rate: starting
+# at the DC component, whole L-shaped layers of rows and columns are added
+# until the kept coefficients hold the requested fraction of the energy.  The
+# energy is that of the layer's input (Sec. 4.1 defines it for an input tensor
+# x through Parseval's theorem).  Readings taken here (listed in the design
+# notes): E1 the energy of a half-plane bin counts twice unless the bin is its
+# own conjugate partner (column 0, and the Nyquist column of an even width):
+# Parseval on the half plane (reading R7); E2 the band kept is the smallest
+# L-shaped band (the most peeled layers t) whose energy is at least the
+# requested fraction of the total ("preserve at least E"); E3 an input with no
+# energy preserves any fraction with any band: the most layers are peeled.
+# Parity: pinned by Parseval, by the band energy evaluated in the signal
+# domain with direct-sum DFTs, and by single-frequency and constant inputs.
+
+
+def parseval_weights(Lw: int) -> np.ndarray:
+    """h_v over the half-plane columns v = 0 .. Lw//2 (reading E1 / R7)."""
+    h = np.full(Lw // 2 + 1, 2.0)
+    h[0] = 1.0
+    if Lw % 2 == 0:
+        h[-1] = 1.0
+    return h
+
+
+def bin_energy_2d(x, pad, fft=None) -> np.ndarray:
+    """[Lh][Lw//2+1]: h_v * sum over samples and channels of |X[n,c,u,v]|^2,
+    X the spectrum of the input placed at (pad top, pad left) of the grid."""
+    N, C, H, W = x.shape
+    Lh, Lw = (H + pad[0] + pad[1], W + pad[2] + pad[3]) if fft is None else fft
+    X = _rfft2(_embed(np.asarray(x, np.float64), Lh, Lw, pad[0], pad[2]))
+    return parseval_weights(Lw)[None, :] * (np.abs(X) ** 2).sum(axis=(0, 1))
+
+
+def bin_energy_1d(x, pad, fft=None) -> np.ndarray:
+    """[L//2+1]: h_v * sum over series of |X[n,c,v]|^2."""
+    N, C, Lx = x.shape
+    L = Lx + pad[0] + pad[1] if fft is None else fft
+    X = np.fft.rfft(_embed1(np.asarray(x, np.float64), L, pad[0]))
+    return parseval_weights(L) * (np.abs(X) ** 2).sum(axis=(0, 1))
+
+
+def last_layer_kept(ndim, L) -> np.ndarray:
+    """For every half-plane bin, the most layers t that can be peeled with the
+    bin still kept (from the band definition, t by t)."""
+    if ndim == 1:
+        t_max = L // 2
+        out = np.full(L // 2 + 1, -1, dtype=np.int64)
+        for t in range(t_max + 1):
+            out[band_1d(L, t).astype(bool)] = t
+        return out
+    Lh, Lw = L
+    t_max = min(Lh // 2, Lw // 2)
+    out = np.full((Lh, Lw // 2 + 1), -1, dtype=np.int64)
+    for t in range(t_max + 1):
+        out[band_2d(Lh, Lw, t).astype(bool)] = t
+    return out
+
+
+def preserved_fractions(E: np.ndarray, last: np.ndarray) -> np.ndarray:
+    """f[t] = energy of the bins kept after peeling t layers / total energy
+    (1 for every t when the total is zero, reading E3)."""
+    t_max = int(last.max())
+    total = float(E.sum())
+    kept = np.array([float(E[last >= t].sum()) for t in range(t_max + 1)])
+    return np.ones(t_max + 1) if total == 0.0 else kept / total
+
+
+def layers_for_energy(fraction: float, f: np.ndarray) -> int:
+    """Reading E2: the most layers t whose band keeps at least `fraction`."""
+    return max(t for t in range(len(f)) if f[t] >= fraction)
+
+
+def energy_rate(x, pad, fraction, fft=None):
+    """Band chosen for input x so that at least `fraction` of its energy is
+    kept: dict(t, kept, total, c_eff, preserved, fractions)."""
+    if x.ndim == 3:
+        L = x.shape[-1] + pad[0] + pad[1] if fft is None else fft
+        E, last = bin_energy_1d(x, pad, fft), last_layer_kept(1, L)
+    else:
+        Lh, Lw = (x.shape[-2] + pad[0] + pad[1], x.shape[-1] + pad[2] + pad[3]) if fft is None else fft
+        E, last = bin_energy_2d(x, pad, fft), last_layer_kept(2, (Lh, Lw))
+    f = preserved_fractions(E, last)
+    t = layers_for_energy(fraction, f)
+    kept, total = int((last >= t).sum()), last.size
+    return dict(t=t, kept=kept, total=total, c_eff=1.0 - kept / total, preserved=float(f[t]), fractions=f)

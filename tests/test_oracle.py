@@ -332,3 +332,99 @@ def test_kept_spectrum_layout_matches_full_spectrum():
     full = br.np.einsum("ui,ncij,vj->ncuv", br.dft_matrix(Lh), emb, br.dft_matrix(Lw))
     for b, (u, v) in enumerate(bins):
         assert np.abs(S[b] - full[:, :, u, v].ravel()).max() < 1e-10
+
+
+# ------------------------------------------- energy-based compression --
+
+
+def _grid_energy_rate(x, pad, fraction):
+    r = bo.energy_rate(x, pad, fraction)
+    return r["t"], r["fractions"]
+
+
+def test_energy_parseval_total():
+    """The half-plane bin energies sum to Lh Lw times the input's energy
+    (Parseval; zero padding adds no energy)."""
+    rng = np.random.default_rng(31)
+    for shape, pad in (((2, 3, 8, 8), (1, 1, 1, 1)), ((1, 2, 7, 9), (0, 2, 1, 0)), ((3, 1, 5, 4), (0, 0, 0, 0))):
+        x = rng.standard_normal(shape)
+        Lh, Lw = shape[2] + pad[0] + pad[1], shape[3] + pad[2] + pad[3]
+        E = bo.bin_energy_2d(x, pad)
+        assert abs(E.sum() - Lh * Lw * (x ** 2).sum()) < 1e-10 * E.sum()
+    for shape, pad in (((2, 3, 30), (2, 2)), ((1, 1, 11), (0, 3))):
+        x = rng.standard_normal(shape)
+        L = shape[2] + pad[0] + pad[1]
+        E = bo.bin_energy_1d(x, pad)
+        assert abs(E.sum() - L * (x ** 2).sum()) < 1e-10 * E.sum()
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_energy_fractions_match_signal_domain(ndim):
+    """f[t] is the energy of the input band-limited to t peeled layers, taken
+    in the signal domain with direct-sum DFTs over the full-plane band,
+    divided by the input's energy."""
+    rng = np.random.default_rng(32 + ndim)
+    if ndim == 2:
+        for shape, pad in (((2, 2, 6, 7), (1, 0, 2, 1)), ((1, 3, 8, 8), (1, 1, 1, 1))):
+            x = rng.standard_normal(shape)
+            Lh, Lw = shape[2] + pad[0] + pad[1], shape[3] + pad[2] + pad[3]
+            _, f = _grid_energy_rate(x, pad, 0.5)
+            z = np.zeros(shape[:2] + (Lh, Lw))
+            z[..., pad[0]:pad[0] + shape[2], pad[2]:pad[2] + shape[3]] = x
+            for t in range(min(Lh // 2, Lw // 2) + 1):
+                lp, _ = br.lowpass_2d(z, br.full_band_2d(Lh, Lw, t))
+                assert abs(f[t] - (lp ** 2).sum() / (z ** 2).sum()) < 1e-10
+    else:
+        for shape, pad in (((2, 2, 13), (2, 1)), ((1, 3, 16), (0, 0))):
+            x = rng.standard_normal(shape)
+            L = shape[2] + pad[0] + pad[1]
+            _, f = _grid_energy_rate(x, pad, 0.5)
+            z = np.zeros(shape[:2] + (L,))
+            z[..., pad[0]:pad[0] + shape[2]] = x
+            for t in range(L // 2 + 1):
+                lp, _ = br.lowpass_1d(z, L // 2 - t)
+                assert abs(f[t] - (lp ** 2).sum() / (z ** 2).sum()) < 1e-10
+
+
+def test_energy_single_frequency():
+    """A cosine at one frequency has all its energy in one bin and its
+    conjugate partner, so the band keeps it all while that bin is kept and
+    none of it after: the chosen band is the one that peels the most layers
+    and still keeps the bin, min(Lh/2 - |s(u0)|, Lw/2 - v0), for any fraction."""
+    Lh, Lw = 10, 12
+    i, j = np.meshgrid(np.arange(Lh), np.arange(Lw), indexing="ij")
+    for u0, v0 in ((3, 2), (Lh - 3, 2), (0, 4), (1, 0), (5, 1)):
+        x = np.cos(2 * np.pi * (u0 * i / Lh + v0 * j / Lw))[None, None]
+        s = u0 if u0 <= Lh // 2 else u0 - Lh
+        expect = min(Lh // 2 - abs(s), Lw // 2 - v0)
+        for fraction in (0.3, 0.9, 1.0):
+            t, f = _grid_energy_rate(x, (0, 0, 0, 0), fraction)
+            assert t == expect, (u0, v0, fraction, t, expect)
+        assert np.all(np.abs(f[: expect + 1] - 1.0) < 1e-12) and np.all(np.abs(f[expect + 1:]) < 1e-12)
+    L = 20
+    n = np.arange(L)
+    for v0 in (0, 3, 10):
+        x = np.cos(2 * np.pi * v0 * n / L)[None, None]
+        t, f = _grid_energy_rate(x, (0, 0), 0.5)
+        assert t == L // 2 - v0
+
+
+def test_energy_constant_and_zero_inputs():
+    """A constant input on the whole grid has all its energy at DC: every band
+    keeps it, so the most layers are peeled; an all-zero input likewise
+    (reading E3)."""
+    for x in (np.full((1, 2, 8, 8), 3.0), np.zeros((1, 1, 6, 8))):
+        t, f = _grid_energy_rate(x, (0, 0, 0, 0), 0.999)
+        assert t == min(x.shape[2] // 2, x.shape[3] // 2) and np.all(np.abs(f - 1.0) < 1e-12)
+    t, _ = _grid_energy_rate(np.full((2, 1, 9), -1.5), (0, 0), 0.999)
+    assert t == 9 // 2
+
+
+def test_energy_fractions_monotone():
+    rng = np.random.default_rng(34)
+    for shape, pad in (((2, 3, 12, 12), (1, 1, 1, 1)), ((1, 4, 9, 5), (2, 0, 0, 1))):
+        x = rng.standard_normal(shape)
+        r = bo.energy_rate(x, pad, 0.8)
+        f = r["fractions"]
+        assert f[0] == 1.0 and np.all(np.diff(f) <= 1e-15)
+        assert r["preserved"] >= 0.8 and (r["t"] == len(f) - 1 or f[r["t"] + 1] < 0.8)
