@@ -155,6 +155,34 @@ bl_status_t bl_conv_backward_input(bl_conv_plan_t plan, const float* dy, const f
 bl_status_t bl_conv_backward_weight(bl_conv_plan_t plan, const float* x, const float* dy, float* dw,
                                     void* ws, unsigned flags, void* stream);
 
+/* Energy-based (adaptive) compression, coarse-grained (Sec. 4.1; supplementary
+ * "Compression Based on Preserved Energy"): the band is grown from the DC
+ * component in whole L-shaped layers until it holds a requested fraction of the
+ * energy of the layer's input.
+ *
+ * bl_conv_input_energy writes, for every kept bin b of the plan (in the order of
+ * bl_conv_plan_get_bins), energy[b] = h_v * sum over samples and input channels
+ * of |X[b]|^2, in fp64, to the device array `energy` of `kept` doubles; h_v = 1 in
+ * column 0 and in the Nyquist column of an even width, else 2 (Parseval on the
+ * half plane), so with a plan of rate 0 the energies sum to L_h L_w times the
+ * energy of x.  X, the input spectrum, is computed from x and left in ws
+ * (BL_REUSE_X: read from ws; x may then be NULL).  One kernel per call on
+ * `stream`, summing in a fixed order (results do not depend on scheduling). */
+bl_status_t bl_conv_input_energy(bl_conv_plan_t plan, const float* x, void* ws, unsigned flags,
+                                 double* energy, void* stream);
+
+/* Host only.  From bin energies in the plan's bin order (host memory, n = kept,
+ * e.g. bl_conv_input_energy's output copied back), the band that keeps at least
+ * `fraction` (0 < fraction <= 1) of their total: the most layers t that can be
+ * peeled, counted from the full half plane (t >= the plan's own), with the bins
+ * it keeps.  Outputs (any may be NULL): t; the rate c for which
+ * bl_conv_plan_create chooses exactly that band; the fraction it preserves.
+ * With a plan of rate 0 the fractions are of the input's whole energy.  Energies
+ * that are all zero keep any fraction: the most layers are peeled.  Negative,
+ * infinite or NaN energies are BL_ERR_INVALID_ARG. */
+bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t plan, const double* energy, size_t n, double fraction,
+                                    int* t, double* c, double* preserved);
+
 const char* bl_status_string(bl_status_t status);
 
 /* Per-kernel timing, for measurement tools.  While enabled, every kernel the

@@ -26,7 +26,8 @@ EXPORTED = (
     "bl_conv_plan_create", "bl_conv_plan_destroy", "bl_conv_plan_info", "bl_conv_plan_get_mask",
     "bl_conv_plan_get_bins", "bl_conv_workspace_size", "bl_conv_workspace_layout", "bl_conv_forward",
     "bl_conv_backward_input", "bl_conv_backward_weight", "bl_status_string", "bl_profile_begin",
-    "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release",
+    "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release", "bl_conv_input_energy",
+    "bl_conv_rate_for_energy",
 )
 
 
@@ -71,6 +72,8 @@ def load():
     lib.bl_conv_workspace_layout.argtypes = [P, ctypes.POINTER(S), ctypes.POINTER(S), ctypes.POINTER(S)]
     for name in ("bl_conv_forward", "bl_conv_backward_input", "bl_conv_backward_weight"):
         getattr(lib, name).argtypes = [P, P, P, P, P, U, P]
+    lib.bl_conv_input_energy.argtypes = [P, P, P, U, P, P]
+    lib.bl_conv_rate_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D)]
     lib.bl_status_string.argtypes = [I]
     lib.bl_status_string.restype = ctypes.c_char_p
     lib.bl_profile_begin.argtypes = [I]
@@ -211,6 +214,29 @@ class Plan:
         _check("bl_conv_backward_weight", self._lib.bl_conv_backward_weight(
             self._h, self._ptr(x, self.x_shape(), "x"), self._ptr(dy, self.y_shape(), "dy"),
             self._ptr(dw, self.w_shape(), "dw"), self._ws(ws), flags, self._stream(stream)))
+
+    def input_energy(self, x, ws, energy=None, flags=0, stream=None):
+        """Per kept bin h_v * sum |X|^2 of the input spectrum (fp64, on the GPU);
+        `energy` (float64 GPU tensor of kept elements) is allocated if None."""
+        import torch
+        if energy is None:
+            energy = torch.empty(self.kept, dtype=torch.float64, device=ws.device)
+        if not (energy.is_cuda and energy.dtype == torch.float64 and energy.is_contiguous()
+                and energy.numel() == self.kept):
+            raise ValueError("energy must be a contiguous float64 GPU tensor of kept elements")
+        _check("bl_conv_input_energy", self._lib.bl_conv_input_energy(
+            self._h, self._ptr(x, self.x_shape(), "x"), self._ws(ws), flags, energy.data_ptr(),
+            self._stream(stream)))
+        return energy
+
+    def rate_for_energy(self, energy, fraction):
+        """(t, c, preserved) of the band keeping at least `fraction` of the bin
+        energies (host array in the plan's bin order)."""
+        e = np.ascontiguousarray(np.asarray(energy, dtype=np.float64))
+        t, c, f = ctypes.c_int(), ctypes.c_double(), ctypes.c_double()
+        _check("bl_conv_rate_for_energy", self._lib.bl_conv_rate_for_energy(
+            self._h, e.ctypes.data, e.size, float(fraction), ctypes.byref(t), ctypes.byref(c), ctypes.byref(f)))
+        return t.value, c.value, f.value
 
     def spectrum(self, ws, which):
         """View of a stored spectrum in the workspace as complex64 [kept][rows][cols]."""

@@ -329,3 +329,61 @@ def test_graph_replays_match_eager(torch):
             torch.cuda.synchronize()
             for name, got, want in zip(("y", "dx", "dw"), (y, dx, dw), ref):
                 assert torch.equal(got, want), (layer.name, r, name)
+
+
+def _oracle_bin_energy(layer, x):
+    if layer.ndim == 1:
+        L = layer.H + layer.pad[0] + layer.pad[1]
+        return bo.bin_energy_1d(x, layer.pad), bo.last_layer_kept(1, L)
+    L = (layer.H + layer.pad[0] + layer.pad[1], layer.W + layer.pad[2] + layer.pad[3])
+    return bo.bin_energy_2d(x, layer.pad), bo.last_layer_kept(2, L)
+
+
+def test_input_energy_parity(torch):
+    """Energy-based compression on the GPU: per-bin input energies (fp64 sums
+    of the fp32 spectrum) against the oracle's, the band chosen from them
+    against the oracle's band, for full-size workload layers (2-D grids 34 and
+    58, the 1-D stack), random odd shapes, a plan that already compresses, and
+    the energies of a spectrum stored by the forward pass (reuse flag)."""
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(2100)
+    cases = [(synth.CONFIGS[3].layers[0], 0.0, synth.layer_inputs(3, 0)[0]),
+             (synth.CONFIGS[5].layers[0], 0.0, synth.layer_inputs(5, 0)[0]),
+             (synth.CONFIGS[2].layers[1], 0.0, synth.layer_inputs(2, 1)[0]),
+             (synth.CONFIGS[4].layers[1], 0.5, synth.layer_inputs(4, 1)[0])]
+    for i in range(6):
+        layer = synth.random_layer(rng, 1 + i % 2)
+        cases.append((layer, float(rng.choice([0.0, 0.0, 0.3])), synth.random_inputs(layer, 2200 + i)[0]))
+    decided = 0
+    for layer, c, x in cases:
+        say(f"[energy] {layer} c={c}")
+        plan = blconv.plan_for_layer(layer, c)
+        ws = plan.workspace(dev)
+        ws.fill_(0xFF)
+        xt = torch.from_numpy(x).to(dev)
+        e = plan.input_energy(xt, ws).cpu().numpy()
+        E, last = _oracle_bin_energy(layer, x.astype(np.float64))
+        u, v = plan.bins()
+        want = E[v] if layer.ndim == 1 else E[u, v]
+        err = rel(e, want)
+        say(f"    rel err {err:.2e}")
+        assert err <= 1e-5
+        assert np.all(np.abs(e - want) <= 1e-4 * want + 1e-7 * want.sum() / want.size)
+        # the band chosen from the GPU's energies is the oracle's
+        own = want.sum()
+        tb = last[v] if layer.ndim == 1 else last[u, v]
+        for fraction in (0.5, 0.9, 0.99):
+            f = np.array([want[tb >= t].sum() / own for t in range(int(tb.min()), int(tb.max()) + 1)])
+            if np.min(np.abs(f - fraction)) < 1e-4:
+                continue  # closer to a tie than the fp32 spectrum resolves
+            expect = int(tb.min()) + max(k for k in range(len(f)) if f[k] >= fraction)
+            t, cc, kept_f = plan.rate_for_energy(e, fraction)
+            assert t == expect, (layer, fraction, t, expect)
+            decided += 1
+        # reuse: the spectrum the forward pass stored gives the same energies
+        w = torch.from_numpy(synth.random_inputs(layer, 7)[1]).to(dev)
+        y = torch.empty(plan.y_shape(), device=dev)
+        plan.forward(xt, w, y, ws)
+        e2 = plan.input_energy(None, ws, flags=blconv.BL_REUSE_X).cpu().numpy()
+        assert np.array_equal(e, e2)
+    assert decided >= 10

@@ -151,3 +151,86 @@ def test_null_arguments_are_rejected_without_gpu():
     m = np.zeros(p.total + 1, np.uint8)
     assert lib.bl_conv_plan_get_mask(h, m.ctypes.data, m.size) == 1
     assert lib.bl_status_string(3) == b"workspace too small"
+
+
+# ------------------------------------------- energy-based rate (host rule) --
+
+
+def _plan_t(plan, layer):
+    L = _grid(layer)
+    return (L // 2 - plan.r_w) if layer.ndim == 1 else (L[0] // 2 - plan.r_h)
+
+
+def _energies_in_bin_order(plan, layer, E):
+    u, v = plan.bins()
+    return E[v] if layer.ndim == 1 else E[u, v]
+
+
+def test_rate_for_energy_matches_oracle():
+    """The library's host rule, fed the oracle's bin energies in the plan's bin
+    order, picks the oracle's band, reports its preserved fraction, and returns a
+    rate for which a new plan peels exactly that many layers."""
+    rng = np.random.default_rng(11)
+    checked = 0
+    for i in range(60):
+        layer = synth.random_layer(rng, 1 if i % 2 else 2)
+        x = synth.random_inputs(layer, 50 + i)[0].astype(np.float64)
+        if layer.ndim == 1:
+            E, last = bo.bin_energy_1d(x, layer.pad), bo.last_layer_kept(1, _grid(layer))
+        else:
+            E, last = bo.bin_energy_2d(x, layer.pad), bo.last_layer_kept(2, _grid(layer))
+        f = bo.preserved_fractions(E, last)
+        plan = blconv.plan_for_layer(layer, 0.0)
+        e = _energies_in_bin_order(plan, layer, E)
+        for fraction in (0.3, 0.6, 0.9, 0.99):
+            want = bo.layers_for_energy(fraction, f)
+            if np.min(np.abs(f - fraction)) < 1e-9:
+                continue  # a tie within rounding: either side is correct
+            t, c, kept_f = plan.rate_for_energy(e, fraction)
+            assert t == want, (layer, fraction, t, want)
+            assert abs(kept_f - f[want]) < 1e-12
+            assert _plan_t(blconv.plan_for_layer(layer, c), layer) == want
+            checked += 1
+    assert checked > 150
+
+
+def test_rate_for_energy_on_a_compressed_plan():
+    """With a plan that already peels t0 layers the fractions are of the energy
+    of its own bins, and the band chosen peels at least t0 layers."""
+    layer = synth.Layer("e2d", 2, 2, 3, 4, 14, 14, 3, (1, 1, 1, 1), "blur")
+    x = synth.random_inputs(layer, 3)[0].astype(np.float64)
+    E, last = bo.bin_energy_2d(x, layer.pad), bo.last_layer_kept(2, _grid(layer))
+    plan = blconv.plan_for_layer(layer, 0.5)
+    t0 = _plan_t(plan, layer)
+    e = _energies_in_bin_order(plan, layer, E)
+    own = E[last >= t0].sum()
+    for fraction in (0.5, 0.8, 0.95, 1.0):
+        t, c, kept_f = plan.rate_for_energy(e, fraction)
+        assert t >= t0
+        assert E[last >= t].sum() / own >= fraction - 1e-12
+        assert t == last.max() or E[last >= t + 1].sum() / own < fraction
+
+
+def test_rate_for_energy_edge_cases():
+    layer = synth.Layer("e1d", 1, 1, 1, 1, 20, 1, 3, (1, 1), "walk")
+    plan = blconv.plan_for_layer(layer, 0.0)
+    zero = np.zeros(plan.kept)
+    t, c, f = plan.rate_for_energy(zero, 0.9)
+    assert t == 22 // 2 and f == 1.0 and _plan_t(blconv.plan_for_layer(layer, c), layer) == t
+    dc = zero.copy()
+    dc[0] = 5.0
+    assert plan.rate_for_energy(dc, 1.0)[0] == 11
+    top = zero.copy()
+    top[-1] = 1.0
+    t, c, f = plan.rate_for_energy(top, 1.0)
+    assert t == 0 and c == 0.0
+    for bad in (0.0, -0.1, 1.5, float("nan")):
+        with pytest.raises(blconv.BlError) as e:
+            plan.rate_for_energy(dc, bad)
+        assert e.value.code == 1
+    neg = dc.copy()
+    neg[3] = -1.0
+    with pytest.raises(blconv.BlError):
+        plan.rate_for_energy(neg, 0.5)
+    with pytest.raises(blconv.BlError):
+        plan.rate_for_energy(dc[:-1], 0.5)
