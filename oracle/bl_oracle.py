@@ -156,13 +156,20 @@ def _irfft2(A, Lh, Lw):
     return np.fft.irfft2(A, s=(Lh, Lw), axes=(-2, -1))
 
 
-def _channel_contract(A, B, conj_b: bool):
+def _channel_contract(A, B, conj_b: bool, rounding=None):
     """Per-frequency complex product summed over a shared channel index.
 
     A: [P, Q, h, w] complex, B: [R, Q, h, w] complex -> [P, R, h, w] with
     out[p, r] = sum_q A[p, q] * (conj(B[r, q]) if conj_b else B[r, q]).
-    Written as one complex matrix product per frequency bin.
+    Written as one complex matrix product per frequency bin.  With
+    `rounding` (a function of real arrays), the real and imaginary parts of
+    both operands are rounded first and the products are exact: the reduced
+    precision operands of the contraction (reduced-precision arithmetic
+    combined with band-limiting), accumulated in fp64.
     """
+    if rounding is not None:
+        A = rounding(A.real) + 1j * rounding(A.imag)
+        B = rounding(B.real) + 1j * rounding(B.imag)
     Bq = np.conj(B) if conj_b else B
     a = np.moveaxis(A, (0, 1), (-2, -1))  # [h, w, P, Q]
     b = np.moveaxis(Bq, (0, 1), (-1, -2))  # [h, w, Q, R]
@@ -180,14 +187,14 @@ def spectra_2d(x, w, pad, c, fft=None):
     return X, Wf, M, g
 
 
-def forward_2d(x, w, pad, c, fft=None):
+def forward_2d(x, w, pad, c, fft=None, rounding=None):
     """y[n,f] = crop_{Ho x Wo} irfft2( sum_c (X[n,c] M) conj(W[f,c] M) )."""
     X, Wf, M, g = spectra_2d(x, w, pad, c, fft)
-    Y = _channel_contract(X, Wf, conj_b=True)
+    Y = _channel_contract(X, Wf, conj_b=True, rounding=rounding)
     return _irfft2(Y, g["Lh"], g["Lw"])[..., : g["Ho"], : g["Wo"]]
 
 
-def backward_input_2d(dy, w, x_hw, pad, c, fft=None):
+def backward_input_2d(dy, w, x_hw, pad, c, fft=None, rounding=None):
     """dx[n,c] = crop_{pad window} irfft2( sum_f (DY[n,f] M) (W[f,c] M) )."""
     H, W = x_hw
     K = w.shape[-1]
@@ -196,12 +203,12 @@ def backward_input_2d(dy, w, x_hw, pad, c, fft=None):
     DY = _rfft2(_embed(np.asarray(dy, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
     Wf = _rfft2(_embed(np.asarray(w, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
     # sum over f of DY[n,f] * W[f,c]: contract DY [n,f] with W^T [c,f]
-    DX = _channel_contract(DY, np.swapaxes(Wf, 0, 1), conj_b=False)
+    DX = _channel_contract(DY, np.swapaxes(Wf, 0, 1), conj_b=False, rounding=rounding)
     full = _irfft2(DX, g["Lh"], g["Lw"])
     return full[..., pad[0]:pad[0] + H, pad[2]:pad[2] + W]
 
 
-def backward_weight_2d(x, dy, K, pad, c, fft=None):
+def backward_weight_2d(x, dy, K, pad, c, fft=None, rounding=None):
     """dw[f,c] = crop_{K x K} irfft2( sum_n (X[n,c] M) conj(DY[n,f] M) )."""
     N, C, H, W = x.shape
     g = geometry_2d(H, W, K, pad, fft)
@@ -209,7 +216,7 @@ def backward_weight_2d(x, dy, K, pad, c, fft=None):
     X = _rfft2(_embed(np.asarray(x, np.float64), g["Lh"], g["Lw"], pad[0], pad[2])) * M
     DY = _rfft2(_embed(np.asarray(dy, np.float64), g["Lh"], g["Lw"], 0, 0)) * M
     # DW[f,c] = sum_n DY*[n,f] X[n,c]: contract over n
-    DW = _channel_contract(np.swapaxes(X, 0, 1), np.swapaxes(DY, 0, 1), conj_b=True)  # [c, f]
+    DW = _channel_contract(np.swapaxes(X, 0, 1), np.swapaxes(DY, 0, 1), conj_b=True, rounding=rounding)  # [c, f]
     return np.swapaxes(_irfft2(DW, g["Lh"], g["Lw"])[..., :K, :K], 0, 1)
 
 
@@ -242,35 +249,36 @@ def _embed1(a, L, o):
     return out
 
 
-def forward_1d(x, w, pad, c, fft=None):
+def forward_1d(x, w, pad, c, fft=None, rounding=None):
     N, C, Lx = x.shape
     K = w.shape[-1]
     g = geometry_1d(Lx, K, pad, fft)
     M = mask_1d(g["L"], c)[0]
     X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
     Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
-    Y = _channel_contract(X[..., None, :], Wf[..., None, :], conj_b=True)[..., 0, :]
+    Y = _channel_contract(X[..., None, :], Wf[..., None, :], conj_b=True, rounding=rounding)[..., 0, :]
     return np.fft.irfft(Y, n=g["L"])[..., : g["Lo"]]
 
 
-def backward_input_1d(dy, w, Lx, pad, c, fft=None):
+def backward_input_1d(dy, w, Lx, pad, c, fft=None, rounding=None):
     K = w.shape[-1]
     g = geometry_1d(Lx, K, pad, fft)
     M = mask_1d(g["L"], c)[0]
     DY = np.fft.rfft(_embed1(np.asarray(dy, np.float64), g["L"], 0)) * M
     Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
-    DX = _channel_contract(DY[..., None, :], np.swapaxes(Wf, 0, 1)[..., None, :], conj_b=False)[..., 0, :]
+    DX = _channel_contract(DY[..., None, :], np.swapaxes(Wf, 0, 1)[..., None, :], conj_b=False,
+                           rounding=rounding)[..., 0, :]
     return np.fft.irfft(DX, n=g["L"])[..., pad[0]:pad[0] + Lx]
 
 
-def backward_weight_1d(x, dy, K, pad, c, fft=None):
+def backward_weight_1d(x, dy, K, pad, c, fft=None, rounding=None):
     N, C, Lx = x.shape
     g = geometry_1d(Lx, K, pad, fft)
     M = mask_1d(g["L"], c)[0]
     X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
     DY = np.fft.rfft(_embed1(np.asarray(dy, np.float64), g["L"], 0)) * M
     DW = _channel_contract(np.swapaxes(X, 0, 1)[..., None, :], np.swapaxes(DY, 0, 1)[..., None, :],
-                           conj_b=True)[..., 0, :]
+                           conj_b=True, rounding=rounding)[..., 0, :]
     return np.swapaxes(np.fft.irfft(DW, n=g["L"])[..., :K], 0, 1)
 
 
@@ -292,18 +300,20 @@ def kept_filter_spectrum_1d(w, L, c):
 # ----------------------------------------------------------------------------
 
 
-def forward(x, w, pad, c, fft=None):
-    return forward_1d(x, w, pad, c, fft) if x.ndim == 3 else forward_2d(x, w, pad, c, fft)
+def forward(x, w, pad, c, fft=None, rounding=None):
+    f = forward_1d if x.ndim == 3 else forward_2d
+    return f(x, w, pad, c, fft, rounding)
 
 
-def backward_input(dy, w, x_spatial, pad, c, fft=None):
+def backward_input(dy, w, x_spatial, pad, c, fft=None, rounding=None):
     if dy.ndim == 3:
-        return backward_input_1d(dy, w, x_spatial[0], pad, c, fft)
-    return backward_input_2d(dy, w, x_spatial, pad, c, fft)
+        return backward_input_1d(dy, w, x_spatial[0], pad, c, fft, rounding)
+    return backward_input_2d(dy, w, x_spatial, pad, c, fft, rounding)
 
 
-def backward_weight(x, dy, K, pad, c, fft=None):
-    return backward_weight_1d(x, dy, K, pad, c, fft) if x.ndim == 3 else backward_weight_2d(x, dy, K, pad, c, fft)
+def backward_weight(x, dy, K, pad, c, fft=None, rounding=None):
+    f = backward_weight_1d if x.ndim == 3 else backward_weight_2d
+    return f(x, dy, K, pad, c, fft, rounding)
 
 
 def mask(ndim, L, c):
@@ -414,3 +424,24 @@ def energy_rate(x, pad, fraction, fft=None):
     t = layers_for_energy(fraction, f)
     kept, total = int((last >= t).sum()), last.size
     return dict(t=t, kept=kept, total=total, c_eff=1.0 - kept / total, preserved=float(f[t]), fractions=f)
+
+
+# ----------------------------------------------------------------------------
+# Reduced-precision contraction operands: the paper compares band-limiting
+# with reduced-precision arithmetic (Sec. 4.3) and combines the two in the
+# supplementary section "Reduced Precision and Bandlimited Training".  Here
+# the operands of the channel contraction are rounded to bfloat16 (reading
+# P1: the exponent range of fp32, which sums of many samples need; the
+# paper's runs used fp16) and the products are accumulated exactly.
+# ----------------------------------------------------------------------------
+
+
+def round_bf16(a) -> np.ndarray:
+    """Values rounded to bfloat16 (8 significant bits, the exponent range of
+    fp32), round to nearest, ties to even: first to fp32 (how the spectra are
+    held), then the 16 low bits of the fp32 pattern are rounded away.
+    Returned as float64."""
+    f = np.asarray(a, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)

@@ -428,3 +428,69 @@ def test_energy_fractions_monotone():
         f = r["fractions"]
         assert f[0] == 1.0 and np.all(np.diff(f) <= 1e-15)
         assert r["preserved"] >= 0.8 and (r["t"] == len(f) - 1 or f[r["t"] + 1] < 0.8)
+
+
+# ------------------------------------- reduced-precision contraction operands --
+
+
+def test_round_bf16_matches_torch_and_ties_to_even():
+    """Rounding to bfloat16 agrees with torch's fp32 -> bfloat16 conversion (a
+    library routine) on values of every magnitude, and ties go to even."""
+    import torch
+    rng = np.random.default_rng(41)
+    v = rng.standard_normal(20000) * np.exp(rng.uniform(-30, 30, 20000))
+    want = torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(bo.round_bf16(v), want)
+    ties = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(2 + 2.0 ** -7), 1.5, 2.0 ** -10, 0.0])
+    assert np.array_equal(bo.round_bf16(ties), [1.0, 1 + 2.0 ** -6, -2.0, 1.5, 2.0 ** -10, 0.0])
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_rounded_operands_exact_on_representable_spectra(ndim):
+    """Unit impulses at the grid origin have constant spectra; with amplitudes
+    that bfloat16 holds exactly, rounding the contraction's operands changes
+    nothing."""
+    if ndim == 2:
+        x = np.zeros((2, 3, 6, 6)); x[..., 0, 0] = [[2.0, -0.5, 1.5], [0.25, 3.0, -1.0]]
+        w = np.zeros((4, 3, 3, 3)); w[..., 0, 0] = 0.5
+        dy = np.zeros((2, 4, 4, 4)); dy[..., 0, 0] = 1.5
+        pad, spatial, K = (0, 0, 0, 0), (6, 6), 3
+    else:
+        x = np.zeros((2, 3, 12)); x[..., 0] = [[2.0, -0.5, 1.5], [0.25, 3.0, -1.0]]
+        w = np.zeros((4, 3, 3)); w[..., 0] = 0.5
+        dy = np.zeros((2, 4, 10)); dy[..., 0] = 1.5
+        pad, spatial, K = (0, 0), (12,), 3
+    for c in (0.0, 0.5):
+        for f, args in ((bo.forward, (x, w, pad, c)), (bo.backward_input, (dy, w, spatial, pad, c)),
+                        (bo.backward_weight, (x, dy, K, pad, c))):
+            assert np.abs(f(*args, None, bo.round_bf16) - f(*args)).max() < 1e-12
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_rounded_operands_error_bound(ndim):
+    """Random inputs: the rounded contraction stays within the bfloat16 error
+    bound of the exact one (8 significant bits per operand, random signs) and
+    does round (the error is not zero)."""
+    rng = np.random.default_rng(42 + ndim)
+    layer = synth.random_layer(rng, ndim)
+    x, w, dy = synth.random_inputs(layer, 9)
+    y, dx, dw = _run(layer, x, w, dy, 0.3)
+    spatial = (layer.H,) if ndim == 1 else (layer.H, layer.W)
+    yr = bo.forward(x, w, layer.pad, 0.3, None, bo.round_bf16)
+    dxr = bo.backward_input(dy, w, spatial, layer.pad, 0.3, None, bo.round_bf16)
+    dwr = bo.backward_weight(x, dy, layer.K, layer.pad, 0.3, None, bo.round_bf16)
+    for a, b in ((yr, y), (dxr, dx), (dwr, dw)):
+        assert 1e-6 < rel(a, b) < 1e-2
+
+
+def test_rounded_operands_both_sides():
+    """Each operand of the contraction is rounded: with the input's spectrum
+    exact in bfloat16 (an impulse) the filter's rounding alone shows, and the
+    other way round."""
+    rng = np.random.default_rng(44)
+    imp = np.zeros((2, 3, 8, 8)); imp[..., 0, 0] = 1.0
+    wimp = np.zeros((4, 3, 3, 3)); wimp[..., 0, 0] = 1.0
+    xr, wr = rng.standard_normal((2, 3, 8, 8)), rng.standard_normal((4, 3, 3, 3))
+    for x, w in ((imp, wr), (xr, wimp)):
+        exact = bo.forward(x, w, (0, 0, 0, 0), 0.0)
+        assert rel(bo.forward(x, w, (0, 0, 0, 0), 0.0, None, bo.round_bf16), exact) > 1e-6
