@@ -69,9 +69,9 @@ def parse():
 class Layer:
     """Device state of one layer: plan, inputs, outputs and workspace."""
 
-    def __init__(self, torch, blconv, layer, arrays, c, dev):
+    def __init__(self, torch, blconv, layer, arrays, c, dev, desc_flags=0):
         self.layer = layer
-        self.plan = blconv.plan_for_layer(layer, c)
+        self.plan = blconv.plan_for_layer(layer, c, None, desc_flags)
         x, w, dy = arrays
         self.x, self.w, self.dy = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
         self.y = torch.empty(self.plan.y_shape(), device=dev)

@@ -95,8 +95,19 @@ typedef struct {
   int pad_hi[2];     /* trailing zeros, same axes */
   double c;          /* compression rate, 0 <= c < 1 */
   int fft_h, fft_w;  /* 0 = padded size; else an FFT grid at least the padded size (1-D: fft_h) */
-  unsigned flags;    /* reserved, must be 0 */
+  unsigned flags;    /* 0, or BL_DESC_BF16_CONTRACTION */
 } bl_conv_desc_t;
+
+/* Descriptor flag: reduced-precision contraction (the paper's reduced-precision
+ * arithmetic combined with band-limiting: Sec. 4.3 and the supplementary section
+ * "Reduced Precision and Bandlimited Training").  Every channel contraction
+ * rounds the real and imaginary parts of both operands to bfloat16 (round to
+ * nearest even; bfloat16 keeps fp32's exponent range, which sums of many
+ * samples need) and accumulates the exact products in fp32; the tiled path
+ * multiplies them on the bf16 matrix cores.  Spectra stay fp32 in the
+ * workspace and the transforms are unchanged.  Expected deviation from the
+ * fp32 path: about 2e-3 relative (8 significant bits per operand). */
+#define BL_DESC_BF16_CONTRACTION 0x1u
 
 typedef struct bl_conv_plan_s* bl_conv_plan_t;
 

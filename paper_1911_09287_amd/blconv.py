@@ -19,6 +19,8 @@ BL_REUSE_X = 0x1
 BL_REUSE_W = 0x2
 BL_REUSE_DY = 0x4
 
+BL_DESC_BF16_CONTRACTION = 0x1
+
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "workspace too small",
           4: "HIP error", 5: "out of host memory"}
 
@@ -96,9 +98,11 @@ class Plan:
 
     2-D: ``Plan(2, N, C_in, C_out, (H, W), K, pad=(top, bottom, left, right), c=...)``.
     1-D: ``Plan(1, N, C_in, C_out, (L,), K, pad=(lo, hi), c=...)``.
+    ``desc_flags``: 0, or BL_DESC_BF16_CONTRACTION (channel contraction on
+    bfloat16-rounded spectra with fp32 sums).
     """
 
-    def __init__(self, ndim, N, C_in, C_out, spatial, K, pad, c, fft=None):
+    def __init__(self, ndim, N, C_in, C_out, spatial, K, pad, c, fft=None, desc_flags=0):
         lib = load()
         d = Desc()
         d.ndim, d.N, d.C_in, d.C_out, d.K = ndim, N, C_in, C_out, K
@@ -114,7 +118,9 @@ class Plan:
             if fft is not None:
                 d.fft_h = fft
         d.c = float(c)
+        d.flags = int(desc_flags)
         self.desc = d
+        self.desc_flags = int(desc_flags)
         self.ndim, self.N, self.C_in, self.C_out, self.K = ndim, N, C_in, C_out, K
         self.spatial = tuple(spatial)
         self.pad = tuple(pad)
@@ -253,10 +259,10 @@ class Plan:
             self._h = None
 
 
-def plan_for_layer(layer, c, fft=None):
+def plan_for_layer(layer, c, fft=None, desc_flags=0):
     """Plan for a layer description with fields ndim, N, C_in, C_out, H, W, K, pad."""
     spatial = (layer.H,) if layer.ndim == 1 else (layer.H, layer.W)
-    return Plan(layer.ndim, layer.N, layer.C_in, layer.C_out, spatial, layer.K, layer.pad, c, fft)
+    return Plan(layer.ndim, layer.N, layer.C_in, layer.C_out, spatial, layer.K, layer.pad, c, fft, desc_flags)
 
 
 class Profile:

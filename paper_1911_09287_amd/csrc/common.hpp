@@ -12,6 +12,14 @@
 namespace blc {
 
 constexpr int kThreads = 256;
+
+// bfloat16 bit pattern of x (round to nearest, ties to even; finite inputs),
+// and x rounded to bfloat16 as a float.
+__device__ __forceinline__ unsigned bf16_bits(float x) {
+  const unsigned u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(bf16_bits(x) << 16); }
 constexpr size_t kMaxLds = 64 * 1024;
 
 // ---- per-kernel timing (bl_profile_*) -------------------------------------

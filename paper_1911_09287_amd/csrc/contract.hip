@@ -47,7 +47,9 @@ constexpr int plane_floats() {
   return ((kBK * (W + 4) + 63) / 64) * 64 + 32;
 }
 
-template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ>
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
+template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16>
 __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
                                                float2* __restrict__ O, CgemmArgs g) {
   constexpr int WM = BM / 2;   // rows per wave
@@ -58,8 +60,16 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
   constexpr int BV = BN / 32;  // 16-byte B loads per thread per stage
   constexpr int SA = BM + 4, SB = BN + 4;  // padded row lengths
   constexpr int PA = plane_floats<BM>(), PB = plane_floats<BN>();
-  __shared__ float As[2][2 * PA];
-  __shared__ float Bs[2][2 * PB];
+  __shared__ float As[BF16 ? 1 : 2][BF16 ? 1 : 2 * PA];
+  __shared__ float Bs[BF16 ? 1 : 2][BF16 ? 1 : 2 * PB];
+  // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
+  // the (even, odd) real-k entries of the 2x2 block column the lane reads.
+  // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
+  // in disjoint banks; the form planes are 16 (mod 64) words apart.
+  constexpr int SA16 = BM + 16, SB16 = BN + 16;
+  constexpr int PB16 = ((kBK * SB16 + 63) / 64) * 64 + 16;
+  __shared__ unsigned As16[BF16 ? 2 : 1][BF16 ? kBK * SA16 : 1];
+  __shared__ unsigned Bs16[BF16 ? 2 : 1][BF16 ? 2 * PB16 : 1];
 
   // XCD-aware numbering: the hardware deals blocks to the 8 XCDs in turn
   const unsigned nb = gridDim.x * gridDim.y;
@@ -128,7 +138,45 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
       rb[q] = *reinterpret_cast<const float4*>(Bb + off);
     }
   };
+  auto pack = [](float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); };
+  // the two forms of complex value (br, bi): conj block [[br, -bi], [bi, br]],
+  // identity block [[br, bi], [-bi, br]]; form f is column f of the block
+  auto form0 = [&](float br, float bi) { return CONJ ? pack(br, bi) : pack(br, -bi); };
+  auto form1 = [&](float br, float bi) { return CONJ ? pack(-bi, br) : pack(bi, br); };
+  auto store16 = [&](int buf, int k0, const float4* ra, const float4* rb) {
+    unsigned* a16 = As16[buf];
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      int m, k;
+      a_pos(q, m, k);
+      const float4 r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
+      if (A_KC) {
+        a16[k * SA16 + m] = pack(r.x, r.y);
+        a16[(k + 1) * SA16 + m] = pack(r.z, r.w);
+      } else {
+        a16[k * SA16 + m] = pack(r.x, r.y);
+        a16[k * SA16 + m + 1] = pack(r.z, r.w);
+      }
+    }
+    unsigned* b16 = Bs16[buf];
+#pragma unroll
+    for (int q = 0; q < BV; ++q) {
+      int k, n;
+      b_pos(q, k, n);
+      const float4 r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
+      // second value at (k, n + 1) when n runs along the vector, else (k + 1, n)
+      const int i0 = k * SB16 + n, i1 = B_NC ? i0 + 1 : i0 + SB16;
+      b16[i0] = form0(r.x, r.y);
+      b16[PB16 + i0] = form1(r.x, r.y);
+      b16[i1] = form0(r.z, r.w);
+      b16[PB16 + i1] = form1(r.z, r.w);
+    }
+  };
   auto store = [&](int buf, int k0, const float4* ra, const float4* rb) {
+    if constexpr (BF16) {
+      store16(buf, k0, ra, rb);
+      return;
+    }
     float* a0 = As[buf];
     float* a1 = As[buf] + PA;
 #pragma unroll
@@ -160,7 +208,38 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
       }
     }
   };
+  auto compute16 = [&](int buf) {
+    // v_mfma_f32_32x32x8_bf16: lane l supplies real k = 4 (l / 32) .. + 3 of its
+    // row (A) or column (B), i.e. complex k = 2 (l / 32) and 2 (l / 32) + 1 of
+    // the four complex k an instruction consumes
+    const unsigned* ap = As16[buf] + wm + jcol;
+    const unsigned* bp = Bs16[buf] + bcol * PB16 + wn + (jcol >> 1);
+#pragma unroll
+    for (int q = 0; q < kBK / 4; ++q) {
+      const int kc = 4 * q + 2 * a_part;
+      shortx4 av[MI], bv[NJ];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const unsigned lo = ap[kc * SA16 + 32 * i], hi = ap[(kc + 1) * SA16 + 32 * i];
+        av[i] = shortx4{(short)(lo & 0xFFFF), (short)(lo >> 16), (short)(hi & 0xFFFF), (short)(hi >> 16)};
+      }
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const unsigned lo = bp[kc * SB16 + 16 * j], hi = bp[(kc + 1) * SB16 + 16 * j];
+        bv[j] = shortx4{(short)(lo & 0xFFFF), (short)(lo >> 16), (short)(hi & 0xFFFF), (short)(hi >> 16)};
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  };
   auto compute = [&](int buf) {
+    if constexpr (BF16) {
+      compute16(buf);
+      return;
+    }
     // all fragments of the stage first, so the LDS reads overlap the MFMAs
     const float* ap = As[buf] + a_part * PA + wm + jcol;
     const float* bp = Bs[buf] + b_src * PB + wn + (jcol >> 1);
@@ -289,9 +368,12 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   const char* name = which == Contract::Forward ? "contract_fwd"
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
   bl_status_t st = BL_ERR_UNSUPPORTED;
-#define BL_GO(BMV, BNV, AK, BN_, CJ)                                                               \
-  st = timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                      \
-    hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g);     \
+#define BL_GO(BMV, BNV, AK, BN_, CJ)                                                                        \
+  st = timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                               \
+    if (p->bf16)                                                                                             \
+      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, true>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
+    else                                                                                                     \
+      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, false>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
   })
 #define BL_SHAPES(AK, BN_, CJ)                       \
   if (BM == 128 && BN == 64) BL_GO(128, 64, AK, BN_, CJ); \

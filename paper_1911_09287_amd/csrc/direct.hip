@@ -481,6 +481,7 @@ struct ContractArgs {
   long sAm, sAk, sBk, sBn, ldo;  // element strides (complex units)
   long bA, bB, bO;               // per-bin strides
   int tiles_n;
+  int bf16;                      // operands rounded to bfloat16 (exact products, fp32 sums)
 };
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
@@ -529,6 +530,7 @@ __global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict_
       }
       float2 v = make_float2(0.f, 0.f);
       if (m0 + m < g.M && k0 + k < g.K) v = Ab[(size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk];
+      if (g.bf16) v = make_float2(bf16_round(v.x), bf16_round(v.y));
       As[0][k][m] = v.x;
       As[1][k][m] = v.y;
     }
@@ -541,6 +543,7 @@ __global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict_
       else { n = e >> 4; k = e & 15; }
       float2 v = make_float2(0.f, 0.f);
       if (n0 + n < g.N && k0 + k < g.K) v = Bb[(size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn];
+      if (g.bf16) v = make_float2(bf16_round(v.x), bf16_round(v.y));
       Bs[0][k][n] = v.x;
       Bs[1][k][n] = v.y;
     }
@@ -754,6 +757,7 @@ bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, con
   }
   const int tiles_m = (g.M + CBM - 1) / CBM;
   g.tiles_n = (g.N + CBN - 1) / CBN;
+  g.bf16 = p->bf16 ? 1 : 0;
   if (B > 65535) return BL_ERR_UNSUPPORTED;
   dim3 grid((unsigned)(tiles_m * g.tiles_n), (unsigned)B);
   // complex MAC = 8 real flops; compulsory traffic: both operands and the result once

@@ -28,11 +28,17 @@ struct ThinArgs {
   int ks;                        // waves splitting k: 1 (a wave per item) or 4 (a block per item)
 };
 
+// BF16: operands rounded to bfloat16 (exact products, fp32 sums)
+template <bool BF16>
+__device__ __forceinline__ float2 operand(float2 v) {
+  return BF16 ? make_float2(bf16_round(v.x), bf16_round(v.y)) : v;
+}
+
 __device__ __forceinline__ float2 cmac(float2 acc, float2 a, float2 b) {
   return make_float2(fmaf(a.x, b.x, fmaf(-a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(a.y, b.x, acc.y)));
 }
 
-template <int MT, bool CONJ>
+template <int MT, bool CONJ, bool BF16>
 __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A, const float2* __restrict__ B,
                                                    float2* __restrict__ O, ThinArgs g) {
   __shared__ float2 red[3][MT][64];
@@ -59,10 +65,10 @@ __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A,
     for (int i = 0; i < MT; ++i) arow[i] = (long)min(m0 + i, g.M - 1) * g.sAm;
 #pragma unroll 4
     for (int k = k0; k < k1; ++k) {
-      float2 b = Bb[(long)k * g.sBk];
+      float2 b = operand<BF16>(Bb[(long)k * g.sBk]);
       if (CONJ) b.y = -b.y;
 #pragma unroll
-      for (int i = 0; i < MT; ++i) acc[i] = cmac(acc[i], Ab[arow[i] + (long)k * g.sAk], b);
+      for (int i = 0; i < MT; ++i) acc[i] = cmac(acc[i], operand<BF16>(Ab[arow[i] + (long)k * g.sAk]), b);
     }
   }
   if (g.ks == 4) {
@@ -85,7 +91,7 @@ __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A,
     if (m0 + i < g.M) Ob[(long)(m0 + i) * g.ldo] = acc[i];
 }
 
-template <int NT, bool CONJ>
+template <int NT, bool CONJ, bool BF16>
 __global__ __launch_bounds__(256) void k_thin_rows(const float2* __restrict__ A, const float2* __restrict__ B,
                                                    float2* __restrict__ O, ThinArgs g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -97,11 +103,11 @@ __global__ __launch_bounds__(256) void k_thin_rows(const float2* __restrict__ A,
 #pragma unroll
   for (int j = 0; j < NT; ++j) acc[j] = make_float2(0.f, 0.f);
   for (int k = lane; k < g.K; k += 64) {
-    const float2 a = Ab[(long)k * g.sAk];
+    const float2 a = operand<BF16>(Ab[(long)k * g.sAk]);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       // columns past N repeat the last one (computed, never written)
-      float2 b = Bb[(long)k * g.sBk + (long)min(j, g.N - 1) * g.sBn];
+      float2 b = operand<BF16>(Bb[(long)k * g.sBk + (long)min(j, g.N - 1) * g.sBn]);
       if (CONJ) b.y = -b.y;
       acc[j] = cmac(acc[j], a, b);
     }
@@ -179,8 +185,10 @@ bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const 
         hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, A, Bm, O, g);
       });
     };
-#define BL_THIN_C(mt)                                                          \
-  if (MT == mt) return conj ? go(k_thin_cols<mt, true>) : go(k_thin_cols<mt, false>);
+#define BL_THIN_C(mt)                                                                              \
+  if (MT == mt)                                                                                    \
+    return p->bf16 ? (conj ? go(k_thin_cols<mt, true, true>) : go(k_thin_cols<mt, false, true>))   \
+                   : (conj ? go(k_thin_cols<mt, true, false>) : go(k_thin_cols<mt, false, false>));
     BL_THIN_C(1) BL_THIN_C(2) BL_THIN_C(4) BL_THIN_C(8)
 #undef BL_THIN_C
     return BL_ERR_UNSUPPORTED;
@@ -193,8 +201,10 @@ bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const 
         hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, A, Bm, O, g);
       });
     };
-#define BL_THIN_R(nt)                                                          \
-  if (NT == nt) return conj ? go(k_thin_rows<nt, true>) : go(k_thin_rows<nt, false>);
+#define BL_THIN_R(nt)                                                                              \
+  if (NT == nt)                                                                                    \
+    return p->bf16 ? (conj ? go(k_thin_rows<nt, true, true>) : go(k_thin_rows<nt, false, true>))   \
+                   : (conj ? go(k_thin_rows<nt, true, false>) : go(k_thin_rows<nt, false, false>));
     BL_THIN_R(1) BL_THIN_R(2) BL_THIN_R(4) BL_THIN_R(8)
 #undef BL_THIN_R
   }

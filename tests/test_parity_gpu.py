@@ -33,8 +33,8 @@ def say(*a):
     print(*a, flush=True)
 
 
-def gpu_passes(torch, layer, c, x, w, dy, reuse=True, poison=True, fft=None):
-    plan = blconv.plan_for_layer(layer, c, fft)
+def gpu_passes(torch, layer, c, x, w, dy, reuse=True, poison=True, fft=None, desc_flags=0):
+    plan = blconv.plan_for_layer(layer, c, fft, desc_flags)
     dev = torch.device("cuda:0")
     ws = plan.workspace(dev)
     if poison:
@@ -51,10 +51,11 @@ def gpu_passes(torch, layer, c, x, w, dy, reuse=True, poison=True, fft=None):
     return y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy(), plan, ws
 
 
-def oracle_passes(layer, c, x, w, dy, fft=None):
+def oracle_passes(layer, c, x, w, dy, fft=None, rounding=None):
     spatial = (layer.H,) if layer.ndim == 1 else (layer.H, layer.W)
-    return (bo.forward(x, w, layer.pad, c, fft), bo.backward_input(dy, w, spatial, layer.pad, c, fft),
-            bo.backward_weight(x, dy, layer.K, layer.pad, c, fft))
+    return (bo.forward(x, w, layer.pad, c, fft, rounding),
+            bo.backward_input(dy, w, spatial, layer.pad, c, fft, rounding),
+            bo.backward_weight(x, dy, layer.K, layer.pad, c, fft, rounding))
 
 
 CASES = [(cfg, li, c) for cfg in sorted(synth.CONFIGS) for li in range(len(synth.CONFIGS[cfg].layers))
@@ -283,6 +284,46 @@ def test_thin_contractions(torch):
             errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
             say(f"    rel err {errs}")
             assert max(errs) <= TOL, errs
+
+
+# bfloat16 operands: a spectrum value that the fp32 transforms leave within
+# their rounding error of a bfloat16 tie can round the other way than in the
+# fp64 oracle (an error of one bfloat16 ulp, 2^-8 relative, in that value); at
+# fp32 transform errors of ~1e-6 this happens to a few values in ten thousand
+# and gives relative errors ~1e-4.  Rounding itself moves the result by ~2e-3,
+# so the tolerance still tells a rounded contraction from an unrounded one.
+BF16_TOL = 5e-4
+BF16_EXACT_TOL = 1e-2
+
+
+def test_bf16_contraction_parity(torch):
+    """Plans with BL_DESC_BF16_CONTRACTION against the oracle whose channel
+    contraction rounds both operands to bfloat16 (round to nearest even) and
+    sums exactly: the MFMA tiles (with and without split k), the thin
+    vector-ALU contraction and the generic one, 1-D and 2-D."""
+    cases = [
+        synth.Layer("bf_tiled_2d", 2, 16, 32, 48, 12, 12, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("bf_tiled_1d", 1, 32, 16, 24, 200, 1, 8, (3, 4), "walk"),
+        synth.Layer("bf_split_2d", 2, 256, 16, 32, 8, 8, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("bf_thin_2d", 2, 4, 3, 64, 12, 12, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("bf_thin_1d", 1, 70, 100, 5, 90, 1, 5, (2, 2), "walk"),
+        synth.Layer("bf_generic_2d", 2, 10, 17, 33, 9, 9, 3, (1, 1, 1, 1), "blur"),
+    ]
+    for i, layer in enumerate(cases):
+        for c in (0.0, 0.5):
+            say(f"[bf16] {layer.name} c={c}")
+            x, w, dy = synth.random_inputs(layer, 1900 + i)
+            got = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_BF16_CONTRACTION)[:3]
+            ref = oracle_passes(layer, c, x, w, dy, rounding=bo.round_bf16)
+            exact = oracle_passes(layer, c, x, w, dy)
+            errs = [rel(a, b) for a, b in zip(got, ref)]
+            errs_exact = [rel(a, b) for a, b in zip(got, exact)]
+            gaps = [rel(a, b) for a, b in zip(ref, exact)]
+            say(f"    rel err vs bf16 oracle {errs}; vs exact {errs_exact}; oracle gap {gaps}")
+            assert all(np.isfinite(a).all() for a in got)
+            assert max(errs) <= BF16_TOL, errs
+            assert max(errs_exact) <= BF16_EXACT_TOL, errs_exact
+            assert min(gaps) > 2 * BF16_TOL, gaps  # the tolerance separates rounded from exact
 
 
 def test_graph_replays_match_eager(torch):

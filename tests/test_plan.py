@@ -122,12 +122,23 @@ def _create(**kw):
     (dict(W=0), 1), (dict(K=0), 1), (dict(K=9), 2), (dict(K=9, H=20, W=20), 2),
     (dict(c=1.0), 1), (dict(c=-0.1), 1), (dict(c=float("nan")), 1), (dict(c=0.999), 0),
     (dict(pad_lo=(-1, 0)), 1), (dict(fft_h=9, fft_w=8), 0), (dict(fft_h=9, fft_w=7), 1), (dict(fft_h=7), 1), (dict(fft_h=12, fft_w=10), 0),
-    (dict(flags=1), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
+    (dict(flags=1), 0), (dict(flags=2), 1), (dict(flags=3), 1), (dict(flags=0x80000000), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
     (dict(ndim=1, W=1, H=10), 0), (dict(ndim=1, W=2, H=10), 1), (dict(ndim=1, W=1, H=10, pad_lo=(0, 1)), 1),
     (dict(ndim=1, W=1, H=10, fft_w=4), 1), (dict(ndim=1, W=1, H=10, fft_h=9), 1),
 ])
 def test_plan_create_validation(kw, code):
     assert _create(**kw) == code
+
+
+def test_bf16_flag_leaves_the_band_and_workspace_unchanged():
+    """The reduced-precision contraction changes only the arithmetic of the
+    channel sums: the band, the grid and the workspace are those of the fp32 plan."""
+    for args in [(2, 3, 16, 24, (20, 20), 3, (1, 1, 1, 1), 0.5), (1, 5, 3, 7, (90,), 5, (2, 2), 0.3)]:
+        a = blconv.Plan(*args)
+        b = blconv.Plan(*args, desc_flags=blconv.BL_DESC_BF16_CONTRACTION)
+        assert (a.fft, a.r_h, a.r_w, a.kept, a.total, a.c_eff) == (b.fft, b.r_h, b.r_w, b.kept, b.total, b.c_eff)
+        assert a.workspace_bytes == b.workspace_bytes and a.offsets == b.offsets
+        assert np.array_equal(a.mask(), b.mask())
 
 
 def test_null_arguments_are_rejected_without_gpu():
