@@ -95,19 +95,22 @@ typedef struct {
   int pad_hi[2];     /* trailing zeros, same axes */
   double c;          /* compression rate, 0 <= c < 1 */
   int fft_h, fft_w;  /* 0 = padded size; else an FFT grid at least the padded size (1-D: fft_h) */
-  unsigned flags;    /* 0, or BL_DESC_BF16_CONTRACTION */
+  unsigned flags;    /* 0, or BL_DESC_BF16_SPECTRA */
 } bl_conv_desc_t;
 
-/* Descriptor flag: reduced-precision contraction (the paper's reduced-precision
- * arithmetic combined with band-limiting: Sec. 4.3 and the supplementary section
- * "Reduced Precision and Bandlimited Training").  Every channel contraction
- * rounds the real and imaginary parts of both operands to bfloat16 (round to
- * nearest even; bfloat16 keeps fp32's exponent range, which sums of many
- * samples need) and accumulates the exact products in fp32; the tiled path
- * multiplies them on the bf16 matrix cores.  Spectra stay fp32 in the
- * workspace and the transforms are unchanged.  Expected deviation from the
- * fp32 path: about 2e-3 relative (8 significant bits per operand). */
-#define BL_DESC_BF16_CONTRACTION 0x1u
+/* Descriptor flag: reduced-precision spectra (the paper's reduced-precision
+ * arithmetic combined with band-limiting: Sec. 4.3 and the supplementary
+ * section "Reduced Precision and Bandlimited Training").  The forward
+ * transforms round the kept spectra X, W and DY to bfloat16 (round to nearest
+ * even on the fp32 transform results; bfloat16 keeps fp32's exponent range,
+ * which sums over many samples need) and store them as 32-bit words holding a
+ * bfloat16 pair, real part in the low 16 bits, imaginary part in the high 16
+ * bits: half the workspace those saved maps take in fp32.  Every channel
+ * contraction multiplies the stored values exactly and accumulates in fp32
+ * (the tiled path on the bf16 matrix cores); its outputs, the transforms'
+ * arithmetic and the layer's inputs and outputs stay fp32.  Expected deviation
+ * from the fp32 path: about 2e-3 relative (8 significant bits per operand). */
+#define BL_DESC_BF16_SPECTRA 0x1u
 
 typedef struct bl_conv_plan_s* bl_conv_plan_t;
 
@@ -145,7 +148,8 @@ bl_status_t bl_conv_plan_get_bins(bl_conv_plan_t plan, int* u, int* v, size_t n)
 bl_status_t bl_conv_workspace_size(bl_conv_plan_t plan, size_t* bytes);
 
 /* Byte offsets of the stored spectra inside the workspace (any pointer may be
- * NULL).  All are interleaved complex64, bin-major:
+ * NULL).  All are bin-major, interleaved complex64 (with BL_DESC_BF16_SPECTRA:
+ * one 32-bit bfloat16 pair per value, as described there):
  *   X  [kept][N][C_in], W [kept][C_in][C_out], DY [kept][N][C_out]. */
 bl_status_t bl_conv_workspace_layout(bl_conv_plan_t plan, size_t* off_x, size_t* off_w, size_t* off_dy);
 
@@ -177,7 +181,8 @@ bl_status_t bl_conv_backward_weight(bl_conv_plan_t plan, const float* x, const f
  * column 0 and in the Nyquist column of an even width, else 2 (Parseval on the
  * half plane), so with a plan of rate 0 the energies sum to L_h L_w times the
  * energy of x.  X, the input spectrum, is computed from x and left in ws
- * (BL_REUSE_X: read from ws; x may then be NULL).  One kernel per call on
+ * (BL_REUSE_X: read from ws; x may then be NULL); the sums are of X as stored
+ * (rounded to bfloat16 in plans with BL_DESC_BF16_SPECTRA).  One kernel per call on
  * `stream`, summing in a fixed order (results do not depend on scheduling). */
 bl_status_t bl_conv_input_energy(bl_conv_plan_t plan, const float* x, void* ws, unsigned flags,
                                  double* energy, void* stream);

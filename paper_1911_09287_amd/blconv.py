@@ -19,7 +19,7 @@ BL_REUSE_X = 0x1
 BL_REUSE_W = 0x2
 BL_REUSE_DY = 0x4
 
-BL_DESC_BF16_CONTRACTION = 0x1
+BL_DESC_BF16_SPECTRA = 0x1
 
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "workspace too small",
           4: "HIP error", 5: "out of host memory"}
@@ -98,8 +98,8 @@ class Plan:
 
     2-D: ``Plan(2, N, C_in, C_out, (H, W), K, pad=(top, bottom, left, right), c=...)``.
     1-D: ``Plan(1, N, C_in, C_out, (L,), K, pad=(lo, hi), c=...)``.
-    ``desc_flags``: 0, or BL_DESC_BF16_CONTRACTION (channel contraction on
-    bfloat16-rounded spectra with fp32 sums).
+    ``desc_flags``: 0, or BL_DESC_BF16_SPECTRA (spectra stored in bfloat16,
+    contracted with fp32 sums).
     """
 
     def __init__(self, ndim, N, C_in, C_out, spatial, K, pad, c, fft=None, desc_flags=0):
@@ -245,12 +245,15 @@ class Plan:
         return t.value, c.value, f.value
 
     def spectrum(self, ws, which):
-        """View of a stored spectrum in the workspace as complex64 [kept][rows][cols]."""
+        """View of a stored spectrum in the workspace, [kept][rows][cols]: complex64,
+        or with BL_DESC_BF16_SPECTRA int32 words each holding a bfloat16 pair
+        (real part in the low 16 bits, imaginary part in the high 16 bits)."""
         import torch
         rows, cols = {"X": (self.N, self.C_in), "W": (self.C_in, self.C_out), "DY": (self.N, self.C_out)}[which]
         off = self.offsets[which]
-        n = self.kept * rows * cols * 8
-        return ws[off:off + n].view(torch.complex64).view(self.kept, rows, cols)
+        bf16 = bool(self.desc_flags & BL_DESC_BF16_SPECTRA)
+        n = self.kept * rows * cols * (4 if bf16 else 8)
+        return ws[off:off + n].view(torch.int32 if bf16 else torch.complex64).view(self.kept, rows, cols)
 
     def __del__(self):
         h = getattr(self, "_h", None)

@@ -35,7 +35,7 @@ hipEvent_t prof_event(int slot, int end) { return g_prof.ev[2 * slot + end]; }
 // Stage dispatch: the fast transform for the shape when there is one, else
 // the direct pruned DFT.
 // ---------------------------------------------------------------------------
-bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s) {
   if (p->Lh == 1) {
     bl_status_t st = launch_bluestein_fwd(p, in, out, P, Win, oj, s);
@@ -47,7 +47,7 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* ou
   return launch_spec_fwd_direct(p, in, out, P, Hin, Win, oi, oj, s);
 }
 
-bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm, float2* O,
                             float2* part, hipStream_t s) {
   bl_status_t st = BL_ERR_UNSUPPORTED;
   if (contract_is_thin(p, which)) st = launch_contract_thin(p, which, A, Bm, O, s);
@@ -71,6 +71,8 @@ bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* ou
 
 namespace {
 inline float2* ws_at(void* ws, size_t off) { return reinterpret_cast<float2*>(static_cast<char*>(ws) + off); }
+// a stored spectrum (complex64 or bfloat16 pairs, as the plan says)
+inline void* spec_at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
 
 #define BL_TRY(expr)                    \
   do {                                  \
@@ -93,8 +95,8 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   if (flags & ~(BL_REUSE_X | BL_REUSE_W)) return BL_ERR_INVALID_ARG;
   if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_W) && !w)) return BL_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* X = ws_at(ws, p->off_X);
-  float2* Wf = ws_at(ws, p->off_W);
+  void* X = spec_at(ws, p->off_X);
+  void* Wf = spec_at(ws, p->off_W);
   float2* T = ws_at(ws, p->off_T);
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
   if (!(flags & BL_REUSE_X))
@@ -109,8 +111,8 @@ extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy,
   if (flags & ~BL_REUSE_W) return BL_ERR_INVALID_ARG;
   if (!(flags & BL_REUSE_W) && !w) return BL_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* Wf = ws_at(ws, p->off_W);
-  float2* DY = ws_at(ws, p->off_DY);
+  void* Wf = spec_at(ws, p->off_W);
+  void* DY = spec_at(ws, p->off_DY);
   float2* T = ws_at(ws, p->off_T);
   BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
@@ -124,8 +126,8 @@ extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x,
   if (flags & ~(BL_REUSE_X | BL_REUSE_DY)) return BL_ERR_INVALID_ARG;
   if ((!(flags & BL_REUSE_X) && !x) || (!(flags & BL_REUSE_DY) && !dy)) return BL_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* X = ws_at(ws, p->off_X);
-  float2* DY = ws_at(ws, p->off_DY);
+  void* X = spec_at(ws, p->off_X);
+  void* DY = spec_at(ws, p->off_DY);
   float2* DW = ws_at(ws, p->off_DW);
   if (!(flags & BL_REUSE_X))
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));

@@ -256,7 +256,8 @@ __device__ __forceinline__ float2 chirp(const BlueArgs& a, int m) {
 //   inverse, paired:  input the conjugate-symmetric extensions of Y1 and Y2
 //                     over k = -(V-1)..V-1 as Y1 + i Y2 (real DC parts); the
 //                     real and imaginary parts of the result are y1 and y2.
-template <int M, int MODE>
+// S: stored-spectrum element of the forward modes' output (float2 or bfloat16 pairs)
+template <int M, int MODE, typename S = float2>
 __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restrict__ in_, void* __restrict__ out_,
                                                            BlueArgs a) {
   constexpr bool INV = MODE & 1, PACK = MODE >= 2;
@@ -333,7 +334,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restric
         if (i < a.n_out) {
           const float2 r = cmul(post[i], cconj(v));
           if constexpr (MODE == 0) {
-            static_cast<float2*>(out_)[(size_t)i * P + s1] = r;
+            spec_put(static_cast<S*>(out_), (size_t)i * P + s1, r);
           } else if constexpr (MODE == 1) {
             static_cast<float*>(out_)[(size_t)s1 * a.n_out + i] = r.x;
           } else if constexpr (MODE == 2) {
@@ -347,14 +348,14 @@ __global__ __launch_bounds__(64 * kWaves) void k_bluestein(const void* __restric
       wave_fft<M>(buf, lane, tw, load_buf, store_out);
       if constexpr (MODE == 2) {
         // Z[k] sits at index k + V - 1
-        float2* X = static_cast<float2*>(out_);
+        S* X = static_cast<S*>(out_);
         for (int v = lane; v < a.V; v += 64) {
           const float2 zp = buf[pidx(a.V - 1 + v)];
           const float2 zm = cconj(buf[pidx(a.V - 1 - v)]);
-          X[(size_t)v * P + s1] = cadd(zp, zm);
+          spec_put(X, (size_t)v * P + s1, cadd(zp, zm));
           if (two) {
             const float2 d = csub(zp, zm);
-            X[(size_t)v * P + s2] = make_float2(d.y, -d.x);
+            spec_put(X, (size_t)v * P + s2, make_float2(d.y, -d.x));
           }
         }
         wave_sync();
@@ -403,7 +404,7 @@ constexpr int floats_per_row() {
   return MODE == 0 ? 1 : MODE == 3 ? 4 : 2;
 }
 
-template <int MODE, int NR>
+template <int MODE, int NR, typename S = float2>
 __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __restrict__ in_, void* __restrict__ out_,
                                                                BlueGeom a, int wpb) {
   constexpr int M = 1024;
@@ -605,13 +606,13 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
         if (m < nfull || (m == nfull && tail)) xb[h + 32 * m] = cmul(post[h + 32 * m], cconj(v[m]));
       }
       wave_sync();
-      float2* X = static_cast<float2*>(out_);
+      S* X = static_cast<S*>(out_);
       if constexpr (MODE == 0) {
         // bins i of the wave's two series, two consecutive series per bin row
         const unsigned s = 2 * p + (lane & 1);
         const float2* src = xw + (lane & 1) * kXS;
         if (s < P) {
-          for (int i = lane >> 1; i < a.n_out; i += 32) X[(unsigned)i * P + s] = src[i];
+          for (int i = lane >> 1; i < a.n_out; i += 32) spec_put(X, (unsigned)i * P + s, src[i]);
         }
       } else {
         // Z[k] sits at index k + V - 1; the two series of a job split by
@@ -621,7 +622,7 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
         if (s < P) {
           for (int k = lane >> 2; k < a.V; k += 16) {
             const float2 zp = src[k], zm = cconj(src[-k]);
-            X[(unsigned)k * P + s] = (lane & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm);
+            spec_put(X, (unsigned)k * P + s, (lane & 1) ? make_float2(zp.y - zm.y, zm.x - zp.x) : cadd(zp, zm));
           }
         }
       }
@@ -643,7 +644,7 @@ int device_cus() {
   return g_cu_count[dev];
 }
 
-template <int M, int MODE>
+template <int M, int MODE, typename S>
 bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
   // algorithmic arithmetic: two M-point complex FFTs (5 M log2 M flops each, the
   // conventional count) per series, or per pair of series when two share an FFT
@@ -673,7 +674,7 @@ bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, d
   const long groups = (a.P + kSeriesPerGroup - 1) / kSeriesPerGroup;
   const long blocks = std::min<long>(groups, 2L * device_cus());
   return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL((k_bluestein<M, MODE>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, e0, e1, 0, in, out, a);
+    hipExtLaunchKernelGGL((k_bluestein<M, MODE, S>), dim3((unsigned)blocks), dim3(64 * kWaves), lds, s, e0, e1, 0, in, out, a);
   });
 }
 
@@ -747,7 +748,7 @@ bl_status_t blue_tables(const bl_conv_plan_s* p, const BlueGeom& a, int mode, co
   return plan_table(p, key, [&](std::vector<float2>& host) { host_tables_1k(a, mode, host); }, out);
 }
 
-template <int MODE, int NR>
+template <int MODE, int NR, typename S>
 bl_status_t launch_1k_nr(const BlueGeom& a, const void* in, void* out, const char* name, double bytes,
                          hipStream_t s) {
   constexpr int M = 1024;
@@ -757,7 +758,7 @@ bl_status_t launch_1k_nr(const BlueGeom& a, const void* in, void* out, const cha
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return BL_ERR_HIP;
   static bool attr_set[64] = {};
   if (!attr_set[dev]) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, NR>),
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, NR, S>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess)
       return BL_ERR_HIP;
     attr_set[dev] = true;
@@ -771,14 +772,14 @@ bl_status_t launch_1k_nr(const BlueGeom& a, const void* in, void* out, const cha
   const long blocks = std::min<long>(cus, (pairs + wpb - 1) / wpb);
   const double flops = (double)jobs * 2.0 * 5.0 * M * 10.0;
   return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL((k_bluestein1k<MODE, NR>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, e0, e1, 0,
+    hipExtLaunchKernelGGL((k_bluestein1k<MODE, NR, S>), dim3((unsigned)blocks), dim3(64 * kWaves1k), lds, s, e0, e1, 0,
                           in, out, a, wpb);
   });
 }
 
 // NR: rows of input per lane as instantiated (the smallest that covers the
 // data); the kernel prefetches the next round when they fit in 32 floats.
-template <int MODE>
+template <int MODE, typename S>
 bl_status_t launch_1k(const bl_conv_plan_s* p, const BlueGeom& a0, const void* in, void* out, const char* name,
                       double bytes, hipStream_t s) {
   // the kernel indexes its input and output with 32-bit element offsets
@@ -789,14 +790,14 @@ bl_status_t launch_1k(const bl_conv_plan_s* p, const BlueGeom& a0, const void* i
   if (ts != BL_OK) return ts;
   if constexpr (MODE == 0 || MODE == 2) {
     const int nr = (a.n_in + 31) / 32;
-    if (nr <= 16) return launch_1k_nr<MODE, 16>(a, in, out, name, bytes, s);
-    return launch_1k_nr<MODE, 32>(a, in, out, name, bytes, s);
+    if (nr <= 16) return launch_1k_nr<MODE, 16, S>(a, in, out, name, bytes, s);
+    return launch_1k_nr<MODE, 32, S>(a, in, out, name, bytes, s);
   } else {
     const int nr = (a.V + 31) / 32;
-    if (nr <= 4) return launch_1k_nr<MODE, 4>(a, in, out, name, bytes, s);
-    if (nr <= 8) return launch_1k_nr<MODE, 8>(a, in, out, name, bytes, s);
-    if (nr <= 16) return launch_1k_nr<MODE, 16>(a, in, out, name, bytes, s);
-    if constexpr (MODE == 1) return launch_1k_nr<MODE, 32>(a, in, out, name, bytes, s);
+    if (nr <= 4) return launch_1k_nr<MODE, 4, S>(a, in, out, name, bytes, s);
+    if (nr <= 8) return launch_1k_nr<MODE, 8, S>(a, in, out, name, bytes, s);
+    if (nr <= 16) return launch_1k_nr<MODE, 16, S>(a, in, out, name, bytes, s);
+    if constexpr (MODE == 1) return launch_1k_nr<MODE, 32, S>(a, in, out, name, bytes, s);
     return BL_ERR_UNSUPPORTED;
   }
 }
@@ -807,12 +808,14 @@ int fft_size_for(int need) {
   return M;
 }
 
-template <int MODE>
+// S: the stored-spectrum element the forward modes write (the inverse modes
+// read complex64 contraction outputs and take float2)
+template <int MODE, typename S = float2>
 bl_status_t launch_mode(const bl_conv_plan_s* p, BlueArgs& a, int M, const void* in, void* out, const char* name,
                         double bytes, hipStream_t s) {
-  if (M == 256) return launch_m<256, MODE>(a, in, out, name, bytes, s);
-  if (M == 512) return launch_m<512, MODE>(a, in, out, name, bytes, s);
-  if (M == 1024) return launch_1k<MODE>(p, a, in, out, name, bytes, s);
+  if (M == 256) return launch_m<256, MODE, S>(a, in, out, name, bytes, s);
+  if (M == 512) return launch_m<512, MODE, S>(a, in, out, name, bytes, s);
+  if (M == 1024) return launch_1k<MODE, S>(p, a, in, out, name, bytes, s);
   return BL_ERR_UNSUPPORTED;
 }
 
@@ -831,11 +834,13 @@ bl_status_t launch_any(const bl_conv_plan_s* p, BlueArgs& a, bool inv, int other
     if (pack) {
       a.n_out = 2 * a.V - 1;
       a.off_out = -(a.V - 1);
-      return launch_mode<2>(p, a, M2, in, out, name, bytes, s);
+      return p->bf16 ? launch_mode<2, unsigned>(p, a, M2, in, out, name, bytes, s)
+                     : launch_mode<2, float2>(p, a, M2, in, out, name, bytes, s);
     }
     a.n_out = a.V;
     a.off_out = 0;
-    return launch_mode<0>(p, a, M1, in, out, name, bytes, s);
+    return p->bf16 ? launch_mode<0, unsigned>(p, a, M1, in, out, name, bytes, s)
+                   : launch_mode<0, float2>(p, a, M1, in, out, name, bytes, s);
   }
   a.n_out = other;
   if (pack) {
@@ -850,7 +855,7 @@ bl_status_t launch_any(const bl_conv_plan_s* p, BlueArgs& a, bool inv, int other
 
 }  // namespace
 
-bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Win, int oj,
+bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Win, int oj,
                                  hipStream_t s) {
   BlueArgs a{};
   a.L = p->Lw;
@@ -859,7 +864,7 @@ bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float
   a.nyq = (p->Lw % 2 == 0) ? p->Lw / 2 : -1;
   a.P = P;
   a.out_scale = 1.0f;
-  const double bytes = (double)P * Win * 4 + (double)P * p->V * 8;
+  const double bytes = (double)P * Win * 4 + (double)P * p->V * (p->bf16 ? 4 : 8);
   return launch_any(p, a, false, Win, in, out, "spec_fwd_1d", bytes, s);
 }
 

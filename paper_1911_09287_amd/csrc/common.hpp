@@ -13,13 +13,26 @@ namespace blc {
 
 constexpr int kThreads = 256;
 
-// bfloat16 bit pattern of x (round to nearest, ties to even; finite inputs),
-// and x rounded to bfloat16 as a float.
+// bfloat16 bit pattern of x (round to nearest, ties to even; finite inputs).
 __device__ __forceinline__ unsigned bf16_bits(float x) {
   const unsigned u = __float_as_uint(x);
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
-__device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(bf16_bits(x) << 16); }
+
+// Stored spectra (X, W and DY in the workspace) hold complex64 values, or in
+// plans with BL_DESC_BF16_SPECTRA bfloat16 pairs in 32-bit words (real
+// part in the low half, imaginary part in the high half).  Kernels that
+// produce or consume them are instantiated for both element types: float2
+// and unsigned.
+__device__ __forceinline__ void spec_put(float2* o, size_t i, float2 v) { o[i] = v; }
+__device__ __forceinline__ void spec_put(unsigned* o, size_t i, float2 v) {
+  o[i] = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
+}
+__device__ __forceinline__ float2 spec_unpack(unsigned u) {
+  return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xFFFF0000u));
+}
+__device__ __forceinline__ float2 spec_get(const float2* o, size_t i) { return o[i]; }
+__device__ __forceinline__ float2 spec_get(const unsigned* o, size_t i) { return spec_unpack(o[i]); }
 constexpr size_t kMaxLds = 64 * 1024;
 
 // ---- per-kernel timing (bl_profile_*) -------------------------------------
@@ -64,46 +77,49 @@ long float_key(float x);  // bit pattern of x, for keys
 // ---- stage launchers --------------------------------------------------------
 // Real planes [P][Hin][Win] placed at (oi, oj) of the grid -> kept spectrum
 // out[b * P + p] (bin-major).
-bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win,
+// `out` holds the plan's stored-spectrum type (complex64 or bfloat16 pairs).
+bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
                             int oi, int oj, hipStream_t s);
 // Kept spectrum in[b * P + p] -> real planes [P][OH][OW] holding the grid
 // window that starts at (ci, cj), scaled by 1 / (Lh Lw).
 bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s);
-// Filter w [F][C][Kh][Kw] -> W[b][c][f].
-bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* out, hipStream_t s);
+// Filter w [F][C][Kh][Kw] -> W[b][c][f] (stored-spectrum type).
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s);
 // DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats.
 bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s);
 
+// Operands A and Bm are stored spectra (complex64 or bfloat16 pairs); the
+// output O and the split-k partials are complex64.
 enum class Contract { Forward, GradInput, GradWeight };
-bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm, float2* O,
                             float2* part, hipStream_t s);
 // One of M, N, K at most 8: memory-bound, on the vector ALUs (thin.hip).
 bool contract_is_thin(const bl_conv_plan_s* p, Contract which);
-bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                  float2* O, hipStream_t s);
 // Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
 // generic one (any strides and sizes).
-bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                   float2* O, float2* part, hipStream_t s);
-bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                     float2* O, hipStream_t s);
 
 // Direct (pruned DFT) transforms: any grid; used where no fast path applies.
-bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win,
+bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
                                    int oi, int oj, hipStream_t s);
 bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW,
                                    int ci, int cj, hipStream_t s);
 
 // 1-D transforms by Bluestein's chirp-z algorithm over a power-of-two FFT.
 // Return BL_ERR_UNSUPPORTED when the shape is outside the fast path.
-bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Win, int oj,
+bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Win, int oj,
                                  hipStream_t s);
 bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
                                  hipStream_t s);
 
 // 2-D transforms on (2 MH) x (2 MW) grids with MH, MW odd (mixed radix 2 x odd).
-bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s);
 bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s);

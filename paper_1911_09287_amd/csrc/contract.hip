@@ -18,7 +18,14 @@
 // operand fetches (one 32-bit read per lane) and the stores are free of bank
 // conflicts.  Blocks are numbered so that consecutive tiles (which share
 // operand rows) run on the same XCD and its L2.
+//
+// With bfloat16 storage of the spectra the operands arrive as 32-bit (re, im)
+// pairs (8-byte vectors, two values each) and run on v_mfma_f32_32x32x8_bf16,
+// four complex k per instruction: A is staged as the pairs themselves, B as
+// its two block columns per value, each a bf16 pair, with the signs applied to
+// the bits.  Products of bfloat16 values are exact in the fp32 accumulators.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -49,9 +56,16 @@ constexpr int plane_floats() {
 
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 
+// BF16: operands stored as bfloat16 pairs (32-bit words, real part in the low
+// half), multiplied on the bf16 matrix cores with fp32 accumulation; else
+// complex64 on the fp32 ones.
 template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16>
-__global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, const float2* __restrict__ Bm,
+__global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, const void* __restrict__ B_,
                                                float2* __restrict__ O, CgemmArgs g) {
+  using S = std::conditional_t<BF16, unsigned, float2>;  // stored operand element
+  using V = std::conditional_t<BF16, uint2, float4>;     // two consecutive elements
+  const S* A = static_cast<const S*>(A_);
+  const S* Bm = static_cast<const S*>(B_);
   constexpr int WM = BM / 2;   // rows per wave
   constexpr int WN = BN / 2;   // complex columns per wave
   constexpr int MI = WM / 32;  // 32-row MFMA blocks per wave
@@ -81,8 +95,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
   const int kend = min(g.K, kbeg + g.kper);
   const int tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const float2* Ab = A + bin * g.bA;
-  const float2* Bb = Bm + bin * g.bB;
+  const S* Ab = A + bin * g.bA;
+  const S* Bb = Bm + bin * g.bB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
 
@@ -104,8 +118,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
-  // Operand positions of this thread's 16-byte vectors in a stage, and whether
+  const V zero4{};
+  // Operand positions of this thread's two-element vectors in a stage, and whether
   // they lie inside the matrices.  Loads are unconditional (a vector outside
   // reads the bin's first one, which always exists) and the zero fill happens
   // when the registers are stored to LDS, so no branch separates a prefetch
@@ -120,14 +134,14 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
     if (B_NC) { k = e / (BN / 2); n = (e - k * (BN / 2)) * 2; }
     else { n = e >> 3; k = (e & 7) * 2; }
   };
-  auto load = [&](int k0, float4* ra, float4* rb) {
+  auto load = [&](int k0, V* ra, V* rb) {
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
       int m, k;
       a_pos(q, m, k);
       const bool in = (m0 + m < g.M) && (k0 + k < kend);
       const unsigned off = in ? (unsigned)(m0 + m) * g.sAm + (unsigned)(k0 + k) * g.sAk : 0u;
-      ra[q] = *reinterpret_cast<const float4*>(Ab + off);
+      ra[q] = *reinterpret_cast<const V*>(Ab + off);
     }
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
@@ -135,27 +149,27 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
       b_pos(q, k, n);
       const bool in = (n0 + n < g.N) && (k0 + k < kend);
       const unsigned off = in ? (unsigned)(k0 + k) * g.sBk + (unsigned)(n0 + n) * g.sBn : 0u;
-      rb[q] = *reinterpret_cast<const float4*>(Bb + off);
+      rb[q] = *reinterpret_cast<const V*>(Bb + off);
     }
   };
-  auto pack = [](float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); };
-  // the two forms of complex value (br, bi): conj block [[br, -bi], [bi, br]],
-  // identity block [[br, bi], [-bi, br]]; form f is column f of the block
-  auto form0 = [&](float br, float bi) { return CONJ ? pack(br, bi) : pack(br, -bi); };
-  auto form1 = [&](float br, float bi) { return CONJ ? pack(-bi, br) : pack(bi, br); };
-  auto store16 = [&](int buf, int k0, const float4* ra, const float4* rb) {
+  // the two forms of a stored value w = (br, bi): conj block [[br, -bi], [bi, br]],
+  // identity block [[br, bi], [-bi, br]]; form f is column f of the block,
+  // (even, odd) halves = (real-k rows 2k, 2k + 1); negation flips a sign bit
+  auto form0 = [](unsigned w) { return CONJ ? w : w ^ 0x80000000u; };
+  auto form1 = [](unsigned w) { return CONJ ? ((w >> 16) ^ 0x8000u) | (w << 16) : (w >> 16) | (w << 16); };
+  auto store16 = [&](int buf, int k0, const V* ra, const V* rb) {
     unsigned* a16 = As16[buf];
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
       int m, k;
       a_pos(q, m, k);
-      const float4 r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
+      const V r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
       if (A_KC) {
-        a16[k * SA16 + m] = pack(r.x, r.y);
-        a16[(k + 1) * SA16 + m] = pack(r.z, r.w);
+        a16[k * SA16 + m] = r.x;
+        a16[(k + 1) * SA16 + m] = r.y;
       } else {
-        a16[k * SA16 + m] = pack(r.x, r.y);
-        a16[k * SA16 + m + 1] = pack(r.z, r.w);
+        a16[k * SA16 + m] = r.x;
+        a16[k * SA16 + m + 1] = r.y;
       }
     }
     unsigned* b16 = Bs16[buf];
@@ -163,48 +177,48 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
     for (int q = 0; q < BV; ++q) {
       int k, n;
       b_pos(q, k, n);
-      const float4 r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
+      const V r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
       // second value at (k, n + 1) when n runs along the vector, else (k + 1, n)
       const int i0 = k * SB16 + n, i1 = B_NC ? i0 + 1 : i0 + SB16;
-      b16[i0] = form0(r.x, r.y);
-      b16[PB16 + i0] = form1(r.x, r.y);
-      b16[i1] = form0(r.z, r.w);
-      b16[PB16 + i1] = form1(r.z, r.w);
+      b16[i0] = form0(r.x);
+      b16[PB16 + i0] = form1(r.x);
+      b16[i1] = form0(r.y);
+      b16[PB16 + i1] = form1(r.y);
     }
   };
-  auto store = [&](int buf, int k0, const float4* ra, const float4* rb) {
+  auto store = [&](int buf, int k0, const V* ra, const V* rb) {
     if constexpr (BF16) {
       store16(buf, k0, ra, rb);
-      return;
-    }
-    float* a0 = As[buf];
-    float* a1 = As[buf] + PA;
+    } else {
+      float* a0 = As[buf];
+      float* a1 = As[buf] + PA;
 #pragma unroll
-    for (int q = 0; q < AV; ++q) {
-      int m, k;
-      a_pos(q, m, k);
-      const float4 r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
-      if (A_KC) {
-        a0[k * SA + m] = r.x; a1[k * SA + m] = r.y;
-        a0[(k + 1) * SA + m] = r.z; a1[(k + 1) * SA + m] = r.w;
-      } else {
-        *reinterpret_cast<float2*>(a0 + k * SA + m) = make_float2(r.x, r.z);
-        *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(r.y, r.w);
+      for (int q = 0; q < AV; ++q) {
+        int m, k;
+        a_pos(q, m, k);
+        const float4 r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
+        if (A_KC) {
+          a0[k * SA + m] = r.x; a1[k * SA + m] = r.y;
+          a0[(k + 1) * SA + m] = r.z; a1[(k + 1) * SA + m] = r.w;
+        } else {
+          *reinterpret_cast<float2*>(a0 + k * SA + m) = make_float2(r.x, r.z);
+          *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(r.y, r.w);
+        }
       }
-    }
-    float* b0 = Bs[buf];
-    float* b1 = Bs[buf] + PB;
+      float* b0 = Bs[buf];
+      float* b1 = Bs[buf] + PB;
 #pragma unroll
-    for (int q = 0; q < BV; ++q) {
-      int k, n;
-      b_pos(q, k, n);
-      const float4 r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
-      if (B_NC) {
-        *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(r.x, r.z);
-        *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(r.y, r.w);
-      } else {
-        b0[k * SB + n] = r.x; b1[k * SB + n] = r.y;
-        b0[(k + 1) * SB + n] = r.z; b1[(k + 1) * SB + n] = r.w;
+      for (int q = 0; q < BV; ++q) {
+        int k, n;
+        b_pos(q, k, n);
+        const float4 r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
+        if (B_NC) {
+          *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(r.x, r.z);
+          *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(r.y, r.w);
+        } else {
+          b0[k * SB + n] = r.x; b1[k * SB + n] = r.y;
+          b0[(k + 1) * SB + n] = r.z; b1[(k + 1) * SB + n] = r.w;
+        }
       }
     }
   };
@@ -269,7 +283,7 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const float2* __restrict__ A, 
   // an all-zero stage (its MFMAs add nothing).
   const int nst = (kend - kbeg + kBK - 1) / kBK;
   auto kof = [&](int st) { return kbeg + min(st, nst - 1) * kBK; };
-  float4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
+  V ra0[AV], rb0[BV], ra1[AV], rb1[BV];
   load(kof(0), ra0, rb0);
   load(kof(1), ra1, rb1);
   store(0, kbeg, ra0, rb0);
@@ -317,7 +331,7 @@ __global__ __launch_bounds__(256) void k_split_reduce(const float4* __restrict__
 
 // Tiled path: needs 16-byte aligned pairs of complex values along the
 // contiguous dimension of each operand; returns BL_ERR_UNSUPPORTED otherwise.
-bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                   float2* O, float2* part, hipStream_t s) {
   CgemmArgs g{};
   const unsigned long long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
@@ -364,7 +378,8 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   // (tile, bin) pairs as a 2-D grid; the kernel renumbers them per XCD
   dim3 grid((unsigned)g.tiles, (unsigned)B, (unsigned)splits);
   const double flops = 8.0 * B * g.M * g.N * g.K;
-  const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
+  const double ob = p->bf16 ? 4.0 : 8.0;  // bytes per stored operand element
+  const double bytes = B * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
   const char* name = which == Contract::Forward ? "contract_fwd"
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
   bl_status_t st = BL_ERR_UNSUPPORTED;

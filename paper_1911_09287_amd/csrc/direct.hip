@@ -44,7 +44,9 @@ struct FwdGeom {
   int TP;
 };
 
-__global__ __launch_bounds__(kThreads) void k_spec_fwd(const float* __restrict__ in, float2* __restrict__ out,
+// S: stored-spectrum element of the output (float2 or bfloat16 pairs)
+template <typename S>
+__global__ __launch_bounds__(kThreads) void k_spec_fwd(const float* __restrict__ in, S* __restrict__ out,
                                                        FwdGeom g) {
   extern __shared__ float2 smem[];
   float2* twh = smem;                       // Lh
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void k_spec_fwd(const float* __restrict__
       idx += u;
       if (idx >= g.Lh) idx -= g.Lh;
     }
-    out[(size_t)b * g.P + p0 + p] = make_float2(re, im);
+    spec_put(out, (size_t)b * g.P + p0 + p, make_float2(re, im));
   }
 }
 
@@ -202,9 +204,9 @@ struct FiltGeom {
   int bins_per_block;
 };
 
-template <int KH, int KW>
+template <int KH, int KW, typename S>
 __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, const float2* __restrict__ roots,
-                                                        float2* __restrict__ out, FiltGeom g) {
+                                                        S* __restrict__ out, FiltGeom g) {
   // roots: e^{-2 pi i k / Lh} (k < Lh) then e^{-2 pi i k / Lw} (k < Lw), from
   // a table built once per plan
   extern __shared__ float2 smem[];
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
       re = fmaf(rr, t.x, fmaf(-ri, t.y, re));
       im = fmaf(rr, t.y, fmaf(ri, t.x, im));
     }
-    out[(size_t)bin * CF + q] = make_float2(re, im);
+    spec_put(out, (size_t)bin * CF + q, make_float2(re, im));
     if (++v == g.V) {
       v = 0;
       ++r;
@@ -481,23 +483,24 @@ struct ContractArgs {
   long sAm, sAk, sBk, sBn, ldo;  // element strides (complex units)
   long bA, bB, bO;               // per-bin strides
   int tiles_n;
-  int bf16;                      // operands rounded to bfloat16 (exact products, fp32 sums)
 };
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int CBM = 64, CBN = 32, CBK = 16;
 
-template <bool A_K_CONTIG, bool B_N_CONTIG, bool CONJ>
-__global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict__ A, const float2* __restrict__ Bm,
+// S: stored-spectrum element of the operands (float2, or bfloat16 pairs whose
+// products the fp32 MFMA forms exactly)
+template <bool A_K_CONTIG, bool B_N_CONTIG, bool CONJ, typename S>
+__global__ __launch_bounds__(kThreads) void k_contract(const S* __restrict__ A, const S* __restrict__ Bm,
                                                        float2* __restrict__ O, ContractArgs g) {
   __shared__ float As[2][CBK][CBM];
   __shared__ float Bs[2][CBK][CBN];
   const int bin = blockIdx.y;
   const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
   const int m0 = tm * CBM, n0 = tn * CBN;
-  const float2* Ab = A + (size_t)bin * g.bA;
-  const float2* Bb = Bm + (size_t)bin * g.bB;
+  const S* Ab = A + (size_t)bin * g.bA;
+  const S* Bb = Bm + (size_t)bin * g.bB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * 32, wn = (wave & 1) * 16;
 
@@ -529,8 +532,7 @@ __global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict_
         k = e >> 6; m = e & 63;
       }
       float2 v = make_float2(0.f, 0.f);
-      if (m0 + m < g.M && k0 + k < g.K) v = Ab[(size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk];
-      if (g.bf16) v = make_float2(bf16_round(v.x), bf16_round(v.y));
+      if (m0 + m < g.M && k0 + k < g.K) v = spec_get(Ab, (size_t)(m0 + m) * g.sAm + (size_t)(k0 + k) * g.sAk);
       As[0][k][m] = v.x;
       As[1][k][m] = v.y;
     }
@@ -542,8 +544,7 @@ __global__ __launch_bounds__(kThreads) void k_contract(const float2* __restrict_
       if (B_N_CONTIG) { k = e >> 5; n = e & 31; }
       else { n = e >> 4; k = e & 15; }
       float2 v = make_float2(0.f, 0.f);
-      if (n0 + n < g.N && k0 + k < g.K) v = Bb[(size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn];
-      if (g.bf16) v = make_float2(bf16_round(v.x), bf16_round(v.y));
+      if (n0 + n < g.N && k0 + k < g.K) v = spec_get(Bb, (size_t)(k0 + k) * g.sBk + (size_t)(n0 + n) * g.sBn);
       Bs[0][k][n] = v.x;
       Bs[1][k][n] = v.y;
     }
@@ -581,7 +582,7 @@ int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap
 // ---------------------------------------------------------------------------
 
 // Real planes [P][Hin][Win] at offset (oi, oj) -> bin-major kept spectrum.
-bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s) {
   FwdGeom g{Hin, Win, oi, oj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0};
   const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
@@ -590,9 +591,14 @@ bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, flo
   g.TP = planes_per_block(fixed, per, P, 16);
   const size_t lds = fixed + g.TP * per;
   const long blocks = (P + g.TP - 1) / g.TP;
-  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
+  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
   return timed_launch("spec_fwd_direct", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL(k_spec_fwd, dim3((unsigned)blocks), dim3(kThreads), lds, s, e0, e1, 0, in, out, g);
+    if (p->bf16)
+      hipExtLaunchKernelGGL(k_spec_fwd<unsigned>, dim3((unsigned)blocks), dim3(kThreads), lds, s, e0, e1, 0, in,
+                            static_cast<unsigned*>(out), g);
+    else
+      hipExtLaunchKernelGGL(k_spec_fwd<float2>, dim3((unsigned)blocks), dim3(kThreads), lds, s, e0, e1, 0, in,
+                            static_cast<float2*>(out), g);
   });
 }
 
@@ -626,7 +632,7 @@ void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
     }
 }
 
-bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* out, hipStream_t s) {
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s) {
   FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
   const float2* roots = nullptr;
   const std::vector<long> key{3, p->Lh, p->Lw};
@@ -641,11 +647,16 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, float2* ou
   chunks = (B + g.bins_per_block - 1) / g.bins_per_block;
   const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
   dim3 grid((unsigned)xblocks, (unsigned)chunks);
-  const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * 8;
-#define X(a, b)                                                                                 \
-  if (p->Kh == a && p->Kw == b)                                                                 \
-    return timed_launch("spec_filt", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {        \
-      hipExtLaunchKernelGGL((k_spec_filt<a, b>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, roots, out, g); \
+  const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * (p->bf16 ? 4 : 8);
+#define X(a, b)                                                                                             \
+  if (p->Kh == a && p->Kw == b)                                                                             \
+    return timed_launch("spec_filt", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {                    \
+      if (p->bf16)                                                                                          \
+        hipExtLaunchKernelGGL((k_spec_filt<a, b, unsigned>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, roots, \
+                              static_cast<unsigned*>(out), g);                                              \
+      else                                                                                                  \
+        hipExtLaunchKernelGGL((k_spec_filt<a, b, float2>), grid, dim3(kThreads), lds, s, e0, e1, 0, w, roots,   \
+                              static_cast<float2*>(out), g);                                                \
     });
   BL_FILT_CASES(X)
 #undef X
@@ -734,7 +745,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   });
 }
 
-bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm, float2* O,
+bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm, float2* O,
                             hipStream_t s) {
   ContractArgs g{};
   const long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
@@ -757,25 +768,33 @@ bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, con
   }
   const int tiles_m = (g.M + CBM - 1) / CBM;
   g.tiles_n = (g.N + CBN - 1) / CBN;
-  g.bf16 = p->bf16 ? 1 : 0;
   if (B > 65535) return BL_ERR_UNSUPPORTED;
   dim3 grid((unsigned)(tiles_m * g.tiles_n), (unsigned)B);
   // complex MAC = 8 real flops; compulsory traffic: both operands and the result once
   const double flops = 8.0 * B * g.M * g.N * g.K;
-  const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
+  const double ob = p->bf16 ? 4.0 : 8.0;  // bytes per stored operand element
+  const double bytes = B * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
+  const char* name = which == Contract::Forward ? "contract_fwd"
+                     : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
+  auto go = [&](auto kern, auto* a, auto* b) {
+    return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+      hipExtLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, e0, e1, 0, a, b, O, g);
+    });
+  };
+  const unsigned* A16 = static_cast<const unsigned*>(A);
+  const unsigned* B16 = static_cast<const unsigned*>(Bm);
+  const float2* A32 = static_cast<const float2*>(A);
+  const float2* B32 = static_cast<const float2*>(Bm);
   switch (which) {
     case Contract::Forward:
-      return timed_launch("contract_fwd", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL((k_contract<true, true, true>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
-      });
+      return p->bf16 ? go(k_contract<true, true, true, unsigned>, A16, B16)
+                     : go(k_contract<true, true, true, float2>, A32, B32);
     case Contract::GradInput:
-      return timed_launch("contract_dgrad", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL((k_contract<true, false, false>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
-      });
+      return p->bf16 ? go(k_contract<true, false, false, unsigned>, A16, B16)
+                     : go(k_contract<true, false, false, float2>, A32, B32);
     case Contract::GradWeight:
-      return timed_launch("contract_wgrad", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL((k_contract<false, true, true>), grid, dim3(kThreads), 0, s, e0, e1, 0, A, Bm, O, g);
-      });
+      return p->bf16 ? go(k_contract<false, true, true, unsigned>, A16, B16)
+                     : go(k_contract<false, true, true, float2>, A32, B32);
   }
   return BL_ERR_INVALID_ARG;
 }

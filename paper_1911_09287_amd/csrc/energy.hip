@@ -23,23 +23,25 @@ namespace {
 
 constexpr int kEnergyThreads = 1024;
 
-__global__ __launch_bounds__(kEnergyThreads) void k_bin_energy(const float2* __restrict__ X, double* __restrict__ e,
+// S: stored-spectrum element (float2 or bfloat16 pairs)
+template <typename S>
+__global__ __launch_bounds__(kEnergyThreads) void k_bin_energy(const S* __restrict__ X, double* __restrict__ e,
                                                                long P, int V, int nyq) {
   __shared__ double red[kEnergyThreads];
   const int b = blockIdx.x, tid = threadIdx.x;
-  const float2* row = X + (size_t)b * P;
+  const S* row = X + (size_t)b * P;
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
   long i = tid;
   // four loads of a thread in flight together
   for (; i + 3 * kEnergyThreads < P; i += 4 * kEnergyThreads) {
     float2 z[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) z[k] = row[i + k * kEnergyThreads];
+    for (int k = 0; k < 4; ++k) z[k] = spec_get(row, i + k * kEnergyThreads);
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[k] += (double)z[k].x * z[k].x + (double)z[k].y * z[k].y;
   }
   for (int k = 0; i < P; i += kEnergyThreads, ++k) {
-    const float2 z = row[i];
+    const float2 z = spec_get(row, i);
     acc[k & 3] += (double)z.x * z.x + (double)z.y * z.y;
   }
   red[tid] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
@@ -66,7 +68,7 @@ extern "C" bl_status_t bl_conv_input_energy(bl_conv_plan_t p, const float* x, vo
   if (!(flags & BL_REUSE_X) && !x) return BL_ERR_INVALID_ARG;
   if (p->kept > 2147483647L) return BL_ERR_UNSUPPORTED;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  float2* X = reinterpret_cast<float2*>(static_cast<char*>(ws) + p->off_X);
+  void* X = static_cast<char*>(ws) + p->off_X;
   const long P = (long)p->N * p->Cin;
   if (!(flags & BL_REUSE_X)) {
     const bl_status_t st = launch_spec_fwd(p, x, X, P, p->Hi, p->Wi, p->pt, p->pl, s);
@@ -76,10 +78,14 @@ extern "C" bl_status_t bl_conv_input_energy(bl_conv_plan_t p, const float* x, vo
   // one block per bin (splitting the bins of small grids over several blocks
   // and summing the slices in a second pass measured slower: the pass costs
   // more than the parallelism gains)
-  const double bytes = 8.0 * (double)p->kept * P + 8.0 * (double)p->kept;
+  const double bytes = (p->bf16 ? 4.0 : 8.0) * (double)p->kept * P + 8.0 * (double)p->kept;
   return timed_launch("input_energy", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL(k_bin_energy, dim3((unsigned)p->kept), dim3(kEnergyThreads), 0, s, e0, e1, 0, X, energy,
-                          P, p->V, nyq);
+    if (p->bf16)
+      hipExtLaunchKernelGGL(k_bin_energy<unsigned>, dim3((unsigned)p->kept), dim3(kEnergyThreads), 0, s, e0, e1, 0,
+                            static_cast<const unsigned*>(X), energy, P, p->V, nyq);
+    else
+      hipExtLaunchKernelGGL(k_bin_energy<float2>, dim3((unsigned)p->kept), dim3(kEnergyThreads), 0, s, e0, e1, 0,
+                            static_cast<const float2*>(X), energy, P, p->V, nyq);
   });
 }
 

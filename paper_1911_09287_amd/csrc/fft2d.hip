@@ -142,8 +142,9 @@ __device__ __forceinline__ int row_slot(int u, int r_h, int R, int LH) {
 
 // LDS layout (complex spectra, column-major per plane): S[p * PS + v * (LH + 1) + i],
 // so a column thread reads its LH rows at fixed offsets.
-template <int MH, int MW>
-__global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, float2* __restrict__ out,
+// S: stored-spectrum element of the output (float2 or bfloat16 pairs)
+template <int MH, int MW, typename S>
+__global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, S* __restrict__ out,
                                                        Fft2Args g) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
   extern __shared__ float2 sm[];
@@ -219,15 +220,15 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
     float2 E[MH], O[MH];
     dft_odd<MH, false>(ev, E);
     dft_odd<MH, false>(od, O);
-    float2* dst = out + (p0 + p) + (unsigned)v * g.P;
+    S* dst = out + (p0 + p) + (unsigned)v * g.P;
     const unsigned rs = (unsigned)g.V * g.P;
 #pragma unroll
     for (int k = 0; k < MH; ++k) {
       const float2 t = cmul(root<LH, false>(k), O[k]);
       const int r_lo = row_slot(k, g.r_h, g.R, LH);
       const int r_hi = row_slot(k + MH, g.r_h, g.R, LH);
-      if (r_lo >= 0) dst[r_lo * rs] = cadd(E[k], t);
-      if (r_hi >= 0) dst[r_hi * rs] = csub(E[k], t);
+      if (r_lo >= 0) spec_put(dst, (unsigned)r_lo * rs, cadd(E[k], t));
+      if (r_hi >= 0) spec_put(dst, (unsigned)r_hi * rs, csub(E[k], t));
     }
   }
 }
@@ -320,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
 unsigned magic_for(unsigned d) { return d > 1 ? (unsigned)((0x100000000ull + d - 1) / d) : 0u; }
 
 template <int MH, int MW>
-bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                          int oj, hipStream_t s) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if (Win % 4 != 0 || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
@@ -339,12 +340,17 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, float2* out, 
   if (Hin > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
   g.G = G;
   const long blocks = (P + G - 1) / G;
-  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * 8;
+  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
   // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
   // complex LH-point column FFTs (5 LH log2 LH) per plane
   const double flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
   return timed_launch("spec_fwd_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0, e1, 0, in, out, g);
+    if (p->bf16)
+      hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0,
+                            e1, 0, in, static_cast<unsigned*>(out), g);
+    else
+      hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0,
+                            e1, 0, in, static_cast<float2*>(out), g);
   });
 }
 
@@ -379,7 +385,7 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
 
 }  // namespace
 
-bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, float2* out, long P, int Hin, int Win, int oi,
+bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s) {
 #define X(a, b) \
   if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_fwd_t<a, b>(p, in, out, P, Hin, Win, oi, oj, s);

@@ -30,7 +30,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   if (d->pad_lo[0] < 0 || d->pad_hi[0] < 0 || d->pad_lo[1] < 0 || d->pad_hi[1] < 0) return BL_ERR_INVALID_ARG;
   if (!(d->c >= 0.0 && d->c < 1.0)) return BL_ERR_INVALID_ARG;  // also rejects NaN
   if (d->fft_h < 0 || d->fft_w < 0) return BL_ERR_INVALID_ARG;
-  if (d->flags & ~BL_DESC_BF16_CONTRACTION) return BL_ERR_INVALID_ARG;
+  if (d->flags & ~BL_DESC_BF16_SPECTRA) return BL_ERR_INVALID_ARG;
   if (d->ndim == 1 && (d->W != 1 || d->pad_lo[1] != 0 || d->pad_hi[1] != 0 || d->fft_w > 1))
     return BL_ERR_INVALID_ARG;
   if (d->ndim == 2 && d->W <= 0) return BL_ERR_INVALID_ARG;
@@ -40,7 +40,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   if (!p) return BL_ERR_OOM;
   p->desc = *d;
   p->ndim = d->ndim;
-  p->bf16 = (d->flags & BL_DESC_BF16_CONTRACTION) != 0;
+  p->bf16 = (d->flags & BL_DESC_BF16_SPECTRA) != 0;
   p->N = d->N; p->Cin = d->C_in; p->Cout = d->C_out;
   if (d->ndim == 2) {
     p->Hi = d->H; p->Wi = d->W; p->Kh = d->K; p->Kw = d->K;
@@ -93,12 +93,13 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
     for (int v = 0; v < p->V; ++v) p->mask[(size_t)u * p->Wh + v] = 1;
   }
 
-  const size_t cb = 8;  // complex64
+  const size_t cb = 8;                  // complex64
+  const size_t sb = p->bf16 ? 4 : cb;  // a stored spectrum's element: complex64 or a bfloat16 pair
   const size_t B = (size_t)p->kept;
   size_t o = 0;
-  p->off_X = o;  o = align_up(o + B * p->N * p->Cin * cb, 256);
-  p->off_W = o;  o = align_up(o + B * p->Cin * p->Cout * cb, 256);
-  p->off_DY = o; o = align_up(o + B * p->N * p->Cout * cb, 256);
+  p->off_X = o;  o = align_up(o + B * p->N * p->Cin * sb, 256);
+  p->off_W = o;  o = align_up(o + B * p->Cin * p->Cout * sb, 256);
+  p->off_DY = o; o = align_up(o + B * p->N * p->Cout * sb, 256);
   p->off_T = o;  o = align_up(o + B * p->N * (size_t)std::max(p->Cin, p->Cout) * cb, 256);
   p->off_DW = o; o = align_up(o + B * p->Cin * p->Cout * cb, 256);
   // partial sums of the weight-gradient inverse DFT over bin slices: enough

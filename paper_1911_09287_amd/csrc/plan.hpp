@@ -58,7 +58,7 @@ inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
 struct bl_conv_plan_s {
   bl_conv_desc_t desc;
   int ndim;
-  bool bf16;           // contraction operands rounded to bfloat16
+  bool bf16;           // stored spectra X, W, DY as bfloat16 pairs (BL_DESC_BF16_SPECTRA)
   int N, Cin, Cout;
   // row form
   int Hi, Wi;          // input plane

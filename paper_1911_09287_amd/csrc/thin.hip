@@ -28,18 +28,13 @@ struct ThinArgs {
   int ks;                        // waves splitting k: 1 (a wave per item) or 4 (a block per item)
 };
 
-// BF16: operands rounded to bfloat16 (exact products, fp32 sums)
-template <bool BF16>
-__device__ __forceinline__ float2 operand(float2 v) {
-  return BF16 ? make_float2(bf16_round(v.x), bf16_round(v.y)) : v;
-}
-
 __device__ __forceinline__ float2 cmac(float2 acc, float2 a, float2 b) {
   return make_float2(fmaf(a.x, b.x, fmaf(-a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(a.y, b.x, acc.y)));
 }
 
-template <int MT, bool CONJ, bool BF16>
-__global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A, const float2* __restrict__ B,
+// S: stored-spectrum element of the operands (float2 or bfloat16 pairs)
+template <int MT, bool CONJ, typename S>
+__global__ __launch_bounds__(256) void k_thin_cols(const S* __restrict__ A, const S* __restrict__ B,
                                                    float2* __restrict__ O, ThinArgs g) {
   __shared__ float2 red[3][MT][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -53,8 +48,8 @@ __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A,
     k0 = min(g.K, wave * kc);
     k1 = min(g.K, k0 + kc);
   }
-  const float2* Ab = A + (size_t)blockIdx.y * g.bA;
-  const float2* Bb = B + (size_t)blockIdx.y * g.bB + (live ? (long)n * g.sBn : 0);
+  const S* Ab = A + (size_t)blockIdx.y * g.bA;
+  const S* Bb = B + (size_t)blockIdx.y * g.bB + (live ? (long)n * g.sBn : 0);
   float2 acc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i] = make_float2(0.f, 0.f);
@@ -65,10 +60,10 @@ __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A,
     for (int i = 0; i < MT; ++i) arow[i] = (long)min(m0 + i, g.M - 1) * g.sAm;
 #pragma unroll 4
     for (int k = k0; k < k1; ++k) {
-      float2 b = operand<BF16>(Bb[(long)k * g.sBk]);
+      float2 b = spec_get(Bb, (long)k * g.sBk);
       if (CONJ) b.y = -b.y;
 #pragma unroll
-      for (int i = 0; i < MT; ++i) acc[i] = cmac(acc[i], operand<BF16>(Ab[arow[i] + (long)k * g.sAk]), b);
+      for (int i = 0; i < MT; ++i) acc[i] = cmac(acc[i], spec_get(Ab, arow[i] + (long)k * g.sAk), b);
     }
   }
   if (g.ks == 4) {
@@ -91,23 +86,23 @@ __global__ __launch_bounds__(256) void k_thin_cols(const float2* __restrict__ A,
     if (m0 + i < g.M) Ob[(long)(m0 + i) * g.ldo] = acc[i];
 }
 
-template <int NT, bool CONJ, bool BF16>
-__global__ __launch_bounds__(256) void k_thin_rows(const float2* __restrict__ A, const float2* __restrict__ B,
+template <int NT, bool CONJ, typename S>
+__global__ __launch_bounds__(256) void k_thin_rows(const S* __restrict__ A, const S* __restrict__ B,
                                                    float2* __restrict__ O, ThinArgs g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m = (int)blockIdx.x * 4 + wave;
   if (m >= g.M) return;  // whole waves leave together; no block barrier follows
-  const float2* Ab = A + (size_t)blockIdx.y * g.bA + (long)m * g.sAm;
-  const float2* Bb = B + (size_t)blockIdx.y * g.bB;
+  const S* Ab = A + (size_t)blockIdx.y * g.bA + (long)m * g.sAm;
+  const S* Bb = B + (size_t)blockIdx.y * g.bB;
   float2 acc[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) acc[j] = make_float2(0.f, 0.f);
   for (int k = lane; k < g.K; k += 64) {
-    const float2 a = operand<BF16>(Ab[(long)k * g.sAk]);
+    const float2 a = spec_get(Ab, (long)k * g.sAk);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       // columns past N repeat the last one (computed, never written)
-      float2 b = operand<BF16>(Bb[(long)k * g.sBk + (long)min(j, g.N - 1) * g.sBn]);
+      float2 b = spec_get(Bb, (long)k * g.sBk + (long)min(j, g.N - 1) * g.sBn);
       if (CONJ) b.y = -b.y;
       acc[j] = cmac(acc[j], a, b);
     }
@@ -144,7 +139,7 @@ bool contract_is_thin(const bl_conv_plan_s* p, Contract which) {
   return std::min({M, Nn, K}) <= 8;
 }
 
-bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const float2* A, const float2* Bm,
+bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                  float2* O, hipStream_t s) {
   ThinArgs g{};
   const long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
@@ -169,7 +164,12 @@ bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const 
   }
   if (B > 65535 || B < 1) return BL_ERR_UNSUPPORTED;
   const double flops = 8.0 * B * g.M * g.N * g.K;
-  const double bytes = 8.0 * B * ((double)g.M * g.K + (double)g.K * g.N + (double)g.M * g.N);
+  const double ob = p->bf16 ? 4.0 : 8.0;  // bytes per stored operand element
+  const double bytes = B * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
+  const unsigned* A16 = static_cast<const unsigned*>(A);
+  const unsigned* B16 = static_cast<const unsigned*>(Bm);
+  const float2* A32 = static_cast<const float2*>(A);
+  const float2* B32 = static_cast<const float2*>(Bm);
   const char* name = which == Contract::Forward ? "contract_fwd"
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
   if (std::min(g.M, g.K) <= 8) {
@@ -180,15 +180,16 @@ bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const 
     g.items = (int)items;
     g.ks = g.K >= 64 ? 4 : 1;
     const dim3 grid((unsigned)(g.ks == 4 ? items : (items + 3) / 4), (unsigned)B);
-    auto go = [&](auto kern) {
+    auto go = [&](auto kern, auto* a, auto* b) {
       return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, A, Bm, O, g);
+        hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, a, b, O, g);
       });
     };
-#define BL_THIN_C(mt)                                                                              \
-  if (MT == mt)                                                                                    \
-    return p->bf16 ? (conj ? go(k_thin_cols<mt, true, true>) : go(k_thin_cols<mt, false, true>))   \
-                   : (conj ? go(k_thin_cols<mt, true, false>) : go(k_thin_cols<mt, false, false>));
+#define BL_THIN_C(mt)                                                                                        \
+  if (MT == mt)                                                                                              \
+    return p->bf16 ? (conj ? go(k_thin_cols<mt, true, unsigned>, A16, B16)                                   \
+                           : go(k_thin_cols<mt, false, unsigned>, A16, B16))                                 \
+                   : (conj ? go(k_thin_cols<mt, true, float2>, A32, B32) : go(k_thin_cols<mt, false, float2>, A32, B32));
     BL_THIN_C(1) BL_THIN_C(2) BL_THIN_C(4) BL_THIN_C(8)
 #undef BL_THIN_C
     return BL_ERR_UNSUPPORTED;
@@ -196,15 +197,16 @@ bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const 
   if (g.N <= 8) {
     const int NT = pow2_at_least(g.N);
     const dim3 grid((unsigned)((g.M + 3) / 4), (unsigned)B);
-    auto go = [&](auto kern) {
+    auto go = [&](auto kern, auto* a, auto* b) {
       return timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-        hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, A, Bm, O, g);
+        hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, e0, e1, 0, a, b, O, g);
       });
     };
-#define BL_THIN_R(nt)                                                                              \
-  if (NT == nt)                                                                                    \
-    return p->bf16 ? (conj ? go(k_thin_rows<nt, true, true>) : go(k_thin_rows<nt, false, true>))   \
-                   : (conj ? go(k_thin_rows<nt, true, false>) : go(k_thin_rows<nt, false, false>));
+#define BL_THIN_R(nt)                                                                                        \
+  if (NT == nt)                                                                                              \
+    return p->bf16 ? (conj ? go(k_thin_rows<nt, true, unsigned>, A16, B16)                                   \
+                           : go(k_thin_rows<nt, false, unsigned>, A16, B16))                                 \
+                   : (conj ? go(k_thin_rows<nt, true, float2>, A32, B32) : go(k_thin_rows<nt, false, float2>, A32, B32));
     BL_THIN_R(1) BL_THIN_R(2) BL_THIN_R(4) BL_THIN_R(8)
 #undef BL_THIN_R
   }

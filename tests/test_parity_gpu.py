@@ -297,7 +297,7 @@ BF16_EXACT_TOL = 1e-2
 
 
 def test_bf16_contraction_parity(torch):
-    """Plans with BL_DESC_BF16_CONTRACTION against the oracle whose channel
+    """Plans with BL_DESC_BF16_SPECTRA against the oracle whose channel
     contraction rounds both operands to bfloat16 (round to nearest even) and
     sums exactly: the MFMA tiles (with and without split k), the thin
     vector-ALU contraction and the generic one, 1-D and 2-D."""
@@ -313,7 +313,7 @@ def test_bf16_contraction_parity(torch):
         for c in (0.0, 0.5):
             say(f"[bf16] {layer.name} c={c}")
             x, w, dy = synth.random_inputs(layer, 1900 + i)
-            got = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_BF16_CONTRACTION)[:3]
+            got = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_BF16_SPECTRA)[:3]
             ref = oracle_passes(layer, c, x, w, dy, rounding=bo.round_bf16)
             exact = oracle_passes(layer, c, x, w, dy)
             errs = [rel(a, b) for a, b in zip(got, ref)]
@@ -324,6 +324,74 @@ def test_bf16_contraction_parity(torch):
             assert max(errs) <= BF16_TOL, errs
             assert max(errs_exact) <= BF16_EXACT_TOL, errs_exact
             assert min(gaps) > 2 * BF16_TOL, gaps  # the tolerance separates rounded from exact
+
+
+def _decode_bf16_pairs(words):
+    u = np.ascontiguousarray(words).view(np.uint32)
+    return (u << np.uint32(16)).view(np.float32), (u & np.uint32(0xFFFF0000)).view(np.float32)
+
+
+def _check_bf16_words(words, ref):
+    """Stored bfloat16 pairs against the oracle's spectrum rounded to bfloat16:
+    equal, except parts whose fp32 value lay within its rounding error of a
+    tie, which may sit one bfloat16 ulp away, and parts that are zero or tiny
+    in exact arithmetic (imaginary parts of real bins), which keep the fp32
+    transform's absolute error (1e-5 of the spectrum's RMS bounds it)."""
+    re, im = _decode_bf16_pairs(words)
+    got = np.concatenate([re.ravel(), im.ravel()]).astype(np.float64)
+    r = np.asarray(ref).ravel()
+    want = np.concatenate([bo.round_bf16(r.real), bo.round_bf16(r.imag)])
+    diff = got != want
+    frac = float(diff.mean())
+    rms = float(np.sqrt(np.mean(np.abs(r) ** 2)))
+    bound = 2.0 ** -7 * np.maximum(np.abs(got), np.abs(want)) + 1e-5 * rms
+    excess = float(np.max((np.abs(got - want) - bound)[diff], initial=-1.0))
+    assert excess <= 0, f"a stored value is more than one bfloat16 ulp off (by {excess:.3e}, rms {rms:.3e})"
+    return frac
+
+
+def test_bf16_stored_spectra_and_energy(torch):
+    """With BL_DESC_BF16_SPECTRA the spectra X, W and DY are stored as
+    bfloat16 pairs: every forward-transform path (2-D radix 2 x odd grids,
+    1-D chirp-z over 1024 points with one or two series per transform and over
+    256/512 points, the direct DFT on odd grids, the filter transform) against
+    the oracle's spectra rounded to bfloat16, and the per-bin input energies of
+    the stored spectrum against the oracle's energies of the rounded one."""
+    dev = torch.device("cuda:0")
+    cases = [(synth.CONFIGS[3].layers[0], 0.25, synth.layer_inputs(3, 0)),
+             (synth.CONFIGS[5].layers[0], 0.5, synth.layer_inputs(5, 0)),
+             (synth.CONFIGS[2].layers[1], 0.0, synth.layer_inputs(2, 1)),
+             (synth.CONFIGS[2].layers[2], 0.5, synth.layer_inputs(2, 2))]
+    small = [synth.Layer("bf_blue512_1d", 1, 24, 3, 5, 200, 1, 8, (3, 4), "walk"),
+             synth.Layer("bf_direct_2d", 2, 6, 5, 7, 9, 9, 3, (1, 1, 1, 1), "blur")]
+    for i, layer in enumerate(small):
+        for c in (0.0, 0.5):
+            cases.append((layer, c, synth.random_inputs(layer, 2300 + i)))
+    for layer, c, (x, w, dy) in cases:
+        say(f"[bf16 spectra] {layer.name} c={c}")
+        _, _, _, plan, ws = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_BF16_SPECTRA)
+        if layer.ndim == 2:
+            Lh, Lw = plan.fft
+            X = bo.kept_spectrum_2d(x, (layer.pad[0], layer.pad[2]), Lh, Lw, c)
+            DY = bo.kept_spectrum_2d(dy, (0, 0), Lh, Lw, c)
+            Wf = bo.kept_filter_spectrum_2d(w, Lh, Lw, c)
+        else:
+            Lw = plan.fft[0]
+            X = bo.kept_spectrum_1d(x, layer.pad[0], Lw, c)
+            DY = bo.kept_spectrum_1d(dy, 0, Lw, c)
+            Wf = bo.kept_filter_spectrum_1d(w, Lw, c)
+        fr = [_check_bf16_words(plan.spectrum(ws, k).cpu().numpy(), ref) for k, ref in (("X", X), ("W", Wf), ("DY", DY))]
+        say(f"    parts one ulp off: X {fr[0]:.1e} W {fr[1]:.1e} DY {fr[2]:.1e}")
+        assert max(fr) <= 5e-2, fr  # systematic mis-rounding (truncation) would put about half off
+        # energies of the stored (rounded) input spectrum, reusing it
+        e = plan.input_energy(None, ws, flags=blconv.BL_REUSE_X).cpu().numpy()
+        Xr = bo.round_bf16(X.real) + 1j * bo.round_bf16(X.imag)
+        _, v = plan.bins()
+        h = np.where((v == 0) | ((Lw % 2 == 0) & (v == Lw // 2)), 1.0, 2.0)
+        want = h * np.sum(np.abs(Xr.reshape(plan.kept, -1)) ** 2, axis=1)
+        err = rel(e, want)
+        say(f"    energy rel err {err:.2e}")
+        assert err <= 1e-4, err
 
 
 def test_graph_replays_match_eager(torch):

@@ -130,15 +130,27 @@ def test_plan_create_validation(kw, code):
     assert _create(**kw) == code
 
 
-def test_bf16_flag_leaves_the_band_and_workspace_unchanged():
-    """The reduced-precision contraction changes only the arithmetic of the
-    channel sums: the band, the grid and the workspace are those of the fp32 plan."""
+def test_bf16_flag_keeps_the_band_and_halves_the_stored_spectra():
+    """Reduced precision changes the stored spectra and the arithmetic of the
+    channel sums only: the band and the grid are those of the fp32 plan, and
+    X, W and DY take 4 bytes per complex value instead of 8."""
+    def up(v):
+        return (v + 255) // 256 * 256
+
     for args in [(2, 3, 16, 24, (20, 20), 3, (1, 1, 1, 1), 0.5), (1, 5, 3, 7, (90,), 5, (2, 2), 0.3)]:
         a = blconv.Plan(*args)
-        b = blconv.Plan(*args, desc_flags=blconv.BL_DESC_BF16_CONTRACTION)
+        b = blconv.Plan(*args, desc_flags=blconv.BL_DESC_BF16_SPECTRA)
         assert (a.fft, a.r_h, a.r_w, a.kept, a.total, a.c_eff) == (b.fft, b.r_h, b.r_w, b.kept, b.total, b.c_eff)
-        assert a.workspace_bytes == b.workspace_bytes and a.offsets == b.offsets
         assert np.array_equal(a.mask(), b.mask())
+        _, N, Ci, Co = args[:4]
+        for plan, eb in ((a, 8), (b, 4)):
+            o = plan.offsets
+            assert o["X"] == 0
+            assert o["W"] == up(plan.kept * N * Ci * eb)
+            assert o["DY"] == o["W"] + up(plan.kept * Ci * Co * eb)
+        saved = (up(a.kept * N * Ci * 8) - up(a.kept * N * Ci * 4) + up(a.kept * Ci * Co * 8)
+                 - up(a.kept * Ci * Co * 4) + up(a.kept * N * Co * 8) - up(a.kept * N * Co * 4))
+        assert a.workspace_bytes - b.workspace_bytes == saved
 
 
 def test_null_arguments_are_rejected_without_gpu():
