@@ -445,3 +445,96 @@ def round_bf16(a) -> np.ndarray:
     u = f.view(np.uint32).astype(np.uint64)
     u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
     return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Fine-grained "top" compression (supplementary section "Error Incurred by 2D
+# Convolution with Compression"): the k coefficients of smallest magnitude in a
+# spectrum are zeroed; the tensors keep their size.
+#
+# Readings (the paper works with one image and one filter):
+# * T1 "the whole tensor" is, for the input, one sample's spectrum over its
+#   channels and the plan's kept half-plane bins, and for the filter one output
+#   filter's spectrum over its input channels and the kept bins; each is ranked
+#   on its own.
+# * T2 among coefficients of equal magnitude the one earlier in (bin, channel)
+#   order, bins in the stored bin-major order, goes first (any order is a valid
+#   reading; this one is deterministic).
+# * T3 a zeroed coefficient loses its real and imaginary parts; column 0 (and
+#   an even width's Nyquist column) keep the inverse transform's real-part
+#   convention, so zeroing one of a conjugate pair halves that frequency.
+# ----------------------------------------------------------------------------
+
+
+def zero_smallest(S: np.ndarray, k: int) -> np.ndarray:
+    """Rows of S (complex, [segments, m]) with the k entries of smallest |S|
+    set to zero (all of them when k >= m); equal magnitudes in row order."""
+    if k < 0:
+        raise ValueError("k must be non-negative")
+    S = np.array(S, dtype=np.complex128, copy=True)
+    if k == 0:
+        return S
+    order = np.argsort(np.abs(S), axis=1, kind="stable")[:, :k]
+    np.put_along_axis(S, order, 0.0, axis=1)
+    return S
+
+
+def _kept_index(M: np.ndarray):
+    """Index arrays of the kept bins of a 2-D (or 1-D) mask in stored order."""
+    if M.ndim == 1:
+        return (np.nonzero(M)[0],)
+    bins = kept_bins_2d(M)
+    return (np.array([u for u, _ in bins], dtype=np.int64), np.array([v for _, v in bins], dtype=np.int64))
+
+
+def _zero_smallest_per_plane_group(A: np.ndarray, idx, k: int) -> np.ndarray:
+    """A: [G, C, *grid] masked spectra; rank the kept coefficients of each
+    group g over (bin, channel) in that order, zero the k smallest."""
+    A = A.copy()
+    Ak = A[(slice(None), slice(None)) + idx]  # [G, C, B]
+    G, C, B = Ak.shape
+    seg = np.swapaxes(Ak, 1, 2).reshape(G, B * C)  # index b * C + c
+    z = zero_smallest(seg, k).reshape(G, B, C)
+    A[(slice(None), slice(None)) + idx] = np.swapaxes(z, 1, 2)
+    return A
+
+
+def forward_top(x, w, pad, c, k_x, k_w, fft=None):
+    """Forward pass (Eq. 1) with the k_x smallest-magnitude coefficients of
+    each sample's input spectrum and the k_w smallest of each filter's
+    spectrum zeroed (readings T1-T3), on the band of rate c."""
+    if x.ndim == 4:
+        X, Wf, M, g = spectra_2d(x, w, pad, c, fft)
+        idx = _kept_index(M)
+        X = _zero_smallest_per_plane_group(X, idx, k_x)
+        Wf = _zero_smallest_per_plane_group(Wf, idx, k_w)
+        Y = _channel_contract(X, Wf, conj_b=True)
+        return _irfft2(Y, g["Lh"], g["Lw"])[..., : g["Ho"], : g["Wo"]]
+    N, C, Lx = x.shape
+    K = w.shape[-1]
+    g = geometry_1d(Lx, K, pad, fft)
+    M = mask_1d(g["L"], c)[0]
+    X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
+    Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
+    idx = _kept_index(M)
+    X = _zero_smallest_per_plane_group(X, idx, k_x)
+    Wf = _zero_smallest_per_plane_group(Wf, idx, k_w)
+    Y = _channel_contract(X[..., None, :], Wf[..., None, :], conj_b=True)[..., 0, :]
+    return np.fft.irfft(Y, n=g["L"])[..., : g["Lo"]]
+
+
+def top_zeroed(S_kept: np.ndarray, k: int, per_last: bool) -> np.ndarray:
+    """Boolean mask of the entries zero_smallest ranks among the k smallest,
+    for a stored kept spectrum laid out bin-major as the library stores it:
+    [B][G][C] for inputs (per_last False: group G = sample, ranked over
+    (b, c)) or [B][C][G] for filters (per_last True: group = output filter)."""
+    S = np.asarray(S_kept)
+    if per_last:
+        S = np.swapaxes(S, 1, 2)  # [B][G][C]
+    B, G, C = S.shape
+    seg = np.swapaxes(S, 0, 1).reshape(G, B * C)
+    z = np.zeros(seg.shape, dtype=bool)
+    if k > 0:
+        np.put_along_axis(z, np.argsort(np.abs(seg), axis=1, kind="stable")[:, :k], True, axis=1)
+    z = np.swapaxes(z.reshape(G, B, C), 0, 1)
+    return np.swapaxes(z, 1, 2) if per_last else z

@@ -494,3 +494,128 @@ def test_rounded_operands_both_sides():
     for x, w in ((imp, wr), (xr, wimp)):
         exact = bo.forward(x, w, (0, 0, 0, 0), 0.0)
         assert rel(bo.forward(x, w, (0, 0, 0, 0), 0.0, None, bo.round_bf16), exact) > 1e-6
+
+
+# --------------------------------------- fine-grained "top" compression --
+
+
+def _rank_by_counting(row):
+    """Rank of each entry: entries of smaller magnitude, plus equal ones
+    earlier in the row (a double loop, independent of any sort)."""
+    m = len(row)
+    a = np.abs(row)
+    return np.array([sum(1 for j in range(m) if a[j] < a[i] or (a[j] == a[i] and j < i)) for i in range(m)])
+
+
+def test_zero_smallest_matches_rank_counting():
+    """The k zeroed entries of each row are those of rank < k, with ranks
+    counted pairwise; ties (crafted equal magnitudes, including conjugates
+    and opposite signs) go to the earlier entry."""
+    rng = np.random.default_rng(61)
+    rows = [rng.standard_normal(7) + 1j * rng.standard_normal(7) for _ in range(5)]
+    rows.append(np.array([1 + 1j, 2, 1 - 1j, -2, 0.5j, -1 - 1j, 2j]))
+    S = np.stack(rows)
+    for k in range(0, 9):
+        Z = bo.zero_smallest(S, k)
+        for i, row in enumerate(S):
+            zeroed = _rank_by_counting(row) < k
+            assert np.array_equal(Z[i] == 0, zeroed), (k, i)
+            assert np.array_equal(Z[i][~zeroed], row[~zeroed])
+    with pytest.raises(ValueError):
+        bo.zero_smallest(S, -1)
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_top_with_nothing_zeroed_is_the_band_limited_forward(ndim):
+    for layer in _rand_layers(ndim, 3, 62 + ndim):
+        x, w, _ = synth.random_inputs(layer, 3)
+        for c in (0.0, 0.4):
+            assert rel(bo.forward_top(x, w, layer.pad, c, 0, 0), bo.forward(x, w, layer.pad, c)) < 1e-13
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_top_zeroing_everything_gives_zero(ndim):
+    layer = _rand_layers(ndim, 1, 64 + ndim)[0]
+    x, w, _ = synth.random_inputs(layer, 4)
+    big = 10 ** 9
+    assert np.abs(bo.forward_top(x, w, layer.pad, 0.3, big, 0)).max() == 0.0
+    assert np.abs(bo.forward_top(x, w, layer.pad, 0.0, 0, big)).max() == 0.0
+
+
+def test_top_keeps_a_single_frequency_and_halves_a_conjugate_pair():
+    """A phase-shifted cosine at row frequency 3 on an 8 x 8 grid (no padding,
+    1 x 1 filters) has two nonzero half-plane coefficients, a conjugate pair in
+    column 0.  Keeping the two largest leaves the layer exact (y = a x);
+    keeping one leaves half the amplitude (reading T3: the real part of one
+    side of the pair); keeping none gives 0.  Zeroing only real parts would
+    leave a different phase."""
+    H = W = 8
+    h = np.arange(H)[:, None] * np.ones((1, W))
+    x = np.cos(2 * np.pi * 3 * h / H + 0.7)[None, None]
+    w = np.full((1, 1, 1, 1), 1.5)
+    total = H * (W // 2 + 1)
+    pad = (0, 0, 0, 0)
+    assert np.abs(bo.forward_top(x, w, pad, 0.0, total - 2, 0) - 1.5 * x).max() < 1e-12
+    assert np.abs(bo.forward_top(x, w, pad, 0.0, total - 1, 0) - 0.75 * x).max() < 1e-12
+    assert np.abs(bo.forward_top(x, w, pad, 0.0, total, 0)).max() == 0.0
+
+
+def test_top_1d_keeps_the_largest_coefficient():
+    """1-D: DC plus a cosine at bin 3 (magnitudes L and L/2): keeping one
+    coefficient keeps the DC term, keeping two keeps the signal."""
+    L = 10
+    n = np.arange(L)
+    x = (1.0 + np.cos(2 * np.pi * 3 * n / L + 0.4))[None, None]
+    w = np.full((1, 1, 1), 2.0)
+    total = L // 2 + 1
+    assert np.abs(bo.forward_top(x, w, (0, 0), 0.0, total - 2, 0) - 2 * x).max() < 1e-12
+    assert np.abs(bo.forward_top(x, w, (0, 0), 0.0, total - 1, 0) - 2.0).max() < 1e-12
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_top_ranks_each_sample_and_each_filter_on_its_own(ndim):
+    """Ranking is scale-invariant within a group, so scaling one sample (or one
+    filter) scales only its own outputs (reading T1); a ranking over the whole
+    batch or over all filters would change the others."""
+    layer = _rand_layers(ndim, 1, 66 + ndim)[0]
+    x, w, _ = (a.astype(np.float64) for a in synth.random_inputs(layer, 5))  # scaled in fp64
+    x = np.concatenate([x, x[:1]], axis=0)
+    w = np.concatenate([w, w[:1]], axis=0)
+    B = bo.forward_top(x, w, layer.pad, 0.2, 7, 5)
+    xs, ws = x.copy(), w.copy()
+    xs[-1] *= 1e-3
+    ws[-1] *= 1e3
+    S = bo.forward_top(xs, ws, layer.pad, 0.2, 7, 5)
+    assert rel(S[:-1, :-1], B[:-1, :-1]) < 1e-12
+    assert rel(S[-1, :-1], 1e-3 * B[-1, :-1]) < 1e-12
+    assert rel(S[:-1, -1], 1e3 * B[:-1, -1]) < 1e-12
+    # the last sample duplicates the first: same result
+    assert rel(B[-1], B[0]) < 1e-12
+
+
+def test_top_zeroed_mask_layouts():
+    """top_zeroed on stored layouts ([B][N][C] inputs, [B][C][F] filters)
+    marks per group exactly the entries zero_smallest zeroes."""
+    rng = np.random.default_rng(67)
+    X = rng.standard_normal((5, 3, 4)) + 1j * rng.standard_normal((5, 3, 4))
+    z = bo.top_zeroed(X, 6, per_last=False)
+    assert z.shape == X.shape and np.all(z.sum(axis=(0, 2)) == 6)
+    for n in range(3):
+        seg = X[:, n, :].reshape(-1)
+        assert np.array_equal(z[:, n, :].reshape(-1), bo.zero_smallest(seg[None], 6)[0] == 0)
+    Wk = rng.standard_normal((5, 4, 2)) + 1j * rng.standard_normal((5, 4, 2))
+    zw = bo.top_zeroed(Wk, 3, per_last=True)
+    for f in range(2):
+        seg = Wk[:, :, f].reshape(-1)
+        assert np.array_equal(zw[:, :, f].reshape(-1), bo.zero_smallest(seg[None], 3)[0] == 0)
+
+
+def test_top_tie_order_is_bin_then_channel():
+    """Reading T2 on a crafted spectrum with an exact tie between (bin 0,
+    channel 1) and (bin 1, channel 0): the earlier in (bin, channel) order is
+    zeroed first."""
+    A = np.full((1, 2, 3), 5.0 + 0j)
+    A[0, 1, 0] = 1.0
+    A[0, 0, 1] = -1.0
+    Z = bo._zero_smallest_per_plane_group(A, (np.arange(3),), 1)
+    assert Z[0, 1, 0] == 0 and Z[0, 0, 1] == -1.0
