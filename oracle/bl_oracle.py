@@ -538,3 +538,30 @@ def top_zeroed(S_kept: np.ndarray, k: int, per_last: bool) -> np.ndarray:
         np.put_along_axis(z, np.argsort(np.abs(seg), axis=1, kind="stable")[:, :k], True, axis=1)
     z = np.swapaxes(z.reshape(G, B, C), 0, 1)
     return np.swapaxes(z, 1, 2) if per_last else z
+
+
+def forward_zeroed(x, w, pad, c, zero_x, zero_w, fft=None):
+    """Forward pass (Eq. 1) with chosen kept coefficients zeroed: zero_x is a
+    boolean [B][N][C_in] over the stored input spectrum, zero_w [B][C_in][C_out]
+    over the stored filter spectrum (bins in stored order).  With the masks of
+    top_zeroed it is forward_top; with none set, the band-limited forward."""
+    if x.ndim == 4:
+        X, Wf, M, g = spectra_2d(x, w, pad, c, fft)
+    else:
+        g = geometry_1d(x.shape[-1], w.shape[-1], pad, fft)
+        M = mask_1d(g["L"], c)[0]
+        X = np.fft.rfft(_embed1(np.asarray(x, np.float64), g["L"], pad[0])) * M
+        Wf = np.fft.rfft(_embed1(np.asarray(w, np.float64), g["L"], 0)) * M
+    idx = _kept_index(M)
+    sel = (slice(None), slice(None)) + idx
+    Xk = X[sel]  # [N, C, B]
+    Xk[np.transpose(np.asarray(zero_x, bool), (1, 2, 0))] = 0.0
+    X[sel] = Xk
+    Wk = Wf[sel]  # [F, C, B]
+    Wk[np.transpose(np.asarray(zero_w, bool), (2, 1, 0))] = 0.0
+    Wf[sel] = Wk
+    if x.ndim == 4:
+        Y = _channel_contract(X, Wf, conj_b=True)
+        return _irfft2(Y, g["Lh"], g["Lw"])[..., : g["Ho"], : g["Wo"]]
+    Y = _channel_contract(X[..., None, :], Wf[..., None, :], conj_b=True)[..., 0, :]
+    return np.fft.irfft(Y, n=g["L"])[..., : g["Lo"]]

@@ -619,3 +619,31 @@ def test_top_tie_order_is_bin_then_channel():
     A[0, 0, 1] = -1.0
     Z = bo._zero_smallest_per_plane_group(A, (np.arange(3),), 1)
     assert Z[0, 1, 0] == 0 and Z[0, 0, 1] == -1.0
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_forward_zeroed_agrees_with_top_and_forward(ndim):
+    """forward_zeroed with the masks top_zeroed picks on the stored layouts is
+    forward_top; with no mask set it is the band-limited forward; zeroing one
+    sample's whole spectrum zeroes that sample's output only."""
+    for layer in _rand_layers(ndim, 2, 68 + ndim):
+        x, w, _ = (a.astype(np.float64) for a in synth.random_inputs(layer, 6))
+        c = 0.25
+        if ndim == 2:
+            Lh, Lw = layer.H + layer.pad[0] + layer.pad[1], layer.W + layer.pad[2] + layer.pad[3]
+            Xk = bo.kept_spectrum_2d(x, (layer.pad[0], layer.pad[2]), Lh, Lw, c)
+            Wk = bo.kept_filter_spectrum_2d(w, Lh, Lw, c)
+        else:
+            L = layer.H + layer.pad[0] + layer.pad[1]
+            Xk = bo.kept_spectrum_1d(x, layer.pad[0], L, c)
+            Wk = bo.kept_filter_spectrum_1d(w, L, c)
+        Xk = Xk.reshape(Xk.shape[0], layer.N, layer.C_in)
+        zx, zw = bo.top_zeroed(Xk, 9, per_last=False), bo.top_zeroed(Wk, 4, per_last=True)
+        want = bo.forward_top(x, w, layer.pad, c, 9, 4)
+        assert rel(bo.forward_zeroed(x, w, layer.pad, c, zx, zw), want) < 1e-13
+        none_x, none_w = np.zeros(Xk.shape, bool), np.zeros(Wk.shape, bool)
+        assert rel(bo.forward_zeroed(x, w, layer.pad, c, none_x, none_w), bo.forward(x, w, layer.pad, c)) < 1e-13
+        one = none_x.copy()
+        one[:, 0, :] = True
+        y = bo.forward_zeroed(x, w, layer.pad, c, one, none_w)
+        assert np.abs(y[0]).max() == 0.0 and rel(y[1:], bo.forward(x, w, layer.pad, c)[1:]) < 1e-13
