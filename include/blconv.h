@@ -199,6 +199,33 @@ bl_status_t bl_conv_input_energy(bl_conv_plan_t plan, const float* x, void* ws, 
 bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t plan, const double* energy, size_t n, double fraction,
                                     int* t, double* c, double* preserved);
 
+/* Fine-grained "top" compression (supplementary section "Error Incurred by 2D
+ * Convolution with Compression"): the k coefficients of smallest magnitude of
+ * a spectrum are set to zero, the tensors keeping their size.
+ *
+ * bl_conv_zero_smallest zeroes, in the stored spectrum `which` of ws, the k
+ * coefficients of smallest |z| of every group: for BL_SPEC_X each sample's
+ * input spectrum, for BL_SPEC_W each output filter's spectrum, each over its
+ * C_in channels at every kept bin of the plan.  Coefficient i of a group is
+ * (bin i / C_in in bl_conv_plan_get_bins order, channel i % C_in); among equal
+ * magnitudes (|z|^2 in fp32) the lower i is zeroed first, so exactly
+ * min(k, kept C_in) coefficients per group are zeroed and the result does not
+ * depend on scheduling.  The spectrum is first computed from `src` (x
+ * [N][C_in][H][W] for BL_SPEC_X, w [C_out][C_in][K][K] for BL_SPEC_W) unless
+ * flags holds the reuse flag of that spectrum (BL_REUSE_X or BL_REUSE_W; src
+ * may then be NULL).  A following bl_conv_forward with BL_REUSE_X | BL_REUSE_W
+ * computes the layer on the zeroed spectra (the backward passes likewise with
+ * their reuse flags).  k = 0 only computes the spectrum.  BL_SPEC_W also uses
+ * workspace outside X, W and DY as scratch (a group-major copy of W).  Errors:
+ * NULL plan or
+ * ws, k < 0, another `which`, other flags, src NULL without the reuse flag:
+ * BL_ERR_INVALID_ARG; a group of 2^31 or more coefficients:
+ * BL_ERR_UNSUPPORTED.  One kernel (plus the transform) on `stream`. */
+#define BL_SPEC_X 0u
+#define BL_SPEC_W 1u
+bl_status_t bl_conv_zero_smallest(bl_conv_plan_t plan, const float* src, void* ws, unsigned which, long long k,
+                                  unsigned flags, void* stream);
+
 const char* bl_status_string(bl_status_t status);
 
 /* Per-kernel timing, for measurement tools.  While enabled, every kernel the

@@ -21,6 +21,9 @@ BL_REUSE_DY = 0x4
 
 BL_DESC_BF16_SPECTRA = 0x1
 
+BL_SPEC_X = 0
+BL_SPEC_W = 1
+
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "workspace too small",
           4: "HIP error", 5: "out of host memory"}
 
@@ -29,7 +32,7 @@ EXPORTED = (
     "bl_conv_plan_get_bins", "bl_conv_workspace_size", "bl_conv_workspace_layout", "bl_conv_forward",
     "bl_conv_backward_input", "bl_conv_backward_weight", "bl_status_string", "bl_profile_begin",
     "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release", "bl_conv_input_energy",
-    "bl_conv_rate_for_energy",
+    "bl_conv_rate_for_energy", "bl_conv_zero_smallest",
 )
 
 
@@ -76,6 +79,7 @@ def load():
         getattr(lib, name).argtypes = [P, P, P, P, P, U, P]
     lib.bl_conv_input_energy.argtypes = [P, P, P, U, P, P]
     lib.bl_conv_rate_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D)]
+    lib.bl_conv_zero_smallest.argtypes = [P, P, P, U, ctypes.c_longlong, U, P]
     lib.bl_status_string.argtypes = [I]
     lib.bl_status_string.restype = ctypes.c_char_p
     lib.bl_profile_begin.argtypes = [I]
@@ -243,6 +247,15 @@ class Plan:
         _check("bl_conv_rate_for_energy", self._lib.bl_conv_rate_for_energy(
             self._h, e.ctypes.data, e.size, float(fraction), ctypes.byref(t), ctypes.byref(c), ctypes.byref(f)))
         return t.value, c.value, f.value
+
+    def zero_smallest(self, src, ws, which, k, flags=0, stream=None):
+        """Zero the k smallest-magnitude coefficients of each sample's ("X") or
+        each filter's ("W") stored spectrum (see bl_conv_zero_smallest); `src`
+        is x or w, or None with the matching reuse flag."""
+        code = {"X": BL_SPEC_X, "W": BL_SPEC_W}[which]
+        shape, name = (self.x_shape(), "x") if which == "X" else (self.w_shape(), "w")
+        _check("bl_conv_zero_smallest", self._lib.bl_conv_zero_smallest(
+            self._h, self._ptr(src, shape, name), self._ws(ws), code, int(k), flags, self._stream(stream)))
 
     def spectrum(self, ws, which):
         """View of a stored spectrum in the workspace, [kept][rows][cols]: complex64,

@@ -394,6 +394,109 @@ def test_bf16_stored_spectra_and_energy(torch):
         assert err <= 1e-4, err
 
 
+def _stored_complex(plan, ws, which):
+    """A stored spectrum as complex128 [kept][rows][cols], decoding bfloat16 pairs."""
+    a = plan.spectrum(ws, which).cpu().numpy()
+    if a.dtype == np.int32:
+        re, im = _decode_bf16_pairs(a)
+        return re.astype(np.float64) + 1j * im.astype(np.float64)
+    return a.astype(np.complex128)
+
+
+def _groups(S, which):
+    """[groups][B * C] views (coefficient i = (bin i / C, channel i % C)) of a
+    stored X [B][N][C] (groups = samples) or W [B][C][F] (groups = filters)."""
+    if which == "X":
+        return np.transpose(S, (1, 0, 2)).reshape(S.shape[1], -1)
+    return np.transpose(S, (2, 0, 1)).reshape(S.shape[2], -1)
+
+
+def _check_zeroed(before, after, ref, k, which, tie_tol):
+    """Exactly the k smallest of each group zeroed (counted with the zeros it
+    already had), the rest untouched bit for bit, the choice valid in the
+    GPU's own values, and equal to the oracle's ranking except among
+    coefficients within tie_tol of the oracle's k-th magnitude.  Returns the
+    zero mask in the stored layout."""
+    gb, ga, gr = _groups(before, which), _groups(after, which), _groups(ref, which)
+    n = gb.shape[1]
+    kk = min(k, n)
+    za = ga == 0
+    assert np.array_equal(ga[~za], gb[~za]), "a coefficient that was kept changed"
+    counts = za.sum(axis=1)
+    assert np.all(counts == np.maximum(kk, (gb == 0).sum(axis=1))), (counts[:4], kk)
+    if 0 < kk < n:
+        mb = np.abs(gb)
+        hi = np.where(za, mb, -np.inf).max(axis=1)
+        lo = np.where(~za, mb, np.inf).min(axis=1)
+        assert np.all(hi <= lo * (1 + 1e-6)), "a zeroed coefficient is larger than a kept one"
+        mr = np.abs(gr)
+        thr = np.sort(mr, axis=1)[:, kk - 1:kk]
+        zo = np.zeros_like(za)
+        np.put_along_axis(zo, np.argsort(mr, axis=1, kind="stable")[:, :kk], True, axis=1)
+        diff = za != zo
+        rms = np.sqrt(np.mean(mr ** 2))
+        assert np.all(np.abs(mr - thr)[diff] <= tie_tol * thr.repeat(n, axis=1)[diff] + 1e-6 * rms), \
+            "the GPU's choice differs from the oracle's away from a tie"
+    # back to the stored layout
+    if which == "X":
+        return np.transpose(za.reshape(before.shape[1], before.shape[0], before.shape[2]), (1, 0, 2))
+    return np.transpose(za.reshape(before.shape[2], before.shape[0], before.shape[1]), (1, 2, 0))
+
+
+def test_zero_smallest_parity(torch):
+    """Fine-grained top compression on the GPU: per sample and per filter the
+    k smallest-magnitude stored coefficients are zeroed (k = 1, a third, all
+    but one, all, more than all), checked against the oracle's ranking and by
+    the forward pass on the zeroed spectra against the oracle's forward with the
+    same coefficients zeroed (and against forward_top where the choices agree);
+    a 2-D workload layer, the 1-D stack's widest layer, small odd shapes, and a
+    plan with bfloat16 spectra."""
+    dev = torch.device("cuda:0")
+    cases = [(synth.CONFIGS[3].layers[0], 0.5, 0, synth.layer_inputs(3, 0)),
+             (synth.CONFIGS[2].layers[1], 0.5, 0, synth.layer_inputs(2, 1))]
+    small = [synth.Layer("top_2d_odd", 2, 3, 5, 7, 9, 11, 3, (1, 1, 1, 1), "blur"),
+             synth.Layer("top_1d", 1, 4, 3, 6, 90, 1, 5, (2, 2), "walk")]
+    for i, layer in enumerate(small):
+        cases.append((layer, 0.0, 0, synth.random_inputs(layer, 2400 + i)))
+        cases.append((layer, 0.3, blconv.BL_DESC_BF16_SPECTRA, synth.random_inputs(layer, 2400 + i)))
+    for layer, c, fl, (x, w, dy) in cases:
+        plan = blconv.plan_for_layer(layer, c, None, fl)
+        n = plan.kept * layer.C_in
+        xt, wt = (torch.from_numpy(a).to(dev) for a in (x, w))
+        if layer.ndim == 2:
+            Lh, Lw = plan.fft
+            Xo = bo.kept_spectrum_2d(x, (layer.pad[0], layer.pad[2]), Lh, Lw, c)
+            Wo = bo.kept_filter_spectrum_2d(w, Lh, Lw, c)
+        else:
+            Xo = bo.kept_spectrum_1d(x, layer.pad[0], plan.fft[0], c)
+            Wo = bo.kept_filter_spectrum_1d(w, plan.fft[0], c)
+        Xo = Xo.reshape(plan.kept, layer.N, layer.C_in)
+        tie = 1e-2 if fl else 1e-5
+        for kx, kw in ((1, n // 3), (n // 3, 1), (n - 1, n), (n, n - 1), (n + 7, 0)):
+            say(f"[top] {layer.name} c={c} flags={fl} kx={kx} kw={kw} of {n}")
+            ws = plan.workspace(dev)
+            ws.fill_(0xFF)
+            y = torch.full(plan.y_shape(), float("nan"), device=dev)
+            plan.forward(xt, wt, y, ws)
+            Xb, Wb = _stored_complex(plan, ws, "X"), _stored_complex(plan, ws, "W")
+            plan.zero_smallest(None, ws, "X", kx, flags=blconv.BL_REUSE_X)
+            plan.zero_smallest(wt, ws, "W", kw)  # recomputes W first
+            Xa, Wa = _stored_complex(plan, ws, "X"), _stored_complex(plan, ws, "W")
+            zx = _check_zeroed(Xb, Xa, Xo, kx, "X", tie)
+            zw = _check_zeroed(Wb, Wa, Wo, kw, "W", tie)
+            plan.forward(None, None, y, ws, flags=blconv.BL_REUSE_X | blconv.BL_REUSE_W)
+            torch.cuda.synchronize()
+            got = y.cpu().numpy()
+            want = bo.forward_zeroed(x, w, layer.pad, c, zx, zw)
+            err = rel(got, want) if np.abs(want).max() > 0 else float(np.abs(got).max())
+            agree = np.array_equal(zx, bo.top_zeroed(Xo, kx, False)) and np.array_equal(zw, bo.top_zeroed(Wo, kw, True))
+            say(f"    forward rel err {err:.2e}; choice equal to the oracle's: {agree}")
+            assert np.isfinite(got).all()
+            assert err <= (BF16_EXACT_TOL if fl else TOL), err
+            if agree and not fl:
+                assert rel(got, bo.forward_top(x, w, layer.pad, c, kx, kw)) <= TOL
+
+
 def test_graph_replays_match_eager(torch):
     """A layer's three passes captured in a HIP graph and replayed several times,
     with other eager library work, a poisoned workspace and outputs, and

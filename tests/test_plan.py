@@ -170,6 +170,15 @@ def test_null_arguments_are_rejected_without_gpu():
     assert lib.bl_conv_forward(h, 8, 8, 8, 8, 0x4, None) == 1
     assert lib.bl_conv_backward_input(h, 8, 8, 8, 8, 0x1, None) == 1
     assert lib.bl_conv_backward_weight(h, 8, 8, 8, 8, 0x2, None) == 1
+    # fine-grained top compression: argument checks happen before any HIP call
+    ws8 = ctypes.c_void_p(8)
+    assert lib.bl_conv_zero_smallest(None, None, ws8, 0, 1, 0, None) == 1
+    assert lib.bl_conv_zero_smallest(h, None, None, 0, 1, 1, None) == 1
+    assert lib.bl_conv_zero_smallest(h, None, ws8, 0, -1, 1, None) == 1
+    assert lib.bl_conv_zero_smallest(h, None, ws8, 2, 1, 1, None) == 1
+    assert lib.bl_conv_zero_smallest(h, None, ws8, 0, 1, 0x2, None) == 1  # BL_REUSE_W with BL_SPEC_X
+    assert lib.bl_conv_zero_smallest(h, None, ws8, 1, 1, 0x1, None) == 1  # BL_REUSE_X with BL_SPEC_W
+    assert lib.bl_conv_zero_smallest(h, None, ws8, 0, 1, 0, None) == 1    # no source, no reuse
     # wrong sizes for host copies
     m = np.zeros(p.total + 1, np.uint8)
     assert lib.bl_conv_plan_get_mask(h, m.ctypes.data, m.size) == 1
