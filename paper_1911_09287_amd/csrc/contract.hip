@@ -157,6 +157,13 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
   // (even, odd) halves = (real-k rows 2k, 2k + 1); negation flips a sign bit
   auto form0 = [](unsigned w) { return CONJ ? w : w ^ 0x80000000u; };
   auto form1 = [](unsigned w) { return CONJ ? ((w >> 16) ^ 0x8000u) | (w << 16) : (w >> 16) | (w << 16); };
+  // Column swizzle of the bf16 stages: row k stores column c at c ^ swz(k).
+  // Threads that load along k store 8 columns x 8 even rows per wave, rows
+  // that the padded strides alone would put on a few banks; the XOR spreads
+  // them over all banks.  Rows 4q .. 4q + 3 share one value, and it only
+  // permutes bits 3-4 of the column, so the MFMA operand reads (32 or 16
+  // consecutive columns of rows 4q + {0, 1, 2, 3}) stay conflict-free.
+  auto swz = [](int k) { return 8 * ((k >> 2) & 3); };
   auto store16 = [&](int buf, int k0, const V* ra, const V* rb) {
     unsigned* a16 = As16[buf];
 #pragma unroll
@@ -164,12 +171,13 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
       int m, k;
       a_pos(q, m, k);
       const V r = ((m0 + m < g.M) && (k0 + k < kend)) ? ra[q] : zero4;
+      const int ms = m ^ swz(k);  // rows k and k + 1 share the swizzle (k even)
       if (A_KC) {
-        a16[k * SA16 + m] = r.x;
-        a16[(k + 1) * SA16 + m] = r.y;
+        a16[k * SA16 + ms] = r.x;
+        a16[(k + 1) * SA16 + ms] = r.y;
       } else {
-        a16[k * SA16 + m] = r.x;
-        a16[k * SA16 + m + 1] = r.y;
+        a16[k * SA16 + ms] = r.x;
+        a16[k * SA16 + ms + 1] = r.y;  // m even: (m + 1) ^ swz = ms + 1
       }
     }
     unsigned* b16 = Bs16[buf];
@@ -179,7 +187,7 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
       b_pos(q, k, n);
       const V r = ((n0 + n < g.N) && (k0 + k < kend)) ? rb[q] : zero4;
       // second value at (k, n + 1) when n runs along the vector, else (k + 1, n)
-      const int i0 = k * SB16 + n, i1 = B_NC ? i0 + 1 : i0 + SB16;
+      const int i0 = k * SB16 + (n ^ swz(k)), i1 = B_NC ? i0 + 1 : i0 + SB16;
       b16[i0] = form0(r.x);
       b16[PB16 + i0] = form1(r.x);
       b16[i1] = form0(r.y);
@@ -226,20 +234,23 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
     // v_mfma_f32_32x32x8_bf16: lane l supplies real k = 4 (l / 32) .. + 3 of its
     // row (A) or column (B), i.e. complex k = 2 (l / 32) and 2 (l / 32) + 1 of
     // the four complex k an instruction consumes
-    const unsigned* ap = As16[buf] + wm + jcol;
-    const unsigned* bp = Bs16[buf] + bcol * PB16 + wn + (jcol >> 1);
+    const unsigned* a16 = As16[buf];
+    const unsigned* b16 = Bs16[buf] + bcol * PB16;
 #pragma unroll
     for (int q = 0; q < kBK / 4; ++q) {
       const int kc = 4 * q + 2 * a_part;
+      const int s = swz(4 * q);  // rows kc and kc + 1 lie in 4q .. 4q + 3
       shortx4 av[MI], bv[NJ];
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
-        const unsigned lo = ap[kc * SA16 + 32 * i], hi = ap[(kc + 1) * SA16 + 32 * i];
+        const int m = wm + 32 * i + (jcol ^ s);  // wm + 32 i has no bits below 5
+        const unsigned lo = a16[kc * SA16 + m], hi = a16[(kc + 1) * SA16 + m];
         av[i] = shortx4{(short)(lo & 0xFFFF), (short)(lo >> 16), (short)(hi & 0xFFFF), (short)(hi >> 16)};
       }
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
-        const unsigned lo = bp[kc * SB16 + 16 * j], hi = bp[(kc + 1) * SB16 + 16 * j];
+        const int n = (wn + 16 * j + (jcol >> 1)) ^ s;
+        const unsigned lo = b16[kc * SB16 + n], hi = b16[(kc + 1) * SB16 + n];
         bv[j] = shortx4{(short)(lo & 0xFFFF), (short)(lo >> 16), (short)(hi & 0xFFFF), (short)(hi >> 16)};
       }
 #pragma unroll
