@@ -95,7 +95,7 @@ typedef struct {
   int pad_hi[2];     /* trailing zeros, same axes */
   double c;          /* compression rate, 0 <= c < 1 */
   int fft_h, fft_w;  /* 0 = padded size; else an FFT grid at least the padded size (1-D: fft_h) */
-  unsigned flags;    /* 0, or BL_DESC_BF16_SPECTRA */
+  unsigned flags;    /* 0, or BL_DESC_BF16_SPECTRA and/or BL_DESC_FUSED_FORWARD */
 } bl_conv_desc_t;
 
 /* Descriptor flag: reduced-precision spectra (the paper's reduced-precision
@@ -111,6 +111,21 @@ typedef struct {
  * arithmetic and the layer's inputs and outputs stay fp32.  Expected deviation
  * from the fp32 path: about 2e-3 relative (8 significant bits per operand). */
 #define BL_DESC_BF16_SPECTRA 0x1u
+
+/* Descriptor flag: fused small-map forward.  bl_conv_forward runs the filter
+ * transform (unless W is reused) and then one kernel that takes x to y: per
+ * sample and group of output channels it transforms the input planes, forms
+ * the per-bin channel sums and transforms them back in on-chip memory, so the
+ * input and output spectra do not pass through HBM as separate stages (X is
+ * still stored in ws for the reuse flags).  It applies to 2-D plans with
+ * complex64 spectra and at most 1024 kept bins whose per-channel working set
+ * fits in 64 KB of LDS, and to calls that do not reuse X; otherwise the flag
+ * has no effect.  The channel sums run on the vector ALUs and each block
+ * transforms its sample's planes again per output-channel group: measured on
+ * the 4x4, 8x8 and 16x16 workload layers it takes 1.6-11x the time of the
+ * unfused forward, whose contraction runs on the matrix cores, so it is not
+ * chosen unless requested. */
+#define BL_DESC_FUSED_FORWARD 0x2u
 
 typedef struct bl_conv_plan_s* bl_conv_plan_t;
 

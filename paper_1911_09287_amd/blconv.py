@@ -20,6 +20,7 @@ BL_REUSE_W = 0x2
 BL_REUSE_DY = 0x4
 
 BL_DESC_BF16_SPECTRA = 0x1
+BL_DESC_FUSED_FORWARD = 0x2
 
 BL_SPEC_X = 0
 BL_SPEC_W = 1
@@ -103,7 +104,8 @@ class Plan:
     2-D: ``Plan(2, N, C_in, C_out, (H, W), K, pad=(top, bottom, left, right), c=...)``.
     1-D: ``Plan(1, N, C_in, C_out, (L,), K, pad=(lo, hi), c=...)``.
     ``desc_flags``: 0, or BL_DESC_BF16_SPECTRA (spectra stored in bfloat16,
-    contracted with fp32 sums).
+    contracted with fp32 sums) and/or BL_DESC_FUSED_FORWARD (fused small-map
+    forward kernel where it applies).
     """
 
     def __init__(self, ndim, N, C_in, C_out, spatial, K, pad, c, fft=None, desc_flags=0):

@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libblconv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["plan.cpp", "api.hip", "tables.hip", "direct.hip", "bluestein.hip", "fft2d.hip", "contract.hip", "thin.hip", "energy.hip", "topk.hip"]
+SOURCES = ["plan.cpp", "api.hip", "tables.hip", "direct.hip", "bluestein.hip", "fft2d.hip", "contract.hip", "thin.hip", "energy.hip", "topk.hip", "small.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950",

@@ -99,6 +99,10 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   void* Wf = spec_at(ws, p->off_W);
   float2* T = ws_at(ws, p->off_T);
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  if (p->fused_fwd && !(flags & BL_REUSE_X) && small_fwd_eligible(p)) {
+    const bl_status_t st = launch_small_fwd(p, x, static_cast<const float2*>(Wf), y, static_cast<float2*>(X), s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
   if (!(flags & BL_REUSE_X))
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
   BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, ws_at(ws, p->off_CPart), s));

@@ -118,6 +118,12 @@ bl_status_t launch_bluestein_fwd(const bl_conv_plan_s* p, const float* in, void*
 bl_status_t launch_bluestein_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OW, int cj,
                                  hipStream_t s);
 
+// Fused small-map forward: x -> y in one kernel (W: the stored filter
+// spectrum; X: where the input spectrum is stored for map reuse).
+bool small_fwd_eligible(const bl_conv_plan_s* p);
+bl_status_t launch_small_fwd(const bl_conv_plan_s* p, const float* x, const float2* Wf, float* y, float2* X,
+                             hipStream_t s);
+
 // 2-D transforms on (2 MH) x (2 MW) grids with MH, MW odd (mixed radix 2 x odd).
 bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s);

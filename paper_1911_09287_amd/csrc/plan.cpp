@@ -30,7 +30,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   if (d->pad_lo[0] < 0 || d->pad_hi[0] < 0 || d->pad_lo[1] < 0 || d->pad_hi[1] < 0) return BL_ERR_INVALID_ARG;
   if (!(d->c >= 0.0 && d->c < 1.0)) return BL_ERR_INVALID_ARG;  // also rejects NaN
   if (d->fft_h < 0 || d->fft_w < 0) return BL_ERR_INVALID_ARG;
-  if (d->flags & ~BL_DESC_BF16_SPECTRA) return BL_ERR_INVALID_ARG;
+  if (d->flags & ~(BL_DESC_BF16_SPECTRA | BL_DESC_FUSED_FORWARD)) return BL_ERR_INVALID_ARG;
   if (d->ndim == 1 && (d->W != 1 || d->pad_lo[1] != 0 || d->pad_hi[1] != 0 || d->fft_w > 1))
     return BL_ERR_INVALID_ARG;
   if (d->ndim == 2 && d->W <= 0) return BL_ERR_INVALID_ARG;
@@ -41,6 +41,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   p->desc = *d;
   p->ndim = d->ndim;
   p->bf16 = (d->flags & BL_DESC_BF16_SPECTRA) != 0;
+  p->fused_fwd = (d->flags & BL_DESC_FUSED_FORWARD) != 0;
   p->N = d->N; p->Cin = d->C_in; p->Cout = d->C_out;
   if (d->ndim == 2) {
     p->Hi = d->H; p->Wi = d->W; p->Kh = d->K; p->Kw = d->K;

@@ -59,6 +59,7 @@ struct bl_conv_plan_s {
   bl_conv_desc_t desc;
   int ndim;
   bool bf16;           // stored spectra X, W, DY as bfloat16 pairs (BL_DESC_BF16_SPECTRA)
+  bool fused_fwd;      // forward through the fused small-map kernel where it applies
   int N, Cin, Cout;
   // row form
   int Hi, Wi;          // input plane

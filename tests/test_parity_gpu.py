@@ -497,6 +497,35 @@ def test_zero_smallest_parity(torch):
                 assert rel(got, bo.forward_top(x, w, layer.pad, c, kx, kw)) <= TOL
 
 
+def test_fused_small_forward(torch):
+    """BL_DESC_FUSED_FORWARD: the forward pass as one kernel after the filter
+    transform, on small maps (4x4 and 8x8 workload layers, odd and even grids,
+    1x1 maps, three input channels, output-channel groups that do not divide
+    C_out), against the oracle; the input spectrum it stores serves the
+    backward passes' reuse flags, and the fused kernel is the one that ran."""
+    cases = [(synth.CONFIGS[4].layers[2], c, synth.layer_inputs(4, 2)) for c in (0.0, 0.5)]
+    cases += [(synth.CONFIGS[3].layers[3], 0.25, synth.layer_inputs(3, 3)),
+              (synth.CONFIGS[3].layers[2], 0.75, synth.layer_inputs(3, 2))]
+    small = [synth.Layer("fz_odd", 2, 5, 3, 7, 7, 9, 3, (1, 1, 1, 1), "blur"),
+             synth.Layer("fz_1x1", 2, 3, 4, 5, 1, 1, 1, (0, 0, 0, 0), "blur"),
+             synth.Layer("fz_pad2", 2, 2, 6, 37, 6, 6, 5, (2, 2, 2, 2), "blur")]
+    for i, layer in enumerate(small):
+        for c in (0.0, 0.4):
+            cases.append((layer, c, synth.random_inputs(layer, 2500 + i)))
+    for layer, c, (x, w, dy) in cases:
+        say(f"[fused] {layer.name} c={c}")
+        prof = blconv.Profile(capacity=256)
+        with prof:
+            y, dx, dw, plan, ws = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_FUSED_FORWARD)
+        names = [r[0] for r in prof.records()]
+        ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        say(f"    rel err {errs}; kernels {sorted(set(names))}")
+        assert "small_fwd" in names and "contract_fwd" not in names
+        assert all(np.isfinite(a).all() for a in (y, dx, dw))
+        assert max(errs) <= TOL, errs
+
+
 def test_graph_replays_match_eager(torch):
     """A layer's three passes captured in a HIP graph and replayed several times,
     with other eager library work, a poisoned workspace and outputs, and

@@ -122,7 +122,7 @@ def _create(**kw):
     (dict(W=0), 1), (dict(K=0), 1), (dict(K=9), 2), (dict(K=9, H=20, W=20), 2),
     (dict(c=1.0), 1), (dict(c=-0.1), 1), (dict(c=float("nan")), 1), (dict(c=0.999), 0),
     (dict(pad_lo=(-1, 0)), 1), (dict(fft_h=9, fft_w=8), 0), (dict(fft_h=9, fft_w=7), 1), (dict(fft_h=7), 1), (dict(fft_h=12, fft_w=10), 0),
-    (dict(flags=1), 0), (dict(flags=2), 1), (dict(flags=3), 1), (dict(flags=0x80000000), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
+    (dict(flags=1), 0), (dict(flags=2), 0), (dict(flags=3), 0), (dict(flags=4), 1), (dict(flags=0x80000000), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
     (dict(ndim=1, W=1, H=10), 0), (dict(ndim=1, W=2, H=10), 1), (dict(ndim=1, W=1, H=10, pad_lo=(0, 1)), 1),
     (dict(ndim=1, W=1, H=10, fft_w=4), 1), (dict(ndim=1, W=1, H=10, fft_h=9), 1),
 ])
