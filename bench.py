@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--config", type=int, default=2, help="workload index (1..5)")
     ap.add_argument("--c", type=float, default=0.5, help="compression rate of the headline value")
     ap.add_argument("--no-sweep", action="store_true", help="skip the per-c sweep")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the bfloat16-spectra variant of the headline workload")
     ap.add_argument("--graph", action="store_true",
                     help="replay per-layer HIP graphs instead of launching every kernel from the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -257,8 +259,8 @@ def main():
     arrays = [synth.layer_inputs(args.config, i) for i in range(len(cfg.layers))]
     eq_flops = sum(3 * L.direct_flops() for L in cfg.layers)
 
-    def build(c):
-        return [Layer(torch, blconv, L, a, c, dev) for L, a in zip(cfg.layers, arrays)]
+    def build(c, desc_flags=0):
+        return [Layer(torch, blconv, L, a, c, dev, desc_flags) for L, a in zip(cfg.layers, arrays)]
 
     def graphs_for(Ls):
         if not args.graph:
@@ -287,6 +289,17 @@ def main():
                           "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12})
             del Ls
 
+    # the same workload with the saved spectra in bfloat16 (reduced precision
+    # combined with band-limiting); reported beside the fp32 headline, not as it
+    variants = {}
+    if not args.no_variants:
+        Ls = build(args.c, blconv.BL_DESC_BF16_SPECTRA)
+        m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs_for(Ls))
+        variants["bf16_spectra"] = {"dtype": "bf16 spectra, fp32 accumulation", "c": args.c, "ms_per_step": m,
+                                    "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12,
+                                    "speedup_vs_f32": ms / m}
+        del Ls
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, args.c, args.cpu_seconds)
@@ -312,6 +325,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": kernels,
         "per_c": per_c,
+        "variants": variants,
         "wall_s_timed": wall,
         "launch": "hip_graph per layer" if args.graph else "eager",
     }
