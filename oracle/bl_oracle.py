@@ -426,6 +426,47 @@ def energy_rate(x, pad, fraction, fft=None):
     return dict(t=t, kept=kept, total=total, c_eff=1.0 - kept / total, preserved=float(f[t]), fractions=f)
 
 
+# Fine-grained energy-based band (the same supplementary section, its
+# fine-grained variant): within the outermost layer that the energy target
+# needs, coefficients are added one at a time, and the layer's others are zeroed
+# in both the activation map's and the filter's spectrum.
+#
+# Readings:
+# * F1 the coarse band is E2's: the most layers t_c whose band keeps at least
+#   the fraction.  The fine-grained band starts from the band with one more
+#   layer peeled (t_c + 1, which keeps less) and adds back bins of layer t_c
+#   (the bins with last_layer_kept == t_c), largest energy first (equal
+#   energies in stored bin order), until it keeps at least the fraction.  With
+#   t_c the deepest band, or an input without energy, it is the coarse band.
+# * F2 it is computed with the coarse band's plan and the dropped bins' stored
+#   coefficients zeroed for every sample and channel, in the input spectrum and
+#   the filter spectrum; that also projects grad-input and grad-weight onto the
+#   fine band (a zero coefficient of W or X contributes nothing to them).
+def fine_energy_band(E, last, fraction):
+    """(t_c, keep): E and last over the same bins in stored order; keep is a
+    boolean over the bins of band t_c (those with last >= t_c), in that order,
+    False for the bins the fine-grained band drops."""
+    E = np.asarray(E, dtype=np.float64).ravel()
+    last = np.asarray(last).ravel()
+    f = preserved_fractions(E, last)
+    t = layers_for_energy(fraction, f)
+    band = last >= t
+    keep = np.ones(int(band.sum()), dtype=bool)
+    total = float(E.sum())
+    if t == len(f) - 1 or total == 0.0:
+        return t, keep
+    Eb, lb = E[band], last[band]
+    layer = np.nonzero(lb == t)[0]
+    keep[layer] = False
+    kept_e = float(Eb[lb > t].sum())
+    for i in layer[np.argsort(-Eb[layer], kind="stable")]:
+        if kept_e / total >= fraction:
+            break
+        keep[i] = True
+        kept_e += float(Eb[i])
+    return t, keep
+
+
 # ----------------------------------------------------------------------------
 # Reduced-precision contraction operands: the paper compares band-limiting
 # with reduced-precision arithmetic (Sec. 4.3) and combines the two in the

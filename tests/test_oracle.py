@@ -647,3 +647,126 @@ def test_forward_zeroed_agrees_with_top_and_forward(ndim):
         one[:, 0, :] = True
         y = bo.forward_zeroed(x, w, layer.pad, c, one, none_w)
         assert np.abs(y[0]).max() == 0.0 and rel(y[1:], bo.forward(x, w, layer.pad, c)[1:]) < 1e-13
+
+
+# --------------------------------------- fine-grained energy-based band --
+
+
+def _layer_of(last, t):
+    return np.nonzero(np.asarray(last).ravel()[np.asarray(last).ravel() >= t] == t)[0]
+
+
+def test_fine_band_is_the_smallest_set_reaching_the_fraction():
+    """On small grids with random energies: the band keeps at least the
+    fraction, contains the next deeper band and lies in the coarse band, and no
+    subset of the outermost layer with fewer added bins reaches the fraction
+    (checked over all subsets); among subsets of its size none keeps more."""
+    from itertools import combinations
+    rng = np.random.default_rng(71)
+    for ndim, L in ((1, 12), (2, (6, 6)), (2, (5, 7))):
+        last = bo.last_layer_kept(ndim, L).ravel()
+        for trial in range(8):
+            E = rng.exponential(1.0, last.size) * rng.choice([1.0, 0.0, 30.0], last.size, p=[0.7, 0.1, 0.2])
+            for fraction in (0.3, 0.6, 0.9, 0.97):
+                t, keep = bo.fine_energy_band(E, last, fraction)
+                band = last >= t
+                Eb, lb = E[band], last[band]
+                total = E.sum()
+                assert Eb[keep].sum() >= fraction * total * (1 - 1e-12)
+                assert np.all(keep[lb > t])  # the deeper band is kept whole
+                layer = np.nonzero(lb == t)[0]
+                added = int(keep[layer].sum())
+                if t == last.max():
+                    assert added == layer.size
+                    continue
+                base = Eb[lb > t].sum()
+                assert base < fraction * total  # the deeper band alone falls short
+                if layer.size <= 12:
+                    best = {k: max(sum(Eb[list(c)]) for c in combinations(layer, k)) if k else 0.0
+                            for k in range(layer.size + 1)}
+                    assert all(base + best[k] < fraction * total for k in range(added))
+                    assert Eb[layer[keep[layer]]].sum() >= best[added] * (1 - 1e-12)
+
+
+def test_fine_band_special_cases():
+    """No energy: the coarse band; a layer whose energy sits in one bin adds
+    that bin only; a fraction met by the deeper band plus nothing is impossible
+    by construction, so at least one bin is added when t_c is not the deepest."""
+    last = bo.last_layer_kept(2, (6, 6)).ravel()
+    t, keep = bo.fine_energy_band(np.zeros(last.size), last, 0.8)
+    assert keep.all() and t == last.max()
+    E = np.zeros(last.size)
+    E[last == last.max()] = 1.0  # the DC band's energy
+    i1 = np.nonzero(last == last.max() - 1)[0][2]
+    E[i1] = 0.5  # one bin of the next layer
+    t, keep = bo.fine_energy_band(E, last, 0.9)
+    band = last >= t
+    assert t == last.max() - 1
+    lb = last[band]
+    assert keep[lb == t].sum() == 1 and keep[np.nonzero(band)[0] == i1][0]
+
+
+def _full_plane_band(keep_half, L):
+    """Full-plane 0/1 band from a half-plane keep mask: a bin and its mirror
+    (-u, -v) together, except columns 0 and Nyquist, whose entries stand alone
+    (the inverse takes their real parts)."""
+    if isinstance(L, int):
+        band = np.zeros(L)
+        for v in range(L // 2 + 1):
+            if keep_half[v]:
+                band[v] = 1.0
+                if 0 < v and 2 * v != L:
+                    band[L - v] = 1.0
+        return band
+    Lh, Lw = L
+    band = np.zeros((Lh, Lw))
+    for u in range(Lh):
+        for v in range(Lw // 2 + 1):
+            if keep_half[u, v]:
+                band[u, v] = 1.0
+                if 0 < v and 2 * v != Lw:
+                    band[(Lh - u) % Lh, Lw - v] = 1.0
+    return band
+
+
+@pytest.mark.parametrize("ndim", [1, 2])
+def test_fine_band_forward_matches_direct_low_pass(ndim):
+    """The fine-grained forward (coarse plan, dropped bins zeroed in X and W)
+    equals the real part of the full correlation low-passed by the kept bins
+    (Eq. 2 with direct-sum DFTs over the full plane and explicit circular
+    sums), for fractions whose fine band drops part of a layer."""
+    for layer in _rand_layers(ndim, 3, 73 + ndim):
+        x, w, _ = (a.astype(np.float64) for a in synth.random_inputs(layer, 8))
+        if ndim == 2:
+            L = (layer.H + layer.pad[0] + layer.pad[1], layer.W + layer.pad[2] + layer.pad[3])
+            E, last = bo.bin_energy_2d(x, layer.pad), bo.last_layer_kept(2, L)
+        else:
+            L = layer.H + layer.pad[0] + layer.pad[1]
+            E, last = bo.bin_energy_1d(x, layer.pad), bo.last_layer_kept(1, L)
+        partial = 0
+        for fraction in (0.8, 0.95, 0.99):
+            t, keep = bo.fine_energy_band(E, last, fraction)
+            partial += int(not keep.all())
+            c = 1.0 - (int((last >= t).sum()) + 0.5) / last.size
+            drop = ~keep
+            zx = np.broadcast_to(drop[:, None, None], (keep.size, layer.N, layer.C_in))
+            zw = np.broadcast_to(drop[:, None, None], (keep.size, layer.C_in, layer.C_out))
+            y = bo.forward_zeroed(x, w, layer.pad, c, zx, zw)
+            kept_half = np.zeros(last.size, bool)
+            kept_half[np.nonzero(last.ravel() >= t)[0][keep]] = True
+            band = _full_plane_band(kept_half.reshape(last.shape), L)
+            if ndim == 2:
+                pt, pl = layer.pad[0], layer.pad[2]
+                xt = np.zeros((layer.N, layer.C_in) + L); xt[:, :, pt:pt + layer.H, pl:pl + layer.W] = x
+                wt = np.zeros((layer.C_out, layer.C_in) + L); wt[:, :, :layer.K, :layer.K] = w
+                z = br.circ_corr_2d(xt[:, None], wt[None]).sum(axis=2)
+                want = br.lowpass_2d(z, band)[0][:, :, :y.shape[-2], :y.shape[-1]]
+            else:
+                xt = np.zeros((layer.N, layer.C_in, L)); xt[:, :, layer.pad[0]:layer.pad[0] + layer.H] = x
+                wt = np.zeros((layer.C_out, layer.C_in, L)); wt[:, :, :layer.K] = w
+                z = br.circ_corr_1d(xt[:, None], wt[None]).sum(axis=2)
+                Z = (z @ br.dft_matrix(L).T) * band
+                want = ((Z @ br.dft_matrix(L, +1).T) / L).real[..., :y.shape[-1]]
+            assert rel(y, want) < 1e-10, (fraction, rel(y, want))
+        # a 1-D layer is a single bin, so only 2-D bands can be cut inside a layer
+        assert (partial > 0) if ndim == 2 else (partial == 0)
