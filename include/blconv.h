@@ -214,6 +214,37 @@ bl_status_t bl_conv_input_energy(bl_conv_plan_t plan, const float* x, void* ws, 
 bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t plan, const double* energy, size_t n, double fraction,
                                     int* t, double* c, double* preserved);
 
+/* Fine-grained energy-based band (the same supplementary section, its
+ * fine-grained variant): the coarse band of bl_conv_rate_for_energy (t layers
+ * peeled) is cut inside its outermost layer.  Starting from the band with one
+ * more layer peeled, that layer's bins are added back one at a time, largest
+ * energy first (equal energies in bin order), until the band keeps at least
+ * `fraction`; the layer's other bins are dropped.  (A 1-D layer is one bin, so
+ * there the fine band is the coarse one.)
+ *
+ * bl_conv_fine_band_for_energy takes the same inputs as
+ * bl_conv_rate_for_energy and returns the same t and c (the coarse band's; a
+ * plan created with rate c has exactly that band), `preserved` = the fraction
+ * the fine band keeps, and in keep[0 .. *keep_n) one byte per bin of the coarse
+ * band in that plan's bin order: 1 kept, 0 dropped.  keep may be NULL to query
+ * *keep_n; otherwise keep_cap must be at least *keep_n.  Host only; the same
+ * errors as bl_conv_rate_for_energy, and BL_ERR_INVALID_ARG when keep_cap is
+ * too small.
+ *
+ * bl_conv_zero_bins sets to zero, for every sample and channel, the stored
+ * spectrum `which` (BL_SPEC_X or BL_SPEC_W) of ws at the bins with keep[b] == 0;
+ * keep is a device array of `kept` bytes in the plan's bin order.  With X and W
+ * so zeroed, bl_conv_forward (BL_REUSE_X | BL_REUSE_W) computes the layer on the
+ * fine band, and grad-input (BL_REUSE_W) and grad-weight (BL_REUSE_X) project
+ * onto it as well, since a zero coefficient of W or X contributes nothing to
+ * them.  Errors: NULL arguments, another `which`: BL_ERR_INVALID_ARG; more than
+ * 65535 kept bins: BL_ERR_UNSUPPORTED.  One kernel on `stream`. */
+bl_status_t bl_conv_fine_band_for_energy(bl_conv_plan_t plan, const double* energy, size_t n, double fraction,
+                                         int* t, double* c, double* preserved, unsigned char* keep,
+                                         size_t keep_cap, size_t* keep_n);
+bl_status_t bl_conv_zero_bins(bl_conv_plan_t plan, void* ws, unsigned which, const unsigned char* keep,
+                              void* stream);
+
 /* Fine-grained "top" compression (supplementary section "Error Incurred by 2D
  * Convolution with Compression"): the k coefficients of smallest magnitude of
  * a spectrum are set to zero, the tensors keeping their size.

@@ -33,7 +33,7 @@ EXPORTED = (
     "bl_conv_plan_get_bins", "bl_conv_workspace_size", "bl_conv_workspace_layout", "bl_conv_forward",
     "bl_conv_backward_input", "bl_conv_backward_weight", "bl_status_string", "bl_profile_begin",
     "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release", "bl_conv_input_energy",
-    "bl_conv_rate_for_energy", "bl_conv_zero_smallest",
+    "bl_conv_rate_for_energy", "bl_conv_zero_smallest", "bl_conv_fine_band_for_energy", "bl_conv_zero_bins",
 )
 
 
@@ -81,6 +81,9 @@ def load():
     lib.bl_conv_input_energy.argtypes = [P, P, P, U, P, P]
     lib.bl_conv_rate_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D)]
     lib.bl_conv_zero_smallest.argtypes = [P, P, P, U, ctypes.c_longlong, U, P]
+    lib.bl_conv_fine_band_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D),
+                                                 P, S, ctypes.POINTER(S)]
+    lib.bl_conv_zero_bins.argtypes = [P, P, U, P, P]
     lib.bl_status_string.argtypes = [I]
     lib.bl_status_string.restype = ctypes.c_char_p
     lib.bl_profile_begin.argtypes = [I]
@@ -249,6 +252,30 @@ class Plan:
         _check("bl_conv_rate_for_energy", self._lib.bl_conv_rate_for_energy(
             self._h, e.ctypes.data, e.size, float(fraction), ctypes.byref(t), ctypes.byref(c), ctypes.byref(f)))
         return t.value, c.value, f.value
+
+    def fine_band_for_energy(self, energy, fraction):
+        """(t, c, preserved, keep) of the fine-grained band: keep is a uint8 array
+        over the bins of the coarse band (rate c), 1 kept, 0 dropped."""
+        e = np.ascontiguousarray(np.asarray(energy, dtype=np.float64))
+        t, c, f, n = ctypes.c_int(), ctypes.c_double(), ctypes.c_double(), ctypes.c_size_t()
+        _check("bl_conv_fine_band_for_energy", self._lib.bl_conv_fine_band_for_energy(
+            self._h, e.ctypes.data, e.size, float(fraction), ctypes.byref(t), ctypes.byref(c), ctypes.byref(f),
+            None, 0, ctypes.byref(n)))
+        keep = np.zeros(n.value, dtype=np.uint8)
+        _check("bl_conv_fine_band_for_energy", self._lib.bl_conv_fine_band_for_energy(
+            self._h, e.ctypes.data, e.size, float(fraction), ctypes.byref(t), ctypes.byref(c), ctypes.byref(f),
+            keep.ctypes.data, keep.size, ctypes.byref(n)))
+        return t.value, c.value, f.value, keep
+
+    def zero_bins(self, ws, which, keep, stream=None):
+        """Zero the stored spectrum ("X" or "W") at the bins where `keep` (a
+        uint8 GPU tensor of kept elements) is 0."""
+        import torch
+        if not (keep.is_cuda and keep.dtype == torch.uint8 and keep.is_contiguous() and keep.numel() == self.kept):
+            raise ValueError("keep must be a contiguous uint8 GPU tensor of kept elements")
+        code = {"X": BL_SPEC_X, "W": BL_SPEC_W}[which]
+        _check("bl_conv_zero_bins", self._lib.bl_conv_zero_bins(self._h, self._ws(ws), code, keep.data_ptr(),
+                                                                self._stream(stream)))
 
     def zero_smallest(self, src, ws, which, k, flags=0, stream=None):
         """Zero the k smallest-magnitude coefficients of each sample's ("X") or

@@ -89,6 +89,20 @@ extern "C" bl_status_t bl_conv_input_energy(bl_conv_plan_t p, const float* x, vo
   });
 }
 
+namespace {
+// The most layers that can be peeled with bin b of plan p still kept.
+int bin_last_layer(const bl_conv_plan_s* p, long b) {
+  const int r = (int)(b / p->V), v = (int)(b % p->V);
+  int tb = p->Lw / 2 - v;
+  if (p->ndim != 1) {
+    const int u = bl_kept_row(r, p->r_h, p->Lh, p->R);
+    const int su = u <= p->Lh / 2 ? u : u - p->Lh;
+    tb = std::min(p->Lh / 2 - std::abs(su), tb);
+  }
+  return tb;
+}
+}  // namespace
+
 extern "C" bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t p, const double* energy, size_t n, double fraction,
                                                int* t_out, double* c_out, double* preserved_out) {
   if (!p || !energy || n != (size_t)p->kept) return BL_ERR_INVALID_ARG;
@@ -102,13 +116,7 @@ extern "C" bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t p, const double* e
   for (long b = 0; b < p->kept; ++b) {
     const double eb = energy[b];
     if (!(eb >= 0.0) || std::isinf(eb)) return BL_ERR_INVALID_ARG;
-    const int r = (int)(b / p->V), v = (int)(b % p->V);
-    int tb = p->Lw / 2 - v;
-    if (!one_d) {
-      const int u = bl_kept_row(r, p->r_h, p->Lh, p->R);
-      const int su = u <= p->Lh / 2 ? u : u - p->Lh;
-      tb = std::min(p->Lh / 2 - std::abs(su), tb);
-    }
+    const int tb = bin_last_layer(p, b);
     if (tb < 0 || tb > t_max) return BL_ERR_INVALID_ARG;
     layer_e[tb] += eb;
     layer_n[tb] += 1;
@@ -144,4 +152,92 @@ extern "C" bl_status_t bl_conv_rate_for_energy(bl_conv_plan_t p, const double* e
     *c_out = c > 0.0 ? c : 0.0;
   }
   return BL_OK;
+}
+
+extern "C" bl_status_t bl_conv_fine_band_for_energy(bl_conv_plan_t p, const double* energy, size_t n,
+                                                    double fraction, int* t_out, double* c_out,
+                                                    double* preserved_out, unsigned char* keep, size_t keep_cap,
+                                                    size_t* keep_n) {
+  int t = 0;
+  double c = 0.0;
+  const bl_status_t st = bl_conv_rate_for_energy(p, energy, n, fraction, &t, &c, nullptr);
+  if (st != BL_OK) return st;
+  const int t_max = p->ndim == 1 ? p->Lw / 2 : std::min(p->Lh / 2, p->Lw / 2);
+  // bins of the coarse band t (plan order), with their layers
+  std::vector<long> band;
+  std::vector<double> layer_e(t_max + 1, 0.0);
+  for (long b = 0; b < p->kept; ++b) {
+    const int tb = bin_last_layer(p, b);
+    layer_e[tb] += energy[b];
+    if (tb >= t) band.push_back(b);
+  }
+  // the same sums, in the same order, as the coarse rule
+  double total = 0.0;
+  for (int l = t_max; l >= 0; --l) total += layer_e[l];
+  double kept_e = 0.0;
+  for (int l = t_max; l > t; --l) kept_e += layer_e[l];
+  std::vector<unsigned char> k(band.size(), 1);
+  if (t < t_max && total > 0.0) {
+    // layer t's bins, largest energy first (equal energies in plan order),
+    // added until the band keeps the fraction; the others are dropped
+    std::vector<size_t> layer;
+    for (size_t i = 0; i < band.size(); ++i)
+      if (bin_last_layer(p, band[i]) == t) layer.push_back(i);
+    std::stable_sort(layer.begin(), layer.end(),
+                     [&](size_t a, size_t b) { return energy[band[a]] > energy[band[b]]; });
+    for (size_t i : layer) k[i] = 0;
+    for (size_t i : layer) {
+      if (kept_e / total >= fraction) break;
+      k[i] = 1;
+      kept_e += energy[band[i]];
+    }
+  } else {
+    kept_e = total;
+  }
+  if (keep_n) *keep_n = band.size();
+  if (keep) {
+    if (keep_cap < band.size()) return BL_ERR_INVALID_ARG;
+    std::copy(k.begin(), k.end(), keep);
+  }
+  if (t_out) *t_out = t;
+  if (c_out) *c_out = c;
+  if (preserved_out) *preserved_out = total > 0.0 ? kept_e / total : 1.0;
+  return BL_OK;
+}
+
+namespace blc {
+namespace {
+// rows of dropped bins set to zero: one block per (bin, slice of the row)
+template <typename S>
+__global__ __launch_bounds__(256) void k_zero_bins(S* __restrict__ spec, const unsigned char* __restrict__ keep,
+                                                   long row) {
+  const long b = blockIdx.y;
+  if (keep[b]) return;
+  S* r = spec + (size_t)b * row;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < row; i += (long)gridDim.x * 256)
+    spec_put(r, (size_t)i, make_float2(0.f, 0.f));
+}
+}  // namespace
+}  // namespace blc
+
+extern "C" bl_status_t bl_conv_zero_bins(bl_conv_plan_t p, void* ws, unsigned which, const unsigned char* keep,
+                                         void* stream) {
+  if (!p || !ws || !keep) return BL_ERR_INVALID_ARG;
+  if (which != BL_SPEC_X && which != BL_SPEC_W) return BL_ERR_INVALID_ARG;
+  if (p->kept > 65535) return BL_ERR_UNSUPPORTED;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* spec = static_cast<char*>(ws) + (which == BL_SPEC_X ? p->off_X : p->off_W);
+  const long row = which == BL_SPEC_X ? (long)p->N * p->Cin : (long)p->Cin * p->Cout;
+  const long slices = std::max<long>(1, std::min<long>(64, (row + 4095) / 4096));
+  const dim3 grid((unsigned)slices, (unsigned)p->kept);
+  // traffic: the mask read; the dropped rows written (at most every row)
+  const double bytes = (double)p->kept + (p->bf16 ? 4.0 : 8.0) * (double)row * (double)p->kept;
+  return timed_launch("zero_bins", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    if (p->bf16)
+      hipExtLaunchKernelGGL(k_zero_bins<unsigned>, grid, dim3(256), 0, s, e0, e1, 0, static_cast<unsigned*>(spec),
+                            keep, row);
+    else
+      hipExtLaunchKernelGGL(k_zero_bins<float2>, grid, dim3(256), 0, s, e0, e1, 0, static_cast<float2*>(spec),
+                            keep, row);
+  });
 }

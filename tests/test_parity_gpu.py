@@ -526,6 +526,63 @@ def test_fused_small_forward(torch):
         assert max(errs) <= TOL, errs
 
 
+def test_fine_band_forward(torch):
+    """Fine-grained energy-based band on the GPU: energies of the input on a
+    rate-0 plan, the fine band from them, a plan at the coarse rate, X and W
+    computed and zeroed at the dropped bins, and the forward pass on them,
+    against the oracle's forward with the same bins zeroed (2-D workload layers
+    and odd shapes, fp32 and bf16 spectra); the backward passes then run on the
+    same zeroed spectra and are checked against the adjoint identity."""
+    dev = torch.device("cuda:0")
+    cases = [(synth.CONFIGS[3].layers[0], 0, synth.layer_inputs(3, 0)),
+             (synth.CONFIGS[5].layers[0], 0, synth.layer_inputs(5, 0)),
+             (synth.CONFIGS[4].layers[2], blconv.BL_DESC_BF16_SPECTRA, synth.layer_inputs(4, 2))]
+    layer = synth.Layer("fine_odd", 2, 3, 4, 5, 11, 9, 3, (1, 1, 1, 1), "blur")
+    cases.append((layer, 0, synth.random_inputs(layer, 2600)))
+    cut = 0
+    for layer, fl, (x, w, dy) in cases:
+        xt, wt, dyt = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        p0 = blconv.plan_for_layer(layer, 0.0)
+        ws0 = p0.workspace(dev)
+        e = p0.input_energy(xt, ws0).cpu().numpy()
+        for fraction in (0.9, 0.99):
+            t, c, kept_f, keep = p0.fine_band_for_energy(e, fraction)
+            say(f"[fine] {layer.name} flags={fl} fraction={fraction}: t={t} c={c:.4f} kept {int(keep.sum())}/{keep.size}")
+            cut += int(not keep.all())
+            plan = blconv.plan_for_layer(layer, c, None, fl)
+            assert plan.kept == keep.size
+            ws = plan.workspace(dev)
+            ws.fill_(0xFF)
+            kt = torch.from_numpy(keep).to(dev)
+            plan.zero_smallest(xt, ws, "X", 0)  # computes X only
+            plan.zero_smallest(wt, ws, "W", 0)  # computes W only
+            plan.zero_bins(ws, "X", kt)
+            plan.zero_bins(ws, "W", kt)
+            y = torch.full(plan.y_shape(), float("nan"), device=dev)
+            dx = torch.full(plan.x_shape(), float("nan"), device=dev)
+            dw = torch.full(plan.w_shape(), float("nan"), device=dev)
+            R = blconv.BL_REUSE_X | blconv.BL_REUSE_W
+            plan.forward(None, None, y, ws, flags=R)
+            plan.backward_input(dyt, None, dx, ws, flags=blconv.BL_REUSE_W)
+            plan.backward_weight(None, dyt, dw, ws, flags=blconv.BL_REUSE_X)
+            torch.cuda.synchronize()
+            drop = keep == 0
+            zx = np.broadcast_to(drop[:, None, None], (keep.size, layer.N, layer.C_in))
+            zw = np.broadcast_to(drop[:, None, None], (keep.size, layer.C_in, layer.C_out))
+            want = bo.forward_zeroed(x, w, layer.pad, c, zx, zw)
+            got = y.cpu().numpy()
+            err = rel(got, want)
+            # adjoint identity of the fine-band layer: <dy, y(x)> = <dx, x> = <dw, w>
+            gx, gw = dx.cpu().numpy().astype(np.float64), dw.cpu().numpy().astype(np.float64)
+            a0 = float(np.sum(dy.astype(np.float64) * got))
+            a1, a2 = float(np.sum(gx * x)), float(np.sum(gw * w))
+            say(f"    forward rel err {err:.2e}; adjoint {a0:.6e} {a1:.6e} {a2:.6e}")
+            assert err <= (BF16_EXACT_TOL if fl else TOL), err
+            tol = 1e-2 if fl else 1e-4
+            assert abs(a1 - a0) <= tol * abs(a0) and abs(a2 - a0) <= tol * abs(a0)
+    assert cut > 0
+
+
 def test_graph_replays_match_eager(torch):
     """A layer's three passes captured in a HIP graph and replayed several times,
     with other eager library work, a poisoned workspace and outputs, and

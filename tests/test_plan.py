@@ -266,3 +266,53 @@ def test_rate_for_energy_edge_cases():
         plan.rate_for_energy(neg, 0.5)
     with pytest.raises(blconv.BlError):
         plan.rate_for_energy(dc[:-1], 0.5)
+
+
+def test_fine_band_for_energy_matches_oracle():
+    """The library's fine-grained band, fed the oracle's bin energies in the
+    plan's bin order, keeps the same bins as the oracle's (compared in the
+    coarse plan's bin order), away from ties of the fraction; 1-D bands are the
+    coarse ones; a too-small keep buffer is an error."""
+    rng = np.random.default_rng(12)
+    cut = checked = 0
+    for i in range(40):
+        layer = synth.random_layer(rng, 1 if i % 4 == 3 else 2)
+        x = synth.random_inputs(layer, 80 + i)[0].astype(np.float64)
+        if layer.ndim == 1:
+            E, last = bo.bin_energy_1d(x, layer.pad), bo.last_layer_kept(1, _grid(layer))
+        else:
+            E, last = bo.bin_energy_2d(x, layer.pad), bo.last_layer_kept(2, _grid(layer))
+        f = bo.preserved_fractions(E, last)
+        plan = blconv.plan_for_layer(layer, 0.0)
+        e = _energies_in_bin_order(plan, layer, E)
+        for fraction in (0.5, 0.8, 0.9, 0.97):
+            if np.min(np.abs(f - fraction)) < 1e-9:
+                continue
+            t_o, keep_o = bo.fine_energy_band(E, last, fraction)
+            # the oracle's kept fraction must not sit on the threshold either
+            band = last.ravel() >= t_o
+            Eb = E.ravel()[band]
+            if abs(Eb[keep_o].sum() / E.sum() - fraction) < 1e-9:
+                continue
+            t, c, kept_f, keep = plan.fine_band_for_energy(e, fraction)
+            assert t == t_o
+            coarse = blconv.plan_for_layer(layer, c)
+            assert coarse.kept == keep.size == keep_o.size
+            # the oracle's bins are in row-major (u, v) order, the same order the plans use
+            assert np.array_equal(keep.astype(bool), keep_o), (layer, fraction)
+            assert abs(kept_f - Eb[keep_o].sum() / E.sum()) < 1e-12
+            cut += int(not keep.all())
+            checked += 1
+            if layer.ndim == 1:
+                assert keep.all()
+    assert checked > 60 and cut > 10
+    lib = blconv.load()
+    plan = blconv.plan_for_layer(synth.Layer("e", 2, 1, 1, 1, 6, 6, 3, (1, 1, 1, 1), "blur"), 0.0)
+    e = np.ones(plan.kept)
+    n = ctypes.c_size_t()
+    t, c, pr = ctypes.c_int(), ctypes.c_double(), ctypes.c_double()
+    buf = np.zeros(1, np.uint8)
+    assert lib.bl_conv_fine_band_for_energy(plan._h, e.ctypes.data, e.size, 0.5, ctypes.byref(t), ctypes.byref(c),
+                                            ctypes.byref(pr), buf.ctypes.data, 0, ctypes.byref(n)) == 1
+    assert lib.bl_conv_zero_bins(None, None, 0, None, None) == 1
+    assert lib.bl_conv_zero_bins(plan._h, ctypes.c_void_p(8), 2, ctypes.c_void_p(8), None) == 1
