@@ -5,7 +5,8 @@
 // kept bin) or one output filter's spectrum (its C_in channels at every kept
 // bin); coefficient i of a group is (bin i / C_in, channel i % C_in).
 //
-//   k_zero_smallest   one block per group: an exact radix select of the k-th
+//   k_zero_smallest   one block per group (k_top_* below split few, large
+//                     groups over several blocks): an exact radix select of the k-th
 //                     smallest key |z|^2 (fp32 bit patterns of non-negative
 //                     values order as unsigned integers) over three digits
 //                     (11, 11 and 10 bits, one histogram pass each), then a
@@ -13,6 +14,7 @@
 //                     first keys equal to it in index order, so that exactly k
 //                     are zeroed and the result does not depend on scheduling.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -173,6 +175,134 @@ __global__ __launch_bounds__(256) void k_transpose_filters(const S* __restrict__
   }
 }
 
+// ---- several blocks per group (groups too few to fill the chip) ----------
+// The same select, with each group's coefficients split into NB slices of
+// `per` (one block of 256 each): per digit, every slice adds its LDS histogram
+// into the group's histogram in global memory and one wave per group picks the
+// digit; then each slice counts its keys equal to the threshold, and the
+// zeroing pass ranks the equal keys of a slice after those of the slices
+// before it, so the zeros are exactly those of the one-block select.
+constexpr int kSliceThreads = 256;
+
+struct TopState {
+  unsigned prefix, pmask, krem, pad;
+};
+
+__global__ __launch_bounds__(256) void k_top_init(unsigned* __restrict__ hist, TopState* __restrict__ st,
+                                                  unsigned k) {
+  const unsigned g = blockIdx.x;
+  for (int j = threadIdx.x; j < kDigitBins; j += 256) hist[(size_t)g * kDigitBins + j] = 0u;
+  if (threadIdx.x == 0) st[g] = TopState{0u, 0u, k, 0u};
+}
+
+template <typename S>
+__global__ __launch_bounds__(kSliceThreads) void k_top_hist(const S* __restrict__ keys, TopArgs g, unsigned per,
+                                                            unsigned* __restrict__ hist,
+                                                            const TopState* __restrict__ st, int pass) {
+  __shared__ unsigned h[kDigitBins];
+  const int tid = threadIdx.x;
+  const unsigned grp = blockIdx.y, i0 = blockIdx.x * per, i1 = min(g.n, i0 + per);
+  const size_t sbase = (size_t)grp * g.src.sG;
+  const TopState cur = st[grp];
+  const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
+  const unsigned dmask = pass == 2 ? 0x3FFu : 0x7FFu;
+  for (int j = tid; j < kDigitBins; j += kSliceThreads) h[j] = 0u;
+  __syncthreads();
+  Walk w(i0 + tid, kSliceThreads, g.src.C);
+  for (unsigned i = i0 + tid; i < i1; i += kSliceThreads, w.next()) {
+    const unsigned key = mag_key(keys, w.at(g.src, sbase));
+    if ((key & cur.pmask) == cur.prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+  }
+  __syncthreads();
+  unsigned* gh = hist + (size_t)grp * kDigitBins;
+  for (int j = tid; j < kDigitBins; j += kSliceThreads)
+    if (h[j]) atomicAdd(&gh[j], h[j]);
+}
+
+// one wave per group: the digit holding the krem-th candidate; the histogram
+// is cleared for the next digit
+__global__ __launch_bounds__(64) void k_top_select(unsigned* __restrict__ hist, TopState* __restrict__ st,
+                                                   int pass) {
+  const int lane = threadIdx.x;
+  const unsigned grp = blockIdx.x;
+  unsigned* gh = hist + (size_t)grp * kDigitBins;
+  const TopState cur = st[grp];
+  const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
+  const unsigned dmask = pass == 2 ? 0x3FFu : 0x7FFu;
+  unsigned s = 0;
+  for (int j = 0; j < 32; ++j) s += gh[lane * 32 + j];
+  unsigned incl = s;
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  const unsigned long long hit = __ballot(incl >= cur.krem);
+  if (lane == __builtin_ctzll(hit)) {
+    unsigned before = incl - s;
+    int d = lane * 32;
+    while (before + gh[d] < cur.krem) before += gh[d++];
+    st[grp] = TopState{cur.prefix | ((unsigned)d << shift), cur.pmask | (dmask << shift), cur.krem - before, 0u};
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  for (int j = lane; j < kDigitBins; j += 64) gh[j] = 0u;
+}
+
+template <typename S>
+__global__ __launch_bounds__(kSliceThreads) void k_top_count(const S* __restrict__ keys, TopArgs g, unsigned per,
+                                                             const TopState* __restrict__ st,
+                                                             unsigned* __restrict__ cnt) {
+  __shared__ unsigned wc[kSliceThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned grp = blockIdx.y, i0 = blockIdx.x * per, i1 = min(g.n, i0 + per);
+  const size_t sbase = (size_t)grp * g.src.sG;
+  const unsigned T = st[grp].prefix;
+  unsigned c = 0;
+  Walk w(i0 + tid, kSliceThreads, g.src.C);
+  for (unsigned i = i0 + tid; i < i1; i += kSliceThreads, w.next()) c += mag_key(keys, w.at(g.src, sbase)) == T;
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+  if (lane == 0) wc[wave] = c;
+  __syncthreads();
+  if (tid == 0) {
+    unsigned t = 0;
+    for (int q = 0; q < kSliceThreads / 64; ++q) t += wc[q];
+    cnt[(size_t)grp * gridDim.x + blockIdx.x] = t;
+  }
+}
+
+template <typename S>
+__global__ __launch_bounds__(kSliceThreads) void k_top_zero(S* __restrict__ spec, const S* __restrict__ keys,
+                                                            TopArgs g, unsigned per,
+                                                            const TopState* __restrict__ st,
+                                                            const unsigned* __restrict__ cnt) {
+  __shared__ unsigned wc[kSliceThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned grp = blockIdx.y, i0 = blockIdx.x * per, i1 = min(g.n, i0 + per);
+  const size_t sbase = (size_t)grp * g.src.sG, dbase = (size_t)grp * g.dst.sG;
+  const TopState cur = st[grp];
+  const unsigned T = cur.prefix;
+  unsigned seen = 0;  // keys equal to T in earlier slices, then earlier chunks
+  for (unsigned q = 0; q < blockIdx.x; ++q) seen += cnt[(size_t)grp * gridDim.x + q];
+  Walk ws(i0 + tid, kSliceThreads, g.src.C), wd(i0 + tid, kSliceThreads, g.dst.C);
+  for (unsigned start = i0; start < i1; start += kSliceThreads, ws.next(), wd.next()) {
+    const bool in = start + tid < i1;
+    const unsigned key = in ? mag_key(keys, ws.at(g.src, sbase)) : 0xFFFFFFFFu;
+    const bool eq = in && key == T;
+    const unsigned long long bal = __ballot(eq);
+    const unsigned below = (unsigned)__popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wc[wave] = (unsigned)__popcll(bal);
+    __syncthreads();
+    unsigned rank = seen + below, total = 0;
+    for (int q = 0; q < kSliceThreads / 64; ++q) {
+      if (q < wave) rank += wc[q];
+      total += wc[q];
+    }
+    if (in && (key < T || (eq && rank < cur.krem))) spec_put(spec, wd.at(g.dst, dbase), make_float2(0.f, 0.f));
+    seen += total;
+    __syncthreads();
+  }
+}
+
 }  // namespace
 }  // namespace blc
 
@@ -229,6 +359,54 @@ extern "C" bl_status_t bl_conv_zero_smallest(bl_conv_plan_t p, const float* src,
   // compulsory traffic: the spectrum read once and the zeroed coefficients written
   const double eb = p->bf16 ? 4.0 : 8.0;
   const double bytes = eb * (double)groups * ((double)g.n + (double)g.k);
+  // few, large groups: slices of at least 4096 coefficients, about 1024
+  // blocks in all, at the price of nine launches instead of one (measured:
+  // C5's 32 samples of 111 360 coefficients 143 -> 54 us; groups of 12 288 to
+  // 39 168 coefficients are faster with one block each); scratch (histograms,
+  // states, counts) in the contraction-output region of ws, which holds
+  // nothing between calls
+  if (g.k < g.n && groups <= 128 && g.n >= 65536) {
+    const long want = std::max<long>(2, (1024 + groups - 1) / groups);
+    const unsigned per = (unsigned)std::max<long>(4096, ((long)g.n + want - 1) / want);
+    const unsigned nb = (g.n + per - 1) / per;
+    char* scratch = static_cast<char*>(ws) + p->off_T;
+    unsigned* hist = reinterpret_cast<unsigned*>(scratch);
+    TopState* st = reinterpret_cast<TopState*>(hist + (size_t)groups * kDigitBins);
+    unsigned* cnt = reinterpret_cast<unsigned*>(st + groups);
+    const size_t need = (size_t)groups * (kDigitBins * 4 + sizeof(TopState) + (size_t)nb * 4);
+    const size_t have = p->off_DW - p->off_T;
+    if (need <= have && nb <= 65535) {
+      const dim3 sg(nb, (unsigned)groups);
+      auto run = [&](auto* sp, auto* kp) -> bl_status_t {
+        using S = std::remove_const_t<std::remove_pointer_t<decltype(kp)>>;
+        bl_status_t r = timed_launch("zero_smallest_init", (double)groups * kDigitBins * 4, 0.0, s,
+                                     [&](hipEvent_t e0, hipEvent_t e1) {
+          hipExtLaunchKernelGGL(k_top_init, dim3((unsigned)groups), dim3(256), 0, s, e0, e1, 0, hist, st, g.k);
+        });
+        for (int pass = 0; pass < 3 && r == BL_OK; ++pass) {
+          r = timed_launch("zero_smallest_hist", eb * groups * (double)g.n, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+            hipExtLaunchKernelGGL(k_top_hist<S>, sg, dim3(kSliceThreads), 0, s, e0, e1, 0, kp, g, per, hist, st,
+                                  pass);
+          });
+          if (r != BL_OK) break;
+          r = timed_launch("zero_smallest_select", (double)groups * kDigitBins * 8, 0.0, s,
+                           [&](hipEvent_t e0, hipEvent_t e1) {
+            hipExtLaunchKernelGGL(k_top_select, dim3((unsigned)groups), dim3(64), 0, s, e0, e1, 0, hist, st, pass);
+          });
+        }
+        if (r != BL_OK) return r;
+        r = timed_launch("zero_smallest_count", eb * groups * (double)g.n, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+          hipExtLaunchKernelGGL(k_top_count<S>, sg, dim3(kSliceThreads), 0, s, e0, e1, 0, kp, g, per, st, cnt);
+        });
+        if (r != BL_OK) return r;
+        return timed_launch("zero_smallest", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+          hipExtLaunchKernelGGL(k_top_zero<S>, sg, dim3(kSliceThreads), 0, s, e0, e1, 0, sp, kp, g, per, st, cnt);
+        });
+      };
+      if (p->bf16) return run(static_cast<unsigned*>(spec), static_cast<const unsigned*>(keys));
+      return run(static_cast<float2*>(spec), static_cast<const float2*>(keys));
+    }
+  }
   return timed_launch("zero_smallest", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
     if (p->bf16)
       hipExtLaunchKernelGGL(k_zero_smallest<unsigned>, dim3((unsigned)groups), dim3(kTopThreads), 0, s, e0, e1, 0,

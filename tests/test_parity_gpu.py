@@ -449,13 +449,16 @@ def test_zero_smallest_parity(torch):
     but one, all, more than all), checked against the oracle's ranking and by
     the forward pass on the zeroed spectra against the oracle's forward with the
     same coefficients zeroed (and against forward_top where the choices agree);
-    a 2-D workload layer, the 1-D stack's widest layer, small odd shapes, and a
-    plan with bfloat16 spectra."""
+    a 2-D workload layer, the 1-D stack's widest layer, small odd shapes, groups
+    large enough to be split over several blocks, and bfloat16 spectra."""
     dev = torch.device("cuda:0")
     cases = [(synth.CONFIGS[3].layers[0], 0.5, 0, synth.layer_inputs(3, 0)),
              (synth.CONFIGS[2].layers[1], 0.5, 0, synth.layer_inputs(2, 1))]
+    # the last: few groups of more than 65 536 coefficients, selected over
+    # several blocks each (the others one block per group)
     small = [synth.Layer("top_2d_odd", 2, 3, 5, 7, 9, 11, 3, (1, 1, 1, 1), "blur"),
-             synth.Layer("top_1d", 1, 4, 3, 6, 90, 1, 5, (2, 2), "walk")]
+             synth.Layer("top_1d", 1, 4, 3, 6, 90, 1, 5, (2, 2), "walk"),
+             synth.Layer("top_2d_wide", 2, 2, 80, 3, 40, 40, 3, (1, 1, 1, 1), "blur")]
     for i, layer in enumerate(small):
         cases.append((layer, 0.0, 0, synth.random_inputs(layer, 2400 + i)))
         cases.append((layer, 0.3, blconv.BL_DESC_BF16_SPECTRA, synth.random_inputs(layer, 2400 + i)))
