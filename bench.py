@@ -224,7 +224,7 @@ def cpu_baseline(cfg, c, target_s):
         n = min(N, n * 2)
         dt, _ = run(n)
     reps, total, flops = 0, 0.0, 0.0
-    while total < target_s * 0.5 or reps == 0:
+    while total < target_s or reps == 0:
         dt, f = run(n)
         total += dt; flops += f; reps += 1
     return {"value": flops / total / 1e12, "unit": "TFLOP-equiv/s", "cores": threads, "kind": "oracle",
