@@ -261,8 +261,10 @@ bl_status_t bl_conv_zero_bins(bl_conv_plan_t plan, void* ws, unsigned which, con
  * flags holds the reuse flag of that spectrum (BL_REUSE_X or BL_REUSE_W; src
  * may then be NULL).  A following bl_conv_forward with BL_REUSE_X | BL_REUSE_W
  * computes the layer on the zeroed spectra (the backward passes likewise with
- * their reuse flags).  k = 0 only computes the spectrum.  BL_SPEC_W also uses
- * workspace outside X, W and DY as scratch (a group-major copy of W).  Errors:
+ * their reuse flags).  k = 0 only computes the spectrum.  The call may use
+ * the workspace outside X, W and DY as scratch (a group-major copy of W; the
+ * histograms of groups split over several blocks), so what the compute calls
+ * leave there is not kept.  Errors:
  * NULL plan or
  * ws, k < 0, another `which`, other flags, src NULL without the reuse flag:
  * BL_ERR_INVALID_ARG; a group of 2^31 or more coefficients:
