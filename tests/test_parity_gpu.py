@@ -591,19 +591,21 @@ def test_graph_replays_match_eager(torch):
     with other eager library work, a poisoned workspace and outputs, and
     synchronisations between the replays: every replay's outputs are
     bit-identical to the eager calls' (1-D chirp-z, 2-D, thin and tiled
-    contractions)."""
+    contractions, bfloat16 spectra, the fused small-map forward)."""
     dev = torch.device("cuda:0")
     cases = [
-        (synth.Layer("graph_1d", 1, 16, 24, 40, 300, 1, 5, (2, 2), "walk"), 0.5),
-        (synth.Layer("graph_2d", 2, 4, 16, 32, 16, 16, 3, (1, 1, 1, 1), "blur"), 0.25),
-        (synth.Layer("graph_thin", 1, 8, 1, 64, 200, 1, 8, (3, 4), "walk"), 0.0),
+        (synth.Layer("graph_1d", 1, 16, 24, 40, 300, 1, 5, (2, 2), "walk"), 0.5, 0),
+        (synth.Layer("graph_2d", 2, 4, 16, 32, 16, 16, 3, (1, 1, 1, 1), "blur"), 0.25, 0),
+        (synth.Layer("graph_thin", 1, 8, 1, 64, 200, 1, 8, (3, 4), "walk"), 0.0, 0),
+        (synth.Layer("graph_bf16", 2, 16, 32, 48, 12, 12, 3, (1, 1, 1, 1), "blur"), 0.25, blconv.BL_DESC_BF16_SPECTRA),
+        (synth.Layer("graph_fused", 2, 4, 8, 6, 8, 8, 3, (1, 1, 1, 1), "blur"), 0.0, blconv.BL_DESC_FUSED_FORWARD),
     ]
     other = synth.Layer("graph_other", 2, 2, 8, 8, 10, 10, 3, (1, 1, 1, 1), "blur")
     ox, ow, ody = synth.random_inputs(other, 5)
-    for i, (layer, c) in enumerate(cases):
-        say(f"[graph] {layer.name} c={c}")
+    for i, (layer, c, fl) in enumerate(cases):
+        say(f"[graph] {layer.name} c={c} flags={fl}")
         x, w, dy = (torch.from_numpy(a).to(dev) for a in synth.random_inputs(layer, 1900 + i))
-        plan = blconv.plan_for_layer(layer, c)
+        plan = blconv.plan_for_layer(layer, c, None, fl)
         ws = plan.workspace(dev)
         y = torch.empty(plan.y_shape(), device=dev)
         dx = torch.empty(plan.x_shape(), device=dev)
