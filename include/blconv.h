@@ -141,7 +141,10 @@ typedef struct bl_conv_plan_s* bl_conv_plan_t;
 #define BL_REUSE_DY 0x4u  /* backward_weight: reuse DY */
 
 /* Build a plan: geometry, the number of peeled layers t for rate c, the kept
- * bin set and the workspace layout.  Host only. */
+ * bin set and the workspace layout.  Host only.  BL_ERR_UNSUPPORTED for
+ * K > 8, a grid side above 4096, more than 65535 kept bins, or a plane whose
+ * direct transform would need more than 160 KB of LDS (e.g. a 2-D grid
+ * 8 x 4096), so that the compute calls of a plan never fail for its shape. */
 bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_desc_t* desc);
 bl_status_t bl_conv_plan_destroy(bl_conv_plan_t plan);
 

@@ -569,10 +569,25 @@ __global__ __launch_bounds__(kThreads) void k_contract(const S* __restrict__ A, 
   }
 }
 
-int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap) {
+int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap, size_t limit = kMaxLds) {
   int tp = (int)std::min<long>(cap, P);
-  while (tp > 1 && fixed_bytes + tp * per_plane_bytes > kMaxLds) --tp;
+  while (tp > 1 && fixed_bytes + tp * per_plane_bytes > limit) --tp;
   return std::max(tp, 1);
+}
+
+// A plane whose working set exceeds 64 KB (long 1-D series, wide maps) runs
+// alone in a block with up to the CU's 160 KB of LDS, which the kernel must
+// be allowed once per device.
+constexpr size_t kMaxLdsLarge = 160 * 1024;
+bool allow_large_lds(const void* kern, bool* done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  if (!done[dev]) {
+    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsLarge) != hipSuccess)
+      return false;
+    done[dev] = true;
+  }
+  return true;
 }
 
 }  // namespace
@@ -587,9 +602,16 @@ bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, voi
   FwdGeom g{Hin, Win, oi, oj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0};
   const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
   const size_t per = (size_t)(Hin * p->V + 1) * sizeof(float2) + (size_t)Hin * Win * sizeof(float);
-  if (fixed + per > kMaxLds) return BL_ERR_UNSUPPORTED;
-  g.TP = planes_per_block(fixed, per, P, 16);
+  const size_t limit = fixed + per > kMaxLds ? kMaxLdsLarge : kMaxLds;
+  if (fixed + per > limit) return BL_ERR_UNSUPPORTED;
+  g.TP = planes_per_block(fixed, per, P, 16, limit);
   const size_t lds = fixed + g.TP * per;
+  if (lds > kMaxLds) {
+    static bool done16[64] = {}, done32[64] = {};
+    const void* kern = p->bf16 ? reinterpret_cast<const void*>(&k_spec_fwd<unsigned>)
+                               : reinterpret_cast<const void*>(&k_spec_fwd<float2>);
+    if (!allow_large_lds(kern, p->bf16 ? done16 : done32)) return BL_ERR_HIP;
+  }
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
   return timed_launch("spec_fwd_direct", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
@@ -607,9 +629,14 @@ bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, fl
   InvGeom g{OH, OW, ci, cj, p->Lh, p->Lw, p->r_h, p->R, p->V, P, 0, 1.0f / ((float)p->Lh * (float)p->Lw)};
   const size_t fixed = (size_t)(p->Lh + p->Lw) * sizeof(float2);
   const size_t per = (size_t)(p->R * p->V + 1 + OH * p->V + 1) * sizeof(float2);
-  if (fixed + per > kMaxLds) return BL_ERR_UNSUPPORTED;
-  g.TP = planes_per_block(fixed, per, P, 16);
+  const size_t limit = fixed + per > kMaxLds ? kMaxLdsLarge : kMaxLds;
+  if (fixed + per > limit) return BL_ERR_UNSUPPORTED;
+  g.TP = planes_per_block(fixed, per, P, 16, limit);
   const size_t lds = fixed + g.TP * per;
+  if (lds > kMaxLds) {
+    static bool done[64] = {};
+    if (!allow_large_lds(reinterpret_cast<const void*>(&k_spec_inv), done)) return BL_ERR_HIP;
+  }
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
   return timed_launch("spec_inv_direct", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {

@@ -86,6 +86,16 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   }
   p->V = p->r_w + 1;
   p->kept = (long)p->R * p->V;
+  // every compute call must find a kernel for the shape, so that a call that
+  // fails has enqueued nothing: the contraction takes at most 65535 kept bins,
+  // and the direct transforms (the fallback of every faster one) hold a plane
+  // in at most 160 KB of LDS
+  {
+    const size_t tw = (size_t)(p->Lh + p->Lw) * 8;
+    const size_t fwd = tw + ((size_t)p->Hi * p->V + 1) * 8 + (size_t)p->Hi * p->Wi * 4;
+    const size_t inv = tw + ((size_t)p->R * p->V + 1 + (size_t)p->Hi * p->V + 1) * 8;
+    if (p->kept > 65535 || fwd > 160 * 1024 || inv > 160 * 1024) { delete p; return BL_ERR_UNSUPPORTED; }
+  }
   p->c_eff = 1.0 - (double)p->kept / (double)p->total;
 
   p->mask.assign((size_t)p->total, 0);

@@ -167,6 +167,25 @@ def test_edge_cases(torch):
             assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL, (layer.name, c)
 
 
+def test_largest_grids(torch):
+    """Grid sides at the 4096-point limit (1-D length 4096), a 2-D map 2048
+    wide, and a large 2-D grid outside the fast transforms (66 x 66), through
+    the direct DFT path (a plane per block with up to 160 KB of LDS where 64 KB
+    does not hold it), at rates 0 and 0.5."""
+    cases = [synth.Layer("max1d", 1, 2, 2, 3, 4090, 1, 7, (3, 3), "walk"),
+             synth.Layer("wide2d", 2, 1, 2, 2, 3, 2046, 3, (1, 1, 1, 1), "blur"),
+             synth.Layer("grid66", 2, 2, 3, 4, 64, 64, 3, (1, 1, 1, 1), "blur")]
+    for i, layer in enumerate(cases):
+        for c in (0.0, 0.5):
+            say(f"[max] {layer.name} c={c}")
+            x, w, dy = synth.random_inputs(layer, 2700 + i)
+            y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
+            ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            say(f"    grid {plan.fft} kept {plan.kept}/{plan.total}; rel err {errs}")
+            assert max(errs) <= TOL, errs
+
+
 def test_1d_long_sequences(torch):
     """1-D lengths that take the chirp-z (Bluestein) path with FFT sizes 256,
     512 and 1024, odd and even grids, offsets, grid overrides, and lengths

@@ -125,6 +125,11 @@ def _create(**kw):
     (dict(flags=1), 0), (dict(flags=2), 0), (dict(flags=3), 0), (dict(flags=4), 1), (dict(flags=0x80000000), 1), (dict(H=2, W=2, K=3), 1), (dict(H=2, W=2, K=3, pad_lo=(1, 1)), 0),
     (dict(ndim=1, W=1, H=10), 0), (dict(ndim=1, W=2, H=10), 1), (dict(ndim=1, W=1, H=10, pad_lo=(0, 1)), 1),
     (dict(ndim=1, W=1, H=10, fft_w=4), 1), (dict(ndim=1, W=1, H=10, fft_h=9), 1),
+    # the largest grid side is 4096 points
+    (dict(ndim=1, W=1, H=4096), 0), (dict(ndim=1, W=1, H=4097), 2), (dict(H=3, W=4096), 0), (dict(H=4097, W=8), 2),
+    (dict(ndim=1, W=1, H=10, fft_h=4097), 2),
+    # shapes no kernel path holds: a plane over 160 KB of LDS, more than 65535 kept bins
+    (dict(H=8, W=4096), 2), (dict(H=400, W=400), 2), (dict(H=128, W=128, c=0.5), 0),
 ])
 def test_plan_create_validation(kw, code):
     assert _create(**kw) == code
