@@ -129,6 +129,7 @@ struct Fft2Args {
   int PS;          // LDS plane stride of the column-major spectra (complex)
   unsigned q4;     // Win / 4 (forward) or OW (inverse): divisor of the flat copy
   unsigned magic;  // ceil(2^32 / q4) for q4 > 1: e / q4 == umulhi(e, magic) for the block's e
+  unsigned K;      // plane groups per 128-byte line of a bin row (plane_group)
   float scale;     // inverse: 1 / (Lh Lw)
 };
 
@@ -138,6 +139,20 @@ __device__ __forceinline__ int row_slot(int u, int r_h, int R, int LH) {
   if (u <= r_h) return u;
   const int r = u - (LH - R);
   return r > r_h ? r : -1;
+}
+
+// Plane group of a block.  A block's planes form runs of G values in every bin
+// row of the bin-major spectra; where a run is shorter than a 128-byte line,
+// the K adjacent groups that fill one line are given to blocks of one XCD (the
+// hardware deals consecutive blocks to the 8 XCDs in turn), so the line is
+// fetched into that XCD's L2 once rather than by K XCDs.  Blocks in flight
+// still cover one contiguous range of planes.  Trailing blocks short of a
+// whole set of 8 K keep their own index.
+__device__ inline unsigned plane_group(unsigned b, unsigned nb, unsigned K) {
+  const unsigned set = 8u * K;
+  if (K <= 1 || b >= nb / set * set) return b;
+  const unsigned r = b % set;
+  return b - r + (r % 8u) * K + r / 8u;
 }
 
 // LDS layout (complex spectra, column-major per plane): S[p * PS + v * (LH + 1) + i],
@@ -151,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
   float* xs = reinterpret_cast<float*>(sm);  // staging: G*Hin padded grid rows of LW1 floats
   float2* T = sm;                            // row spectra, column-major; aliases xs
   const int tid = threadIdx.x;
-  const unsigned p0 = blockIdx.x * (unsigned)g.G;
+  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
   const int nrows = np * g.Hin;
 
@@ -242,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   float* ys = reinterpret_cast<float*>(sm);  // output staging: G*OH grid rows of LW1 floats; aliases Zs
   const int tid = threadIdx.x;
   const int OH = g.Hin, OW = g.Win;
-  const unsigned p0 = blockIdx.x * (unsigned)g.G;
+  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
 
   // column pass: thread = (kept column, plane), planes fastest
@@ -320,12 +335,15 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
 // ceil(2^32 / d) for d > 1 (d = 1 is handled by the kernels directly).
 unsigned magic_for(unsigned d) { return d > 1 ? (unsigned)((0x100000000ull + d - 1) / d) : 0u; }
 
+// Plane groups whose runs of G elements of `elem` bytes fill a 128-byte line.
+unsigned line_groups(int G, int elem) { return (unsigned)std::max(1, (128 + G * elem - 1) / (G * elem)); }
+
 template <int MH, int MW>
 bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                          int oj, hipStream_t s) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if (Win % 4 != 0 || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
-  Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)(Win / 4), 0, 1.0f};
+  Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)(Win / 4), 0, 1u, 1.0f};
   g.magic = magic_for(g.q4);
   g.PS = (p->V * (LH + 1)) | 1;
   // rows of a block must fit one pass of 256 threads; LDS for staging and spectra
@@ -339,6 +357,10 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, lo
   while (G > 1 && lds_for(G) > kMaxLds) --G;
   if (Hin > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
   g.G = G;
+  // the forward writes its runs; sharing lines paid off for runs of 32 bytes
+  // (1.2x) and cost time for runs of 64 bytes, so it is kept to the shorter runs
+  const int run = G * (p->bf16 ? 4 : 8);
+  g.K = run < 64 ? line_groups(G, p->bf16 ? 4 : 8) : 1u;
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
   // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
@@ -359,7 +381,7 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
                          int cj, hipStream_t s) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if ((double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
-  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)OW, 0,
+  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)OW, 0, 1u,
              1.0f / ((float)p->Lh * (float)p->Lw)};
   g.magic = magic_for(g.q4);
   g.PS = (p->V * (LH + 1)) | 1;
@@ -373,6 +395,7 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   while (G > 1 && lds_for(G) > kMaxLds) --G;
   if (OH > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
   g.G = G;
+  g.K = line_groups(G, 8);
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
   const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
