@@ -202,7 +202,7 @@ def cpu_baseline(cfg, c, target_s):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         threads = 1
-    layers = synth.CONFIGS[cfg].layers
+    layers = synth.WORKLOADS[cfg].layers
     arrays = [synth.layer_inputs(cfg, i) for i in range(len(layers))]
 
     def run(n):
@@ -255,7 +255,7 @@ def main():
         torch.mul(src, 1.0, out=dst)  # reads 4n bytes, writes 4n bytes
         torch.cuda.synchronize()
         del src, dst
-    cfg = synth.CONFIGS[args.config]
+    cfg = synth.WORKLOADS[args.config]
     arrays = [synth.layer_inputs(args.config, i) for i in range(len(cfg.layers))]
     eq_flops = sum(3 * L.direct_flops() for L in cfg.layers)
 
@@ -333,8 +333,8 @@ def main():
 
     if args.table:
         with open(args.table, "w") as fh:
-            for ci in sorted(synth.CONFIGS):
-                cf = synth.CONFIGS[ci]
+            for ci in sorted(synth.WORKLOADS):
+                cf = synth.WORKLOADS[ci]
                 arr = [synth.layer_inputs(ci, i) for i in range(len(cf.layers))]
                 for c in cf.rates:
                     for li, (L, a) in enumerate(zip(cf.layers, arr)):

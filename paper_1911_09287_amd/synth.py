@@ -84,7 +84,7 @@ def _same(K):
     return lo, K - 1 - lo
 
 
-CONFIGS = {
+WORKLOADS = {
     1: Config(1, "tiny 2-D layer 3->16 @32x32, batch 2",
               (Layer("tiny_3to16_32", 2, 2, 3, 16, 32, 32, 3, (1, 1, 1, 1), "blur", 1.5),),
               (0.0, 0.5)),
@@ -174,7 +174,7 @@ def make_dy(layer: Layer, seed: int) -> np.ndarray:
 def layer_inputs(config: int, layer_index: int, layer: Layer | None = None):
     """(x, w, dy) fp32 arrays for one layer of a workload, from the fixed seeds."""
     if layer is None:
-        layer = CONFIGS[config].layers[layer_index]
+        layer = WORKLOADS[config].layers[layer_index]
     return (make_x(layer, seed_for(config, layer_index, "x")),
             make_w(layer, seed_for(config, layer_index, "w")),
             make_dy(layer, seed_for(config, layer_index, "dy")))

@@ -8,7 +8,7 @@ spectrum, and the band chosen for 90 %, 99 % and 99.9 % of the input's energy
 A reporting script, not a test (pytest does not collect it).  Run it on a GPU
 host from the repository root:
 
-    python tests/report_energy.py --out gpurun_out/energy.jsonl
+    python tests/report_energy.py --out energy.jsonl
 """
 import argparse
 import json
@@ -37,8 +37,8 @@ def main():
     blconv.load()
     dev = torch.device("cuda:0")
     with open(args.out, "w") as fh:
-        for ci in sorted(synth.CONFIGS):
-            for li, layer in enumerate(synth.CONFIGS[ci].layers):
+        for ci in sorted(synth.WORKLOADS):
+            for li, layer in enumerate(synth.WORKLOADS[ci].layers):
                 x = torch.from_numpy(synth.layer_inputs(ci, li)[0]).to(dev)
                 plan = blconv.plan_for_layer(layer, 0.0)
                 ws = plan.workspace(dev)

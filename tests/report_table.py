@@ -8,7 +8,7 @@ own CPU time for the three passes with the cores it used.
 A reporting script, not a test (pytest does not collect it).  Run it on a
 GPU host from the repository root:
 
-    python tests/report_table.py --out gpurun_out/table.jsonl [--configs 1 2 ...]
+    python tests/report_table.py --out table.jsonl [--configs 1 2 ...]
 
 The oracle runs single-shot per row (fp64 NumPy; numpy.fft is single
 threaded, the per-bin matmuls use the BLAS threads reported in the row).
@@ -70,7 +70,7 @@ def stage_fracs(kernels):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", required=True)
-    ap.add_argument("--configs", type=int, nargs="*", default=sorted(synth.CONFIGS))
+    ap.add_argument("--configs", type=int, nargs="*", default=sorted(synth.WORKLOADS))
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     args = ap.parse_args()
@@ -82,7 +82,7 @@ def main():
     cores = len(os.sched_getaffinity(0))
     with open(args.out, "w") as fh:
         for ci in args.configs:
-            cfg = synth.CONFIGS[ci]
+            cfg = synth.WORKLOADS[ci]
             for li, layer in enumerate(cfg.layers):
                 x, w, dy = synth.layer_inputs(ci, li)
                 for c in cfg.rates:

@@ -71,7 +71,7 @@ def test_c0_equals_torch_conv_fp64():
     """A library routine as a second c = 0 witness: torch conv + autograd, fp64."""
     torch = pytest.importorskip("torch")
     import torch.nn.functional as Fn
-    for layer in (synth.CONFIGS[1].layers[0],
+    for layer in (synth.WORKLOADS[1].layers[0],
                   synth.Layer("odd", 2, 2, 3, 5, 9, 7, 4, (2, 1, 0, 3), "blur"),
                   synth.Layer("even1d", 1, 2, 3, 4, 20, 1, 8, (3, 4), "walk")):
         x, w, dy = synth.random_inputs(layer, 7)

@@ -58,13 +58,13 @@ def oracle_passes(layer, c, x, w, dy, fft=None, rounding=None):
             bo.backward_weight(x, dy, layer.K, layer.pad, c, fft, rounding))
 
 
-CASES = [(cfg, li, c) for cfg in sorted(synth.CONFIGS) for li in range(len(synth.CONFIGS[cfg].layers))
-         for c in synth.CONFIGS[cfg].rates]
+CASES = [(cfg, li, c) for cfg in sorted(synth.WORKLOADS) for li in range(len(synth.WORKLOADS[cfg].layers))
+         for c in synth.WORKLOADS[cfg].rates]
 
 
 @pytest.mark.parametrize("cfg,li,c", CASES, ids=[f"C{a}-L{b}-c{c}" for a, b, c in CASES])
 def test_config_parity(torch, cfg, li, c):
-    layer = synth.CONFIGS[cfg].layers[li]
+    layer = synth.WORKLOADS[cfg].layers[li]
     say(f"[parity] config {cfg} layer {layer.name} c={c}")
     x, w, dy = synth.layer_inputs(cfg, li)
     y, dx, dw, plan, ws = gpu_passes(torch, layer, c, x, w, dy)
@@ -78,7 +78,7 @@ def test_config_parity(torch, cfg, li, c):
 def test_stored_spectra_match_oracle(torch):
     """Unit level: X, W and DY left in the workspace vs the oracle's kept spectra."""
     for cfg, li, c in ((1, 0, 0.5), (3, 0, 0.25), (2, 1, 0.5), (5, 0, 0.75), (3, 3, 0.0)):
-        layer = synth.CONFIGS[cfg].layers[li]
+        layer = synth.WORKLOADS[cfg].layers[li]
         say(f"[spectra] config {cfg} layer {layer.name} c={c}")
         x, w, dy = synth.layer_inputs(cfg, li)
         _, _, _, plan, ws = gpu_passes(torch, layer, c, x, w, dy)
@@ -123,7 +123,7 @@ def test_random_small_layers(torch, ndim):
 
 def test_reuse_flags_give_identical_results(torch):
     for cfg, li, c in ((1, 0, 0.5), (2, 0, 0.25), (4, 1, 0.75)):
-        layer = synth.CONFIGS[cfg].layers[li]
+        layer = synth.WORKLOADS[cfg].layers[li]
         say(f"[reuse] config {cfg} layer {layer.name} c={c}")
         x, w, dy = synth.layer_inputs(cfg, li)
         a = gpu_passes(torch, layer, c, x, w, dy, reuse=True)
@@ -135,7 +135,7 @@ def test_reuse_flags_give_identical_results(torch):
 def test_adjoint_identity_fp32(torch):
     """<dy, y> = <dx, x> = <dw, w> on the GPU path: the three passes are adjoint."""
     for cfg, li, c in ((1, 0, 0.5), (3, 1, 0.25), (2, 2, 0.75), (5, 0, 0.5)):
-        layer = synth.CONFIGS[cfg].layers[li]
+        layer = synth.WORKLOADS[cfg].layers[li]
         say(f"[adjoint] config {cfg} layer {layer.name} c={c}")
         x, w, dy = synth.layer_inputs(cfg, li)
         y, dx, dw, _, _ = gpu_passes(torch, layer, c, x, w, dy)
@@ -377,10 +377,10 @@ def test_bf16_stored_spectra_and_energy(torch):
     the oracle's spectra rounded to bfloat16, and the per-bin input energies of
     the stored spectrum against the oracle's energies of the rounded one."""
     dev = torch.device("cuda:0")
-    cases = [(synth.CONFIGS[3].layers[0], 0.25, synth.layer_inputs(3, 0)),
-             (synth.CONFIGS[5].layers[0], 0.5, synth.layer_inputs(5, 0)),
-             (synth.CONFIGS[2].layers[1], 0.0, synth.layer_inputs(2, 1)),
-             (synth.CONFIGS[2].layers[2], 0.5, synth.layer_inputs(2, 2))]
+    cases = [(synth.WORKLOADS[3].layers[0], 0.25, synth.layer_inputs(3, 0)),
+             (synth.WORKLOADS[5].layers[0], 0.5, synth.layer_inputs(5, 0)),
+             (synth.WORKLOADS[2].layers[1], 0.0, synth.layer_inputs(2, 1)),
+             (synth.WORKLOADS[2].layers[2], 0.5, synth.layer_inputs(2, 2))]
     small = [synth.Layer("bf_blue512_1d", 1, 24, 3, 5, 200, 1, 8, (3, 4), "walk"),
              synth.Layer("bf_direct_2d", 2, 6, 5, 7, 9, 9, 3, (1, 1, 1, 1), "blur")]
     for i, layer in enumerate(small):
@@ -471,8 +471,8 @@ def test_zero_smallest_parity(torch):
     a 2-D workload layer, the 1-D stack's widest layer, small odd shapes, groups
     large enough to be split over several blocks, and bfloat16 spectra."""
     dev = torch.device("cuda:0")
-    cases = [(synth.CONFIGS[3].layers[0], 0.5, 0, synth.layer_inputs(3, 0)),
-             (synth.CONFIGS[2].layers[1], 0.5, 0, synth.layer_inputs(2, 1))]
+    cases = [(synth.WORKLOADS[3].layers[0], 0.5, 0, synth.layer_inputs(3, 0)),
+             (synth.WORKLOADS[2].layers[1], 0.5, 0, synth.layer_inputs(2, 1))]
     # the last: few groups of more than 65 536 coefficients, selected over
     # several blocks each (the others one block per group)
     small = [synth.Layer("top_2d_odd", 2, 3, 5, 7, 9, 11, 3, (1, 1, 1, 1), "blur"),
@@ -525,9 +525,9 @@ def test_fused_small_forward(torch):
     1x1 maps, three input channels, output-channel groups that do not divide
     C_out), against the oracle; the input spectrum it stores serves the
     backward passes' reuse flags, and the fused kernel is the one that ran."""
-    cases = [(synth.CONFIGS[4].layers[2], c, synth.layer_inputs(4, 2)) for c in (0.0, 0.5)]
-    cases += [(synth.CONFIGS[3].layers[3], 0.25, synth.layer_inputs(3, 3)),
-              (synth.CONFIGS[3].layers[2], 0.75, synth.layer_inputs(3, 2))]
+    cases = [(synth.WORKLOADS[4].layers[2], c, synth.layer_inputs(4, 2)) for c in (0.0, 0.5)]
+    cases += [(synth.WORKLOADS[3].layers[3], 0.25, synth.layer_inputs(3, 3)),
+              (synth.WORKLOADS[3].layers[2], 0.75, synth.layer_inputs(3, 2))]
     small = [synth.Layer("fz_odd", 2, 5, 3, 7, 7, 9, 3, (1, 1, 1, 1), "blur"),
              synth.Layer("fz_1x1", 2, 3, 4, 5, 1, 1, 1, (0, 0, 0, 0), "blur"),
              synth.Layer("fz_pad2", 2, 2, 6, 37, 6, 6, 5, (2, 2, 2, 2), "blur")]
@@ -556,9 +556,9 @@ def test_fine_band_forward(torch):
     and odd shapes, fp32 and bf16 spectra); the backward passes then run on the
     same zeroed spectra and are checked against the adjoint identity."""
     dev = torch.device("cuda:0")
-    cases = [(synth.CONFIGS[3].layers[0], 0, synth.layer_inputs(3, 0)),
-             (synth.CONFIGS[5].layers[0], 0, synth.layer_inputs(5, 0)),
-             (synth.CONFIGS[4].layers[2], blconv.BL_DESC_BF16_SPECTRA, synth.layer_inputs(4, 2))]
+    cases = [(synth.WORKLOADS[3].layers[0], 0, synth.layer_inputs(3, 0)),
+             (synth.WORKLOADS[5].layers[0], 0, synth.layer_inputs(5, 0)),
+             (synth.WORKLOADS[4].layers[2], blconv.BL_DESC_BF16_SPECTRA, synth.layer_inputs(4, 2))]
     layer = synth.Layer("fine_odd", 2, 3, 4, 5, 11, 9, 3, (1, 1, 1, 1), "blur")
     cases.append((layer, 0, synth.random_inputs(layer, 2600)))
     cut = 0
@@ -669,10 +669,10 @@ def test_input_energy_parity(torch):
     the energies of a spectrum stored by the forward pass (reuse flag)."""
     dev = torch.device("cuda:0")
     rng = np.random.default_rng(2100)
-    cases = [(synth.CONFIGS[3].layers[0], 0.0, synth.layer_inputs(3, 0)[0]),
-             (synth.CONFIGS[5].layers[0], 0.0, synth.layer_inputs(5, 0)[0]),
-             (synth.CONFIGS[2].layers[1], 0.0, synth.layer_inputs(2, 1)[0]),
-             (synth.CONFIGS[4].layers[1], 0.5, synth.layer_inputs(4, 1)[0])]
+    cases = [(synth.WORKLOADS[3].layers[0], 0.0, synth.layer_inputs(3, 0)[0]),
+             (synth.WORKLOADS[5].layers[0], 0.0, synth.layer_inputs(5, 0)[0]),
+             (synth.WORKLOADS[2].layers[1], 0.0, synth.layer_inputs(2, 1)[0]),
+             (synth.WORKLOADS[4].layers[1], 0.5, synth.layer_inputs(4, 1)[0])]
     for i in range(6):
         layer = synth.random_layer(rng, 1 + i % 2)
         cases.append((layer, float(rng.choice([0.0, 0.0, 0.3])), synth.random_inputs(layer, 2200 + i)[0]))

@@ -35,10 +35,10 @@ def _grid(layer):
     return (layer.H + layer.pad[0] + layer.pad[1], layer.W + layer.pad[2] + layer.pad[3])
 
 
-@pytest.mark.parametrize("cfg", sorted(synth.CONFIGS))
+@pytest.mark.parametrize("cfg", sorted(synth.WORKLOADS))
 def test_config_masks_match_oracle(cfg):
-    for layer in synth.CONFIGS[cfg].layers:
-        for c in (0.0, 0.25, 0.5, 0.75) + synth.CONFIGS[cfg].rates:
+    for layer in synth.WORKLOADS[cfg].layers:
+        for c in (0.0, 0.25, 0.5, 0.75) + synth.WORKLOADS[cfg].rates:
             plan = blconv.plan_for_layer(layer, c)
             L = _grid(layer)
             assert (plan.mask() == bo.mask(layer.ndim, L, c)).all()
@@ -87,8 +87,8 @@ def test_bins_order_is_documented_order():
 
 
 def test_workspace_layout_is_disjoint_and_large_enough():
-    for cfg in sorted(synth.CONFIGS):
-        for layer in synth.CONFIGS[cfg].layers:
+    for cfg in sorted(synth.WORKLOADS):
+        for layer in synth.WORKLOADS[cfg].layers:
             p = blconv.plan_for_layer(layer, 0.0)
             sizes = {"X": p.kept * p.N * p.C_in * 8, "W": p.kept * p.C_in * p.C_out * 8,
                      "DY": p.kept * p.N * p.C_out * 8}
