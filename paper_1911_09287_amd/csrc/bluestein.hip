@@ -754,15 +754,8 @@ bl_status_t launch_1k_nr(const BlueGeom& a, const void* in, void* out, const cha
   constexpr int M = 1024;
   const size_t lds = (size_t)(2 * kWaves1k * kXS + a.n_in + a.n_out + 2 * M) * sizeof(float2);
   if (lds > 160 * 1024) return BL_ERR_UNSUPPORTED;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return BL_ERR_HIP;
-  static bool attr_set[64] = {};
-  if (!attr_set[dev]) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bluestein1k<MODE, NR, S>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess)
-      return BL_ERR_HIP;
-    attr_set[dev] = true;
-  }
+  const bl_status_t at = lds_opt_in(reinterpret_cast<const void*>(&k_bluestein1k<MODE, NR, S>), 160 * 1024);
+  if (at != BL_OK) return at;
   const long jobs = (MODE >= 2) ? (a.P + 1) / 2 : a.P;
   const long pairs = (jobs + 1) / 2;  // one job per half-wave
   // one block per CU at most; when there is less than a full block of work

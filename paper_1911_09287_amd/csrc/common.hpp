@@ -73,6 +73,9 @@ __device__ inline int kept_row_d(int r, int r_h, int Lh, int R) { return r <= r_
 bl_status_t plan_table(const bl_conv_plan_s* p, const std::vector<long>& key,
                        const std::function<void(std::vector<float2>&)>& build, const float2** out);
 long float_key(float x);  // bit pattern of x, for keys
+// Allows kernel `kern` up to `bytes` of dynamic LDS on the current device
+// (hipFuncAttributeMaxDynamicSharedMemorySize), once per kernel and device.
+bl_status_t lds_opt_in(const void* kern, int bytes);
 
 // ---- stage launchers --------------------------------------------------------
 // Real planes [P][Hin][Win] placed at (oi, oj) of the grid -> kept spectrum

@@ -579,16 +579,7 @@ int planes_per_block(size_t fixed_bytes, size_t per_plane_bytes, long P, int cap
 // alone in a block with up to the CU's 160 KB of LDS, which the kernel must
 // be allowed once per device.
 constexpr size_t kMaxLdsLarge = 160 * 1024;
-bool allow_large_lds(const void* kern, bool* done) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
-  if (!done[dev]) {
-    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsLarge) != hipSuccess)
-      return false;
-    done[dev] = true;
-  }
-  return true;
-}
+bool allow_large_lds(const void* kern) { return lds_opt_in(kern, (int)kMaxLdsLarge) == BL_OK; }
 
 }  // namespace
 
@@ -607,10 +598,9 @@ bl_status_t launch_spec_fwd_direct(const bl_conv_plan_s* p, const float* in, voi
   g.TP = planes_per_block(fixed, per, P, 16, limit);
   const size_t lds = fixed + g.TP * per;
   if (lds > kMaxLds) {
-    static bool done16[64] = {}, done32[64] = {};
     const void* kern = p->bf16 ? reinterpret_cast<const void*>(&k_spec_fwd<unsigned>)
                                : reinterpret_cast<const void*>(&k_spec_fwd<float2>);
-    if (!allow_large_lds(kern, p->bf16 ? done16 : done32)) return BL_ERR_HIP;
+    if (!allow_large_lds(kern)) return BL_ERR_HIP;
   }
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
@@ -634,8 +624,7 @@ bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, fl
   g.TP = planes_per_block(fixed, per, P, 16, limit);
   const size_t lds = fixed + g.TP * per;
   if (lds > kMaxLds) {
-    static bool done[64] = {};
-    if (!allow_large_lds(reinterpret_cast<const void*>(&k_spec_inv), done)) return BL_ERR_HIP;
+    if (!allow_large_lds(reinterpret_cast<const void*>(&k_spec_inv))) return BL_ERR_HIP;
   }
   const long blocks = (P + g.TP - 1) / g.TP;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
@@ -716,16 +705,9 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
     const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
     auto go = [&](auto kern, int nw) {
       // the static reduction buffer plus up to kWgradSliceLds of weights can
-      // pass 64 KB of LDS: allow that once per kernel and device
-      static bool allowed[64] = {};
-      int dev = 0;
-      if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return BL_ERR_HIP;
-      if (!allowed[dev]) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)kWgradSliceLds) != hipSuccess)
-          return BL_ERR_HIP;
-        allowed[dev] = true;
-      }
+      // pass 64 KB of LDS: allowed once per kernel instantiation and device
+      const bl_status_t at = lds_opt_in(reinterpret_cast<const void*>(kern), (int)kWgradSliceLds);
+      if (at != BL_OK) return at;
       return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
         hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * nw), lds, s, e0, e1, 0, DW, Et, dw, g);
       });

@@ -6,6 +6,7 @@
 #include <cstring>
 #include <mutex>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "common.hpp"
@@ -45,6 +46,19 @@ bl_status_t plan_table(const bl_conv_plan_s* p, const std::vector<long>& key,
   }
   cache->push_back(TabEntry{dev, key, d});
   *out = d;
+  return BL_OK;
+}
+
+bl_status_t lds_opt_in(const void* kern, int bytes) {
+  static std::mutex mu;
+  static std::vector<std::pair<const void*, int>> done;  // (kernel, device)
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BL_ERR_HIP;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const auto& e : done)
+    if (e.first == kern && e.second == dev) return BL_OK;
+  if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) != hipSuccess) return BL_ERR_HIP;
+  done.emplace_back(kern, dev);
   return BL_OK;
 }
 

@@ -334,6 +334,81 @@ def test_kept_spectrum_layout_matches_full_spectrum():
         assert np.abs(S[b] - full[:, :, u, v].ravel()).max() < 1e-10
 
 
+def _direct_kept_1d(a, offset, L, r):
+    """Kept half spectrum [r + 1][planes] of real series a[..., n] placed at
+    `offset` of a length-L grid: A[v] = sum_n a[n - offset] e^{-2 pi i v n / L}
+    for v = 0..r, written as an explicit sum over the series' samples."""
+    planes = a.reshape(-1, a.shape[-1])
+    n = np.arange(a.shape[-1]) + offset
+    out = np.zeros((r + 1, planes.shape[0]), complex)
+    for v in range(r + 1):
+        out[v] = planes @ np.exp(-2j * np.pi * v * n / L)
+    return out
+
+
+def _direct_half_plane_bins(Lh, Lw, t):
+    """Kept half-plane bins in storage order, from the full-plane band of
+    tests/brute_ref (rows in increasing u, within a row increasing v)."""
+    band = br.full_band_2d(Lh, Lw, t)
+    return [(u, v) for u in range(Lh) for v in range(Lw // 2 + 1) if band[u, v]]
+
+
+@pytest.mark.parametrize("L,offset,c,kept", [(11, 3, 0.5, 3), (12, 2, 0.25, 5), (9, 0, 0.0, 5), (16, 5, 0.6, 3),
+                                              (7, 1, 0.9, 1)])
+def test_kept_spectrum_1d_matches_direct_sum(L, offset, c, kept):
+    """Input-spectrum helper (Sec. 3.2.1 zero padding at the placement offset,
+    Sec. 3.2.2 low prefix of the half spectrum): bin order, embedding phase and
+    sign of the exponent against explicit sums, odd and even L."""
+    rng = np.random.default_rng(L * 10 + offset)
+    a = rng.standard_normal((2, 3, L - offset - 1))
+    assert int(bo.mask_1d(L, c)[0].sum()) == kept  # the "at least c" rule, counted by hand
+    S = bo.kept_spectrum_1d(a, offset, L, c)
+    ref = _direct_kept_1d(a, offset, L, kept - 1)
+    assert S.shape == (kept, 6)
+    assert np.abs(S - ref).max() < 1e-10
+    # a planted mistake: the spectrum of the series placed at offset 0 differs
+    # (except at DC, which no placement changes)
+    if offset and kept > 1:
+        assert np.abs(bo.kept_spectrum_1d(a, 0, L, c) - ref).max() > 1e-3
+
+
+@pytest.mark.parametrize("L,c,kept", [(10, 0.5, 3), (13, 0.0, 7), (8, 0.3, 3)])
+def test_kept_filter_spectrum_1d_matches_direct_sum(L, c, kept):
+    """Filter-spectrum helper: W[v][c][f] = sum_a w[f][c][a] e^{-2 pi i v a / L}
+    (taps at the origin, unconjugated), in [bin][C_in][C_out] order."""
+    rng = np.random.default_rng(L)
+    F, C, K = 4, 3, 3
+    w = rng.standard_normal((F, C, K))
+    assert int(bo.mask_1d(L, c)[0].sum()) == kept
+    S = bo.kept_filter_spectrum_1d(w, L, c)
+    assert S.shape == (kept, C, F)
+    taps = np.arange(K)
+    for v in range(kept):
+        e = np.exp(-2j * np.pi * v * taps / L)
+        for ci in range(C):
+            for f in range(F):
+                assert abs(S[v, ci, f] - np.sum(w[f, ci] * e)) < 1e-10
+
+
+@pytest.mark.parametrize("Lh,Lw,c", [(9, 8, 0.5), (6, 6, 0.3), (7, 5, 0.0), (10, 7, 0.6)])
+def test_kept_filter_spectrum_2d_matches_direct_sum(Lh, Lw, c):
+    """2-D filter-spectrum helper: W[b][c][f] = sum_{a,b'} w[f][c][a][b']
+    e^{-2 pi i (u a / Lh + v b' / Lw)} at the kept half-plane bins in storage
+    order, [bin][C_in][C_out]; odd and even sides."""
+    rng = np.random.default_rng(Lh * Lw)
+    F, C, K = 3, 2, 3
+    w = rng.standard_normal((F, C, K, K))
+    t = bo.mask_2d(Lh, Lw, c)[1]
+    bins = _direct_half_plane_bins(Lh, Lw, t)
+    S = bo.kept_filter_spectrum_2d(w, Lh, Lw, c)
+    assert S.shape == (len(bins), C, F)
+    ia, ib = np.meshgrid(np.arange(K), np.arange(K), indexing="ij")
+    for b, (u, v) in enumerate(bins):
+        e = np.exp(-2j * np.pi * (u * ia / Lh + v * ib / Lw))
+        ref = np.einsum("fcab,ab->cf", w, e)
+        assert np.abs(S[b] - ref).max() < 1e-10
+
+
 # ------------------------------------------- energy-based compression --
 
 

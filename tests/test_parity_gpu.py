@@ -1,8 +1,10 @@
 """GPU parity: the HIP library against the fp64 oracle on identical inputs.
 
-Bar: relative Frobenius error <= 1e-4 for y, dx and dw (fp32 path vs fp64
-oracle); stored spectra <= 1e-5 at unit level; masks byte-equal (CPU test).
-Every compute call goes through the C ABI (ctypes binding).
+Bar: for each of y, dx and dw (fp32 path vs fp64 oracle) both the relative
+Frobenius error and the largest element error max|g - o| / max|o| are at most
+1e-4, so an error confined to a few elements of a large output is not diluted
+by the norm; stored spectra <= 1e-5 at unit level; masks byte-equal (CPU
+test).  Every compute call goes through the C ABI (ctypes binding).
 """
 import numpy as np
 import pytest
@@ -18,6 +20,17 @@ SPEC_TOL = 1e-5
 
 def rel(a, b):
     return float(np.linalg.norm(np.ravel(a - b)) / max(np.linalg.norm(np.ravel(b)), 1e-30))
+
+
+def elem(a, b):
+    """Largest element error relative to the largest reference element."""
+    d = np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64))
+    return float(d.max() / max(float(np.abs(b).max()), 1e-30)) if d.size else 0.0
+
+
+def err(a, b):
+    """The fp32 parity measure: the larger of the norm-wise and element-wise errors."""
+    return max(rel(a, b), elem(a, b))
 
 
 @pytest.fixture(scope="module")
@@ -69,7 +82,7 @@ def test_config_parity(torch, cfg, li, c):
     x, w, dy = synth.layer_inputs(cfg, li)
     y, dx, dw, plan, ws = gpu_passes(torch, layer, c, x, w, dy)
     ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-    errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+    errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
     say(f"    rel err y={errs[0]:.2e} dx={errs[1]:.2e} dw={errs[2]:.2e} kept={plan.kept}/{plan.total}")
     assert all(np.isfinite(a).all() for a in (y, dx, dw))
     assert max(errs) <= TOL, errs
@@ -95,7 +108,7 @@ def test_stored_spectra_match_oracle(torch):
         gX = plan.spectrum(ws, "X").cpu().numpy().reshape(X.shape)
         gW = plan.spectrum(ws, "W").cpu().numpy().reshape(Wf.shape)
         gDY = plan.spectrum(ws, "DY").cpu().numpy().reshape(DY.shape)
-        assert rel(gX, X) <= SPEC_TOL and rel(gW, Wf) <= SPEC_TOL and rel(gDY, DY) <= SPEC_TOL
+        assert err(gX, X) <= SPEC_TOL and err(gW, Wf) <= SPEC_TOL and err(gDY, DY) <= SPEC_TOL
 
 
 @pytest.mark.parametrize("ndim", [1, 2])
@@ -118,7 +131,7 @@ def test_random_small_layers(torch, ndim):
         x, w, dy = synth.random_inputs(layer, 500 + i)
         y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
         ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
-        assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL
+        assert max(err(y, ry), err(dx, rdx), err(dw, rdw)) <= TOL
 
 
 def test_reuse_flags_give_identical_results(torch):
@@ -164,7 +177,7 @@ def test_edge_cases(torch):
             x, w, dy = synth.random_inputs(layer, 11)
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-            assert max(rel(y, ry), rel(dx, rdx), rel(dw, rdw)) <= TOL, (layer.name, c)
+            assert max(err(y, ry), err(dx, rdx), err(dw, rdw)) <= TOL, (layer.name, c)
 
 
 def test_largest_grids(torch):
@@ -181,7 +194,7 @@ def test_largest_grids(torch):
             x, w, dy = synth.random_inputs(layer, 2700 + i)
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
             say(f"    grid {plan.fft} kept {plan.kept}/{plan.total}; rel err {errs}")
             assert max(errs) <= TOL, errs
 
@@ -203,7 +216,7 @@ def test_1d_long_sequences(torch):
         x, w, dy = synth.random_inputs(layer, 900 + i)
         y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
         ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
-        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
         say(f"    rel err {errs}")
         assert max(errs) <= TOL
 
@@ -223,7 +236,7 @@ def test_1d_many_series(torch):
         x, w, dy = synth.random_inputs(layer, 1300 + i)
         y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
         ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
         say(f"    rel err {errs}")
         assert max(errs) <= TOL
 
@@ -251,7 +264,7 @@ def test_2d_fast_grids(torch):
             x, w, dy = synth.random_inputs(layer, 77)
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy, fft=fft)
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy, fft)
-            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
             assert max(errs) <= TOL, errs
 
 
@@ -274,10 +287,10 @@ def test_wgrad_paths(torch):
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
             # the oracle's forward of the 65536-filter case takes a minute: dw only there
             rdw = bo.backward_weight(x, dy, layer.K, layer.pad, c, None)
-            errs = [rel(dw, rdw)]
+            errs = [err(dw, rdw)]
             if layer.C_in * layer.C_out < 65536:
                 ry, rdx, _ = oracle_passes(layer, c, x, w, dy)
-                errs += [rel(y, ry), rel(dx, rdx)]
+                errs += [err(y, ry), err(dx, rdx)]
             say(f"    rel err {errs}")
             assert max(errs) <= TOL, errs
 
@@ -300,7 +313,7 @@ def test_thin_contractions(torch):
             x, w, dy = synth.random_inputs(layer, 1700 + i)
             y, dx, dw, plan, _ = gpu_passes(torch, layer, c, x, w, dy)
             ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-            errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+            errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
             say(f"    rel err {errs}")
             assert max(errs) <= TOL, errs
 
@@ -541,7 +554,7 @@ def test_fused_small_forward(torch):
             y, dx, dw, plan, ws = gpu_passes(torch, layer, c, x, w, dy, desc_flags=blconv.BL_DESC_FUSED_FORWARD)
         names = [r[0] for r in prof.records()]
         ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
-        errs = (rel(y, ry), rel(dx, rdx), rel(dw, rdw))
+        errs = (err(y, ry), err(dx, rdx), err(dw, rdw))
         say(f"    rel err {errs}; kernels {sorted(set(names))}")
         assert "small_fwd" in names and "contract_fwd" not in names
         assert all(np.isfinite(a).all() for a in (y, dx, dw))
