@@ -2,18 +2,30 @@
 
 One step = forward + grad-input + grad-weight (with map reuse) of every layer
 of the workload at compression rate c, on synthetic inputs already resident
-in HBM.  Default workload: the 3-layer FCN time-series stack (batch 64,
-length 512; channels 1->128->256->128, filters 8/5/3, 'same' padding), c = 0.5.
+in HBM.  Default workload: the ResNet-18-shaped stack of 3x3 layers at CIFAR
+resolution (batch 128; 64->64 @32x32, 128->128 @16x16, 256->256 @8x8,
+512->512 @4x4; padding 1), c = 0.5, plus the per-rate sweep c in
+{0, 0.25, 0.5, 0.75}.  The 1-D FCN time-series stack is timed as an extra
+workload beside it.
 
-Kernels are launched from the host every step; with --graph each layer's
-three passes are captured once in a HIP graph and replayed instead (on this
-stack the replays measured slower than the direct launches).
+Timing: W untimed warm-up steps, then K timed steps between two device
+synchronisations (HIP events on the stream the kernels run on); ms_per_step
+is the mean over the K steps and the median of the per-step times is reported
+beside it.  Then the same K steps run again with the library stamping every
+kernel's own start and end (hipExtLaunchKernelGGL with two events on the
+kernel's stream).  Those events lengthen the gaps between kernels, so they
+are kept out of the headline steps; they give the per-kernel averages (which
+agree with rocprofv3's kernel trace) and the roofline of the dominant kernel:
+  * FFT stages (spectra of x, dy and w, the inverse transforms, the
+    weight-gradient inverse DFT and the partial-sum passes): algorithmic
+    bytes / time against 8 TB/s HBM;
+  * channel contractions: algorithmic flops (8 per complex multiply-add) /
+    time against 157.3 TFLOP/s fp32 MFMA where their intensity is above the
+    ridge (19.7 flop/B), else bytes against HBM.
 
 Prints ONE JSON line: value = TFLOP-equiv/s, where the equivalent work of a
-layer is that of the direct convolution, 3 passes x 2 N C_in C_out Lo K^d
-flops.  Also reported: ms per layer for every c of the workload, the
-roofline of the dominant kernel (per-launch HIP events inside the library)
-and the fp64 CPU oracle timed on a bounded sample (cpu_baseline).
+layer is that of the direct convolution, 3 passes x 2 N C_in C_out Ho Wo K^d
+flops.  `cpu_baseline` is the fp64 CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -30,30 +42,27 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 MFMA_F32_PEAK_TF = 157.3   # MI355X dense fp32 matrix, TFLOP/s
-# fp32 vector arithmetic without packed math (the build disables it):
-# 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz
-VALU_F32_PEAK_TF = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 RIDGE = MFMA_F32_PEAK_TF * 1e12 / (HBM_PEAK_GBS * 1e9)
-VALU_RIDGE = VALU_F32_PEAK_TF * 1e12 / (HBM_PEAK_GBS * 1e9)
 
 
 def bound_of(name, nbytes, nflops):
-    """Roofline that applies to a kernel: its arithmetic unit when the launch's
-    algorithmic intensity is above that unit's ridge, else HBM."""
+    """Roofline of a kernel: fp32 MFMA for a channel contraction whose
+    algorithmic intensity is above the ridge, else HBM (every transform,
+    inverse DFT and partial-sum pass is a memory-bound stage)."""
     if nflops and name.startswith("contract") and nflops / nbytes > RIDGE:
         return "mfma", MFMA_F32_PEAK_TF
-    if nflops and name.startswith("spec_") and nflops / nbytes > VALU_RIDGE:
-        return "alu", VALU_F32_PEAK_TF
     return "hbm", HBM_PEAK_GBS
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index (1..5)")
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=3, help="workload index (1..5)")
     ap.add_argument("--c", type=float, default=0.5, help="compression rate of the headline value")
+    ap.add_argument("--extra-config", type=int, default=2,
+                    help="a second workload timed at the same rate beside the headline (0: none)")
     ap.add_argument("--no-sweep", action="store_true", help="skip the per-c sweep")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the bfloat16-spectra variant of the headline workload")
@@ -103,9 +112,9 @@ def capture(torch, layers):
 
 
 def time_steps(torch, layers, steps, warmup, graphs=None):
-    """Median-free whole-loop timing: ms per step and ms per layer (events between
-    layers).  With `graphs` (from capture) each layer's passes are replayed from
-    its graph instead of launched one by one."""
+    """W warm-up steps, then `steps` timed steps between two synchronisations.
+    Returns (mean ms per step, median ms per step, median ms per layer, wall
+    seconds).  Events on the current stream bracket every step and layer."""
     run = [g.replay for g in graphs] if graphs else [L.step for L in layers]
     for _ in range(warmup):
         for r in run:
@@ -114,6 +123,9 @@ def time_steps(torch, layers, steps, warmup, graphs=None):
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(layers) + 1)] for _ in range(steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
+    # a short spin kernel before and after the timed steps (outside the
+    # events) marks them in a profiler's kernel trace
+    torch.cuda._sleep(1000)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record()
@@ -125,23 +137,42 @@ def time_steps(torch, layers, steps, warmup, graphs=None):
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    torch.cuda._sleep(1000)
+    torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
+    per_step = [ev[s][0].elapsed_time(ev[s][-1]) for s in range(steps)]
     per_layer = [float(np.median([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)]))
                  for i in range(len(layers))]
-    return total_ms / steps, per_layer, wall
+    return total_ms / steps, float(np.median(per_step)), per_layer, wall
 
 
-def roofline(torch, blconv, layers, steps):
-    """Per-kernel HIP-event timing inside the library over `steps` steps."""
+def profile_steps(torch, blconv, layers, steps):
+    """The same steps again with the library stamping every kernel's own start
+    and end (two HIP events per launch on the stream it runs on).  The events
+    add gaps between kernels (the step takes longer), not time inside them.
+    Returns (all records, records per layer)."""
     prof = blconv.Profile(capacity=64 * steps * len(layers))
+    lib = blconv.load()
+    bounds = []
     torch.cuda.synchronize()
     with prof:
         for _ in range(steps):
-            for L in layers:
+            for i, L in enumerate(layers):
+                a = lib.bl_profile_count()
                 L.step()
+                bounds.append((i, a, lib.bl_profile_count()))
     torch.cuda.synchronize()
     recs = prof.records()
     prof.release()
+    per_layer = [[] for _ in layers]
+    for i, a, b in bounds:
+        per_layer[i].extend(recs[a:b])
+    return recs, per_layer
+
+
+def kernel_table(recs):
+    """Per library kernel name: launches, average duration, algorithmic rates
+    and the fraction of the roofline that applies to it."""
     agg = {}
     for name, ms, nb, nf in recs:
         a = agg.setdefault(name, [0, 0.0, 0.0, 0.0])
@@ -150,26 +181,31 @@ def roofline(torch, blconv, layers, steps):
     for name, (n, ms, nb, nf) in agg.items():
         s = ms * 1e-3
         bound, peak = bound_of(name, nb, nf)
+        gbs = nb / s / 1e9
+        contraction = name.startswith("contract") and nf > 0
+        tfs = nf / s / 1e12 if contraction else None
         kernels[name] = {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms,
-                         "GBps": nb / s / 1e9, "TFLOPs": nf / s / 1e12 if nf else None,
-                         "hbm_frac": nb / s / 1e9 / HBM_PEAK_GBS,
-                         "mfma_frac": (nf / s / 1e12 / MFMA_F32_PEAK_TF) if nf and name.startswith("contract") else None,
-                         "alu_frac": (nf / s / 1e12 / VALU_F32_PEAK_TF) if nf and name.startswith("spec_") else None,
-                         "ai": (nf / nb) if nf else None, "bound": bound}
+                         "bytes_per_launch": nb / n, "flops_per_launch": nf / n if contraction else None,
+                         "GBps": gbs, "TFLOPs": tfs, "ai": (nf / nb) if contraction else None, "bound": bound,
+                         "frac": (tfs if bound == "mfma" else gbs) / peak}
+    return agg, kernels
+
+
+def roofline(agg):
+    """Roofline object of the dominant kernel (largest total time)."""
     dom = max(agg, key=lambda k: agg[k][1])
     n, ms, nb, nf = agg[dom]
     s = ms * 1e-3
     bound, peak = bound_of(dom, nb, nf)
     if bound == "hbm":
-        roof = {"kernel": dom, "bound": "hbm", "achieved": nb / s / 1e9, "peak": HBM_PEAK_GBS,
+        return {"kernel": dom, "bound": "hbm", "achieved": nb / s / 1e9, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": nb / s / 1e9 / HBM_PEAK_GBS, "traffic": None,
                 "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_bytes": nb / n}
-    else:
-        roof = {"kernel": dom, "bound": bound, "achieved": nf / s / 1e12, "peak": peak,
-                "unit": "TFLOP/s", "frac": nf / s / 1e12 / peak, "traffic": None,
-                "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_flops": nf / n,
-                "per_launch_bytes": nb / n, "hbm_GBps": nb / s / 1e9}
-    return roof, kernels
+    return {"kernel": dom, "bound": "mfma", "achieved": nf / s / 1e12, "peak": MFMA_F32_PEAK_TF,
+            "unit": "TFLOP/s", "frac": nf / s / 1e12 / MFMA_F32_PEAK_TF, "traffic": None,
+            "avg_launch_us": 1e3 * ms / n, "launches": n, "per_launch_flops": nf / n,
+            "per_launch_bytes": nb / n, "hbm_GBps": nb / s / 1e9,
+            "flop_count": "algorithmic: 8 real flops per complex multiply-add"}
 
 
 KERNEL_SOURCES = {"spec_fwd_1d": "bluestein.hip", "spec_inv_1d": "bluestein.hip", "spec_fwd_2d": "fft2d.hip",
@@ -184,7 +220,7 @@ def measured_traffic(kernel, workload):
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
         return None
-    t = json.load(open(path)).get(kernel, {})
+    t = json.load(open(path)).get(f"{kernel} @ {workload}", {})
     src = os.path.join(ROOT, "paper_1911_09287_amd", "csrc", KERNEL_SOURCES[kernel])
     if t.get("kernel") != kernel or t.get("workload") != workload or not os.path.exists(src):
         return None
@@ -255,12 +291,14 @@ def main():
         torch.mul(src, 1.0, out=dst)  # reads 4n bytes, writes 4n bytes
         torch.cuda.synchronize()
         del src, dst
-    cfg = synth.WORKLOADS[args.config]
-    arrays = [synth.layer_inputs(args.config, i) for i in range(len(cfg.layers))]
-    eq_flops = sum(3 * L.direct_flops() for L in cfg.layers)
 
-    def build(c, desc_flags=0):
-        return [Layer(torch, blconv, L, a, c, dev, desc_flags) for L, a in zip(cfg.layers, arrays)]
+    def workload(ci):
+        cf = synth.WORKLOADS[ci]
+        arr = [synth.layer_inputs(ci, i) for i in range(len(cf.layers))]
+        return cf, arr, sum(3 * L.direct_flops() for L in cf.layers)
+
+    def build(cf, arr, c, desc_flags=0):
+        return [Layer(torch, blconv, L, a, c, dev, desc_flags) for L, a in zip(cf.layers, arr)]
 
     def graphs_for(Ls):
         if not args.graph:
@@ -270,34 +308,61 @@ def main():
         torch.cuda.synchronize()
         return capture(torch, Ls)
 
-    layers = build(args.c)
+    cfg, arrays, eq_flops = workload(args.config)
+    layers = build(cfg, arrays, args.c)
     graphs = graphs_for(layers)
-    ms, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup, graphs)
-    roof, kernels = roofline(torch, blconv, layers, max(1, min(args.steps, 10)))
+    ms, med, per_layer, wall = time_steps(torch, layers, args.steps, args.warmup, graphs)
+    value = eq_flops / (ms * 1e-3) / 1e12
+    # per-kernel durations: the same K steps again with kernel events
+    recs, recs_by_layer = profile_steps(torch, blconv, layers, args.steps)
+    agg, kernels = kernel_table(recs)
+    roof = roofline(agg)
     workload_key = f"config {args.config} c={args.c}"
     roof["traffic"] = measured_traffic(roof["kernel"], workload_key)
     if roof["traffic"] is not None:
         roof["traffic_over_algorithmic"] = roof["traffic"] / roof["per_launch_bytes"]
-    value = eq_flops / (ms * 1e-3) / 1e12
+    by_layer = {}
+    for L, rl in zip(layers, recs_by_layer):
+        _, ks = kernel_table(rl)
+        by_layer[L.layer.name] = {k: {"avg_us": round(v["avg_us"], 3), "frac": round(v["frac"], 4),
+                                      "bound": v["bound"]} for k, v in ks.items()}
 
     per_c = []
     if not args.no_sweep:
         for c in cfg.rates:
-            Ls = layers if c == args.c else build(c)
-            m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs if c == args.c else graphs_for(Ls))
-            per_c.append({"c": c, "c_eff": [L.plan.c_eff for L in Ls], "ms_per_step": m,
-                          "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12})
+            Ls = layers if c == args.c else build(cfg, arrays, c)
+            m, md, pl, _ = time_steps(torch, Ls, args.steps, args.warmup,
+                                      graphs if c == args.c else graphs_for(Ls))
+            entry = {"c": c, "c_eff": [L.plan.c_eff for L in Ls], "ms_per_step": m, "ms_per_step_median": md,
+                     "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12}
+            rc, _ = profile_steps(torch, blconv, Ls, min(args.steps, 10))
+            _, ks = kernel_table(rc)
+            entry["kernel_frac"] = {k: round(v["frac"], 4) for k, v in ks.items()}
+            per_c.append(entry)
             del Ls
 
     # the same workload with the saved spectra in bfloat16 (reduced precision
     # combined with band-limiting); reported beside the fp32 headline, not as it
     variants = {}
     if not args.no_variants:
-        Ls = build(args.c, blconv.BL_DESC_BF16_SPECTRA)
-        m, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs_for(Ls))
+        Ls = build(cfg, arrays, args.c, blconv.BL_DESC_BF16_SPECTRA)
+        m, md, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs_for(Ls))
         variants["bf16_spectra"] = {"dtype": "bf16 spectra, fp32 accumulation", "c": args.c, "ms_per_step": m,
                                     "ms_per_layer": pl, "tflop_equiv_s": eq_flops / (m * 1e-3) / 1e12,
                                     "speedup_vs_f32": ms / m}
+        del Ls
+
+    extra = None
+    if args.extra_config and args.extra_config != args.config:
+        ecf, earr, eflops = workload(args.extra_config)
+        Ls = build(ecf, earr, args.c)
+        m, md, pl, _ = time_steps(torch, Ls, args.steps, args.warmup, graphs_for(Ls))
+        extra = {"workload": ecf.name, "config_index": args.extra_config, "c": args.c, "ms_per_step": m,
+                 "ms_per_step_median": md, "ms_per_layer": pl, "tflop_equiv_s": eflops / (m * 1e-3) / 1e12}
+        rc, _ = profile_steps(torch, blconv, Ls, args.steps)
+        eagg, eks = kernel_table(rc)
+        extra["roofline"] = roofline(eagg)
+        extra["kernels"] = eks
         del Ls
 
     cpu = None
@@ -312,6 +377,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "ms_per_step_median": med,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -324,8 +390,10 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "kernels_by_layer": by_layer,
         "per_c": per_c,
         "variants": variants,
+        "extra_workload": extra,
         "wall_s_timed": wall,
         "launch": "hip_graph per layer" if args.graph else "eager",
     }
@@ -334,15 +402,16 @@ def main():
     if args.table:
         with open(args.table, "w") as fh:
             for ci in sorted(synth.WORKLOADS):
-                cf = synth.WORKLOADS[ci]
-                arr = [synth.layer_inputs(ci, i) for i in range(len(cf.layers))]
+                cf, arr, _ = workload(ci)
                 for c in cf.rates:
-                    for li, (L, a) in enumerate(zip(cf.layers, arr)):
+                    for L, a in zip(cf.layers, arr):
                         Ls = [Layer(torch, blconv, L, a, c, dev)]
-                        m, _, _ = time_steps(torch, Ls, args.steps, args.warmup)
-                        r, ks = roofline(torch, blconv, Ls, 5)
+                        m, md, _, _ = time_steps(torch, Ls, args.steps, args.warmup)
+                        rc, _ = profile_steps(torch, blconv, Ls, min(args.steps, 10))
+                        _, ks = kernel_table(rc)
                         fh.write(json.dumps({"config": ci, "layer": L.name, "c": c, "c_eff": Ls[0].plan.c_eff,
-                                             "ms": m, "tflop_equiv_s": 3 * L.direct_flops() / (m * 1e-3) / 1e12,
+                                             "ms": m, "ms_median": md,
+                                             "tflop_equiv_s": 3 * L.direct_flops() / (m * 1e-3) / 1e12,
                                              "kernels": ks}) + "\n")
                         fh.flush()
                         del Ls

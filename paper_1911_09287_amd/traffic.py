@@ -44,6 +44,8 @@ def main():
     ap.add_argument("--write", required=True)
     ap.add_argument("--kernel", required=True, help="substring of the kernel symbol")
     ap.add_argument("--match", default="", help="further substring (e.g. template arguments)")
+    ap.add_argument("--regex", default="", help="or: a regular expression the kernel symbol must match "
+                                                 "(several instantiations under one library name)")
     ap.add_argument("--name", required=True, help="the library's name for the kernel")
     ap.add_argument("--source", required=True)
     ap.add_argument("--copy-mib", type=int, required=True)
@@ -55,8 +57,8 @@ def main():
     f, w = read(a.fetch), read(a.write)
     copy_bytes = a.copy_mib * (1 << 20)
 
-    def pick(rows, sub, extra=""):
-        return [v for (n, v) in rows.values() if sub in n and extra in n]
+    def pick(rows, sub, extra="", rx=""):
+        return [v for (n, v) in rows.values() if sub in n and extra in n and (not rx or re.search(rx, n))]
 
     cf, cw = pick(f, a.copy_kernel), pick(w, a.copy_kernel)
     if not cf or not cw:
@@ -64,12 +66,12 @@ def main():
     # the largest dispatch of the copy kernel is the calibration copy
     read_scale = copy_bytes / (max(cf) * 1024.0)
     write_scale = copy_bytes / (max(cw) * 1024.0)
-    kf, kw = pick(f, a.kernel, a.match), pick(w, a.kernel, a.match)
+    kf, kw = pick(f, a.kernel, a.match, a.regex), pick(w, a.kernel, a.match, a.regex)
     if not kf or not kw:
         raise SystemExit("kernel not found")
     fetch = sum(kf) / len(kf) * 1024.0 * read_scale
     write = sum(kw) / len(kw) * 1024.0 * write_scale
-    out = {"kernel": a.name, "symbol": a.kernel + a.match, "workload": a.workload,
+    out = {"kernel": a.name, "symbol": a.regex or (a.kernel + a.match), "workload": a.workload,
            "source": a.source, "source_sha256_16": source_hash(a.source),
            "dispatches": len(kf), "copy_mib": a.copy_mib,
            "read_scale": read_scale, "write_scale": write_scale,
@@ -78,9 +80,8 @@ def main():
     # the file holds one entry per kernel name; other kernels' entries are kept
     os.makedirs(os.path.dirname(os.path.abspath(a.out)), exist_ok=True)
     table = json.load(open(a.out)) if os.path.exists(a.out) else {}
-    if "kernel" in table:  # a single-entry file
-        table = {table["kernel"]: table}
-    table[a.name] = out
+    # one entry per (library kernel name, workload)
+    table[f"{a.name} @ {a.workload}"] = out
     json.dump(table, open(a.out, "w"), indent=1, sort_keys=True)
     print(json.dumps(out))
 

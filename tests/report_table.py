@@ -29,7 +29,7 @@ import numpy as np  # noqa: E402
 import bench  # noqa: E402
 from oracle import bl_oracle as bo  # noqa: E402
 from paper_1911_09287_amd import blconv, synth  # noqa: E402
-from test_parity_gpu import gpu_passes, oracle_passes, rel  # noqa: E402
+from test_parity_gpu import elem, gpu_passes, oracle_passes, rel  # noqa: E402
 
 SPECTRAL = ("spec_", "wgrad_idft", "wgrad_reduce")
 
@@ -88,8 +88,9 @@ def main():
                 for c in cfg.rates:
                     print(f"[table] config {ci} layer {layer.name} c={c}", flush=True)
                     L = bench.Layer(torch, blconv, layer, (x, w, dy), c, dev)
-                    ms, _, _ = bench.time_steps(torch, [L], args.steps, args.warmup)
-                    _, ks = bench.roofline(torch, blconv, [L], 5)
+                    ms, _, _, _ = bench.time_steps(torch, [L], args.steps, args.warmup)
+                    recs, _ = bench.profile_steps(torch, blconv, [L], 5)
+                    _, ks = bench.kernel_table(recs)
                     fft_hbm, (cbound, cfrac) = stage_fracs(ks)
                     c_eff = L.plan.c_eff
                     del L
@@ -102,7 +103,8 @@ def main():
                     row = {"config": ci, "layer": layer.name, "c": c, "c_eff": c_eff, "ms": ms,
                            "tflop_equiv_s": 3 * layer.direct_flops() / (ms * 1e-3) / 1e12,
                            "fft_hbm_frac": fft_hbm, "contract_bound": cbound, "contract_frac": cfrac,
-                           "rel_err": [rel(gy, ry), rel(gdx, rdx), rel(gdw, rdw)], "mask_exact": mask_ok,
+                           "rel_err": [rel(gy, ry), rel(gdx, rdx), rel(gdw, rdw)],
+                           "elem_err": [elem(gy, ry), elem(gdx, rdx), elem(gdw, rdw)], "mask_exact": mask_ok,
                            "oracle_cpu_ms": 1e3 * t_cpu, "oracle_cores": cores, "oracle_blas_threads": blas_threads(),
                            "kernels": ks}
                     fh.write(json.dumps(row) + "\n")
