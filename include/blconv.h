@@ -81,7 +81,7 @@ typedef enum {
   BL_OK = 0,
   BL_ERR_INVALID_ARG = 1,         /* null pointer, non-positive size, c outside [0,1), grid too small */
   BL_ERR_UNSUPPORTED = 2,         /* valid but outside what this library implements (e.g. K > 8) */
-  BL_ERR_WORKSPACE_TOO_SMALL = 3, /* reserved for callers that check bl_conv_workspace_size */
+  BL_ERR_WORKSPACE_TOO_SMALL = 3, /* bl_conv_forward_noalloc: the plan's spectra exceed its static array */
   BL_ERR_HIP = 4,                 /* a HIP launch or runtime call failed */
   BL_ERR_OOM = 5                  /* host or device allocation failed */
 } bl_status_t;
@@ -187,6 +187,30 @@ bl_status_t bl_conv_backward_input(bl_conv_plan_t plan, const float* dy, const f
  * cropped to the K x K filter support.  Writes X and DY to ws. */
 bl_status_t bl_conv_backward_weight(bl_conv_plan_t plan, const float* x, const float* dy, float* dw,
                                     void* ws, unsigned flags, void* stream);
+
+/* Forward pass that allocates nothing, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  It computes what bl_conv_forward computes (flags 0:
+ * X and W are always computed from x and w) but keeps the input, filter and
+ * output spectra (and the contraction's partial sums) in one static device
+ * array of 64 MiB that the library holds on each GPU it runs on until the
+ * process ends, instead of a caller workspace; it calls no hipMalloc or
+ * hipFree and uses no plan table (the chirp-z 1-D transforms are replaced by
+ * the direct DFT, and the filter transform computes its roots of unity), so
+ * even a plan's first call allocates nothing.  The array is located once per
+ * device (hipGetSymbolAddress), on the first call on that device.
+ *
+ * Limit: kept * (N * C_in + C_in * C_out) stored elements (8 bytes, 4 with
+ * BL_DESC_BF16_SPECTRA) plus kept * N * C_out * 8 bytes of output spectrum
+ * (plus the contraction's k-split partials where the plan's tiling splits k),
+ * each rounded up to 256 bytes, must fit 64 MiB; larger plans return
+ * BL_ERR_WORKSPACE_TOO_SMALL before anything is enqueued.  Every call on a GPU
+ * shares that GPU's array and leaves its spectra there: calls that overlap on
+ * one GPU (other streams, other threads) race and give wrong results, so
+ * serialise them.  Nothing in the array needs to start at zero: each call
+ * writes every part it reads.  Errors as bl_conv_forward; x, w, y may not be
+ * NULL.  The spectra it leaves are not accessible to the caller. */
+bl_status_t bl_conv_forward_noalloc(bl_conv_plan_t plan, const float* x, const float* w, float* y, void* stream);
 
 /* Energy-based (adaptive) compression, coarse-grained (Sec. 4.1; supplementary
  * "Compression Based on Preserved Energy"): the band is grown from the DC

@@ -34,6 +34,7 @@ EXPORTED = (
     "bl_conv_backward_input", "bl_conv_backward_weight", "bl_status_string", "bl_profile_begin",
     "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release", "bl_conv_input_energy",
     "bl_conv_rate_for_energy", "bl_conv_zero_smallest", "bl_conv_fine_band_for_energy", "bl_conv_zero_bins",
+    "bl_conv_forward_noalloc",
 )
 
 
@@ -78,6 +79,7 @@ def load():
     lib.bl_conv_workspace_layout.argtypes = [P, ctypes.POINTER(S), ctypes.POINTER(S), ctypes.POINTER(S)]
     for name in ("bl_conv_forward", "bl_conv_backward_input", "bl_conv_backward_weight"):
         getattr(lib, name).argtypes = [P, P, P, P, P, U, P]
+    lib.bl_conv_forward_noalloc.argtypes = [P, P, P, P, P]
     lib.bl_conv_input_energy.argtypes = [P, P, P, U, P, P]
     lib.bl_conv_rate_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D)]
     lib.bl_conv_zero_smallest.argtypes = [P, P, P, U, ctypes.c_longlong, U, P]
@@ -219,6 +221,13 @@ class Plan:
         _check("bl_conv_forward", self._lib.bl_conv_forward(
             self._h, self._ptr(x, self.x_shape(), "x"), self._ptr(w, self.w_shape(), "w"),
             self._ptr(y, self.y_shape(), "y"), self._ws(ws), flags, self._stream(stream)))
+
+    def forward_noalloc(self, x, w, y, stream=None):
+        """Forward pass on the library's static device array (no workspace, no
+        allocation); calls on one GPU must not overlap."""
+        _check("bl_conv_forward_noalloc", self._lib.bl_conv_forward_noalloc(
+            self._h, self._ptr(x, self.x_shape(), "x"), self._ptr(w, self.w_shape(), "w"),
+            self._ptr(y, self.y_shape(), "y"), self._stream(stream)))
 
     def backward_input(self, dy, w, dx, ws, flags=0, stream=None):
         _check("bl_conv_backward_input", self._lib.bl_conv_backward_input(

@@ -1,5 +1,6 @@
 // C ABI compute entry points, stage dispatch and per-kernel timing.
 #include <mutex>
+#include <utility>
 #include <vector>
 
 #include "common.hpp"
@@ -139,6 +140,92 @@ extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x,
     BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
   BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, ws_at(ws, p->off_CPart), s));
   return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
+}
+
+// ---------------------------------------------------------------------------
+// Forward pass without any allocation: the spectra live in a fixed static
+// device array instead of a caller workspace.
+// ---------------------------------------------------------------------------
+constexpr size_t kNoAllocBytes = (size_t)64 << 20;  // the array's size on each device
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+namespace blc {
+namespace {
+
+// Address of `scratch` on the current device.  In host code the array's name
+// is a host-side stand-in, not a device address: only the pointer
+// hipGetSymbolAddress returns (looked up once per device, with that device
+// current) is ever passed to kernels.
+std::mutex g_scratch_mu;
+std::vector<std::pair<int, void*>> g_scratch_at;
+
+bl_status_t scratch_on_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BL_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  for (const auto& e : g_scratch_at)
+    if (e.first == dev) {
+      *out = e.second;
+      return BL_OK;
+    }
+  void* ptr = nullptr;
+  if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return BL_ERR_HIP;
+  g_scratch_at.emplace_back(dev, ptr);
+  *out = ptr;
+  return BL_OK;
+}
+
+inline size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
+// The transforms that need no plan table: the 2-D mixed-radix kernels where
+// the grid has them, else the direct DFT (whose blocks compute their roots of
+// unity).  1-D plans take the direct DFT (the chirp-z kernels use tables).
+bl_status_t spec_fwd_no_tables(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
+                               int oi, int oj, hipStream_t s) {
+  if (p->Lh != 1) {
+    const bl_status_t st = launch_fft2_fwd(p, in, out, P, Hin, Win, oi, oj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
+  return launch_spec_fwd_direct(p, in, out, P, Hin, Win, oi, oj, s);
+}
+
+bl_status_t spec_inv_no_tables(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW,
+                               int ci, int cj, hipStream_t s) {
+  if (p->Lh != 1) {
+    const bl_status_t st = launch_fft2_inv(p, in, out, P, OH, OW, ci, cj, s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
+  return launch_spec_inv_direct(p, in, out, P, OH, OW, ci, cj, s);
+}
+
+}  // namespace
+}  // namespace blc
+
+extern "C" bl_status_t bl_conv_forward_noalloc(bl_conv_plan_t p, const float* x, const float* w, float* y,
+                                               void* stream) {
+  if (!p || !x || !w || !y) return BL_ERR_INVALID_ARG;
+  // layout inside the array: X, W, the output spectrum, the k-split partials
+  const size_t sb = p->bf16 ? 4 : 8, B = (size_t)p->kept;
+  const size_t nX = up256(B * p->N * p->Cin * sb), nW = up256(B * p->Cin * p->Cout * sb);
+  const size_t nT = up256(B * p->N * p->Cout * 8);
+  const size_t nP = p->ct[0].splits > 1 ? up256((size_t)p->ct[0].splits * B * p->N * p->Cout * 8) : 0;
+  if (nX + nW + nT + nP > ::kNoAllocBytes) return BL_ERR_WORKSPACE_TOO_SMALL;
+  void* base = nullptr;
+  BL_TRY(scratch_on_current_device(&base));
+  char* b = static_cast<char*>(base);
+  void* X = b;
+  void* Wf = b + nX;
+  float2* T = reinterpret_cast<float2*>(b + nX + nW);
+  float2* part = reinterpret_cast<float2*>(b + nX + nW + nT);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  BL_TRY(launch_spec_filt(p, w, Wf, s, /*use_table=*/false));
+  if (p->fused_fwd && small_fwd_eligible(p)) {
+    const bl_status_t st = launch_small_fwd(p, x, static_cast<const float2*>(Wf), y, static_cast<float2*>(X), s);
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
+  BL_TRY(spec_fwd_no_tables(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, part, s));
+  return spec_inv_no_tables(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
 }
 
 // ---------------------------------------------------------------------------

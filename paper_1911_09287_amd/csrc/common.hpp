@@ -87,8 +87,11 @@ bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, void* out,
 // window that starts at (ci, cj), scaled by 1 / (Lh Lw).
 bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s);
-// Filter w [F][C][Kh][Kw] -> W[b][c][f] (stored-spectrum type).
-bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s);
+// Filter w [F][C][Kh][Kw] -> W[b][c][f] (stored-spectrum type).  The roots of
+// unity come from the plan's device table (built on first use), or with
+// use_table = false are computed by each block (no table, no allocation).
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s,
+                             bool use_table = true);
 // DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats.
 bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s);
 

@@ -208,11 +208,16 @@ template <int KH, int KW, typename S>
 __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, const float2* __restrict__ roots,
                                                         S* __restrict__ out, FiltGeom g) {
   // roots: e^{-2 pi i k / Lh} (k < Lh) then e^{-2 pi i k / Lw} (k < Lw), from
-  // a table built once per plan
+  // a table built once per plan, or (roots == nullptr) computed here
   extern __shared__ float2 smem[];
   float2* twh = smem;
   float2* tww = twh + g.Lh;
-  for (int k = threadIdx.x; k < g.Lh + g.Lw; k += blockDim.x) smem[k] = roots[k];
+  if (roots) {
+    for (int k = threadIdx.x; k < g.Lh + g.Lw; k += blockDim.x) smem[k] = roots[k];
+  } else {
+    fill_roots(twh, g.Lh, -1.0);
+    fill_roots(tww, g.Lw, -1.0);
+  }
   __syncthreads();
   const long CF = (long)g.C * g.F;
   const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;  // q = c * F + f
@@ -648,12 +653,14 @@ void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
     }
 }
 
-bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s) {
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s, bool use_table) {
   FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
   const float2* roots = nullptr;
-  const std::vector<long> key{3, p->Lh, p->Lw};
-  const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_filt_roots(p, h); }, &roots);
-  if (ts != BL_OK) return ts;
+  if (use_table) {
+    const std::vector<long> key{3, p->Lh, p->Lw};
+    const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_filt_roots(p, h); }, &roots);
+    if (ts != BL_OK) return ts;
+  }
   const long CF = (long)p->Cin * p->Cout;
   const int B = p->R * p->V;
   const long xblocks = (CF + kThreads - 1) / kThreads;
