@@ -295,6 +295,45 @@ def test_wgrad_paths(torch):
             assert max(errs) <= TOL, errs
 
 
+def test_contraction_shapes(torch):
+    """The tiled contraction at edge shapes: ragged tiles in m, n and k; a
+    single bin with 2048 input channels (k split over many partial tiles,
+    summed in a fixed order); few bins with long k; an odd channel count (the
+    operands' 16-byte pairs do not align: the generic path); a 1-D layer.
+    Each twice in a row on one workspace: results equal run to run."""
+    cases = [
+        (synth.Layer("ragged", 2, 70, 66, 130, 6, 6, 3, (1, 1, 1, 1), "blur"), 0.0),
+        (synth.Layer("one_bin", 2, 64, 2048, 256, 1, 1, 1, (0, 0, 0, 0), "blur"), 0.0),
+        (synth.Layer("long_k", 2, 96, 640, 640, 2, 2, 1, (0, 0, 0, 0), "blur"), 0.0),
+        (synth.Layer("odd_k", 2, 64, 65, 64, 4, 4, 3, (1, 1, 1, 1), "blur"), 0.5),
+        (synth.Layer("one_d", 1, 64, 96, 192, 60, 1, 3, (1, 1), "walk"), 0.5),
+    ]
+    for i, (layer, c) in enumerate(cases):
+        say(f"[contraction] {layer.name} c={c}")
+        x, w, dy = synth.random_inputs(layer, 1900 + i)
+        plan = blconv.plan_for_layer(layer, c)
+        dev = torch.device("cuda:0")
+        ws = plan.workspace(dev)
+        ws.fill_(0xFF)
+        xt, wt, dyt = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        outs = []
+        for rep in range(2):
+            y = torch.full(plan.y_shape(), float("nan"), device=dev)
+            dx = torch.full(plan.x_shape(), float("nan"), device=dev)
+            dw = torch.full(plan.w_shape(), float("nan"), device=dev)
+            plan.forward(xt, wt, y, ws)
+            plan.backward_input(dyt, wt, dx, ws, flags=blconv.BL_REUSE_W)
+            plan.backward_weight(xt, dyt, dw, ws, flags=blconv.BL_REUSE_X | blconv.BL_REUSE_DY)
+            torch.cuda.synchronize()
+            outs.append([t.cpu().numpy() for t in (y, dx, dw)])
+        for a, b in zip(*outs):
+            assert np.array_equal(a, b)
+        ry, rdx, rdw = oracle_passes(layer, c, x, w, dy)
+        errs = (err(outs[0][0], ry), err(outs[0][1], rdx), err(outs[0][2], rdw))
+        say(f"    err {errs}")
+        assert max(errs) <= TOL, errs
+
+
 def test_thin_contractions(torch):
     """Layers where a contraction size (batch, input or output channels) is at
     most 8, which run the memory-bound vector-ALU contraction: lanes over
