@@ -191,12 +191,6 @@ __global__ __launch_bounds__(kThreads) void k_spec_inv(const float2* __restrict_
 // spec_filt: w [F][C][Kh][Kw] -> W[b][c][f] at the kept bins (origin placement).
 // One thread per (c, f) pair; blockIdx.y strides over chunks of bins.
 // ---------------------------------------------------------------------------
-// Channel tile of the weight-gradient inverse DFT: TC input x 256 / TC output
-// channels.  Rows wider than 256 output channels take 32-channel spans of 8
-// input channels, so that the gradient rows dw[f][c0 .. c0 + 8][taps] are
-// written 8 x taps floats at a time; otherwise a block spans whole rows of
-// one input channel.
-inline int chan_tile(int taps, int F) { return (taps <= 16 && F > 256) ? 8 : 1; }
 
 struct FiltGeom {
   int F, C, Kh, Kw;
@@ -280,19 +274,22 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
 // wgrad_idft: DW[b][q] (q = c * F + f) -> dw[f][c][t], t = (a, b') < Kh x Kw:
 //   dw = sum over kept bins (u, v) of Re(DW[u, v] * E[b][t]),
 //   E[b][t] = h_v e^{+2 pi i (u a / Lh + v b' / Lw)} / (Lh Lw)
-// (the c2r inverse restricted to the filter support).  The bins are split
-// into `chunks` slices (blockIdx.y); each block copies E for its slice from a
-// table built once per plan into LDS and reduces 256 (c, f) pairs over it:
-// consecutive q when TC = 1, a TC x TF tile otherwise.  With more than one
-// slice the partial sums go to part[chunk][t][q] (contiguous in q) and
-// k_wgrad_reduce adds them in a fixed order, so results do not depend on
-// scheduling; with one slice and TC > 1 the results go through LDS so that
-// each row dw[f][c0 .. c0 + TC][:] is written contiguously.
+// (the c2r inverse restricted to the filter support), E tabulated once per
+// plan.  Results do not depend on scheduling: every sum is taken in a fixed
+// order.
 // ---------------------------------------------------------------------------
+// Channel tile of the weight-gradient inverse DFT: TC input x 256 / TC output
+// channels.  Rows wider than 256 output channels take 32-channel spans of 8
+// input channels, so that the gradient rows dw[f][c0 .. c0 + 8][taps] are
+// written 8 x taps floats at a time; otherwise a block spans whole rows of
+// one input channel.
+inline int chan_tile(int taps, int F) { return (taps <= 16 && F > 256) ? 8 : 1; }
+
 struct WgradGeom {
   int F, C, Kh, Kw, T;
   int Lh, Lw, r_h, R, V;
   int bins_per_chunk, chunks;
+  int tiles_f;  // 16-filter tiles along F (k_wgrad_tile)
 };
 
 template <int TMAX, int TC>
@@ -450,6 +447,79 @@ __global__ __launch_bounds__(64 * NW) void k_wgrad_wide(const float2* __restrict
       for (int w = 1; w < NW; ++w) sum += red[w][lane][t];
       if (t < g.T) o[t] = sum;
     }
+  }
+}
+
+// Layers with many channel pairs (at least 128 tiles of 16 x 16): a block
+// takes a tile of 16 input channels x 16 filters and all kept bins; its NG
+// groups of 256 threads (one pair (c, f) per thread) each sum a contiguous
+// part of the bins, reading DW[bin][c][f] as runs of 16 filters (128 bytes)
+// and E from LDS, 16 bins' loads in flight at a time.  The groups' sums are
+// added in a fixed order through LDS and written transposed, so that each
+// filter's row dw[f][c0 .. c0 + 16][:] is one contiguous run.
+template <int TMAX, int NG>
+__global__ __launch_bounds__(256 * NG) void k_wgrad_tile(const float2* __restrict__ DW, const float2* __restrict__ Et,
+                                                         float* __restrict__ out, WgradGeom g) {
+  extern __shared__ float2 smem2[];
+  float2* E = smem2;                                                 // [bins_per_chunk][TMAX], zero beyond T
+  float* red = reinterpret_cast<float*>(smem2 + (size_t)g.bins_per_chunk * TMAX);  // [NG][256][TMAX]
+  const int B = g.R * g.V;
+  const int b0 = blockIdx.y * g.bins_per_chunk;
+  const int nb = min(g.bins_per_chunk, B - b0);
+  const float2* Es = Et + (size_t)b0 * g.T;
+  for (int e = threadIdx.x; e < nb * TMAX; e += blockDim.x) {
+    const int bb = e / TMAX, t = e - bb * TMAX;
+    E[e] = t < g.T ? Es[bb * g.T + t] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  const size_t Q = (size_t)g.C * g.F;
+  const int c0 = (blockIdx.x / g.tiles_f) * 16, f0 = (blockIdx.x % g.tiles_f) * 16;
+  const int grp = threadIdx.x >> 8, pr = threadIdx.x & 255, cl = pr >> 4, fl = pr & 15;
+  const int c = c0 + cl, f = f0 + fl;
+  const bool valid = c < g.C && f < g.F;
+  const int bb0 = grp * nb / NG, bb1 = (grp + 1) * nb / NG;
+  float acc[TMAX];
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
+  const float2* src = DW + (size_t)b0 * Q + (valid ? (size_t)c * g.F + f : 0);
+  for (int bb = bb0; bb < bb1; bb += 16) {
+    float2 d[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) d[j] = src[(size_t)min(bb + j, bb1 - 1) * Q];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float2 dj = bb + j < bb1 ? d[j] : make_float2(0.f, 0.f);
+      const float2* Eb = E + min(bb + j, bb1 - 1) * TMAX;
+#pragma unroll
+      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) red[((size_t)grp * 256 + pr) * TMAX + t] = acc[t];
+  __syncthreads();
+  if (grp == 0) {
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t) {
+      float sum = red[pr * TMAX + t];
+#pragma unroll
+      for (int w = 1; w < NG; ++w) sum += red[((size_t)w * 256 + pr) * TMAX + t];
+      acc[t] = sum;
+    }
+  }
+  __syncthreads();
+  // transposed: filter fl's 16 channels x T taps contiguous
+  if (grp == 0) {
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t)
+      if (t < g.T) red[(fl * 16 + cl) * g.T + t] = acc[t];
+  }
+  __syncthreads();
+  float* o = out;
+  const int seg = 16 * g.T;
+  for (int e = threadIdx.x; e < 16 * seg; e += blockDim.x) {
+    const int ef = e / seg, r = e - ef * seg;
+    const int oc = c0 + r / g.T, of = f0 + ef;
+    if (oc < g.C && of < g.F) o[((size_t)of * g.C + c0) * g.T + r] = red[e];
   }
 }
 
@@ -687,7 +757,8 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
 }
 
 bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s) {
-  WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
+  WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0,
+              (p->Cout + 15) / 16};
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept;
   // one pass over all bins when there are at least 256 blocks of 64 pairs,
@@ -699,6 +770,34 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
   const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
   if (ts != BL_OK) return ts;
+  if (p->wg_groups > 0) {  // 16 x 16 channel tiles over all bins
+    const int tmax = wgrad_tmax(g.T), NG = p->wg_groups;
+    g.bins_per_chunk = B;
+    g.chunks = 1;
+    const size_t lds = (size_t)B * tmax * sizeof(float2) + (size_t)NG * 256 * tmax * sizeof(float);
+    const long tiles = (long)((p->Cin + 15) / 16) * g.tiles_f;
+    const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
+    bl_status_t st = BL_ERR_UNSUPPORTED;
+    auto go = [&](auto kern, int ng) {
+      if (lds > 64 * 1024) {
+        const bl_status_t at = lds_opt_in(reinterpret_cast<const void*>(kern), 160 * 1024);
+        if (at != BL_OK) return at;
+      }
+      return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+        hipExtLaunchKernelGGL(kern, dim3((unsigned)tiles), dim3(256 * ng), lds, s, e0, e1, 0, DW, Et, dw, g);
+      });
+    };
+#define BL_WG(TM)                                                                                            \
+  case TM:                                                                                                   \
+    st = NG == 4 ? go(k_wgrad_tile<TM, 4>, 4) : NG == 2 ? go(k_wgrad_tile<TM, 2>, 2) : go(k_wgrad_tile<TM, 1>, 1); \
+    break;
+    switch (tmax) {
+      BL_WG(1) BL_WG(2) BL_WG(3) BL_WG(4) BL_WG(5) BL_WG(6) BL_WG(7) BL_WG(8) BL_WG(9) BL_WG(16)
+      default: return BL_ERR_UNSUPPORTED;
+    }
+#undef BL_WG
+    return st;
+  }
   const int tmax_w = g.T <= 9 ? g.T : 16;
   if ((Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && g.T <= 16 &&
       (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&

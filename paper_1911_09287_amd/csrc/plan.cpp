@@ -129,6 +129,19 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
     const long chunks = (p->kept + per - 1) / per;
     p->wg_bins = (int)per;
     p->wg_chunks = (int)chunks;
+    // 128 to 511 tiles of 16 x 16 channel pairs: one pass over all bins with
+    // 2 or 4 groups of 256 threads per tile (k_wgrad_tile), at least 2048
+    // waves, the bins' weights and the groups' sums within 64 KB of LDS each.
+    // With more tiles one group per tile would sum every bin in series; the
+    // bin slices above split that work instead.
+    {
+      const long tiles = (long)((p->Cin + 15) / 16) * ((p->Cout + 15) / 16);
+      int ng = 2;
+      while (ng < 4 && tiles * ng * 4 < 2048) ng *= 2;
+      const int tm = wgrad_tmax(T);
+      p->wg_groups = (tiles < 512 && tiles * ng * 4 >= 2048 && T <= 16 && p->kept * tm * 8 <= 64 * 1024 &&
+                      (long)ng * 256 * tm * 4 <= 64 * 1024) ? ng : 0;
+    }
     p->off_Part = o;
     o = align_up(o + (chunks > 1 ? (size_t)chunks * Q * p->Kh * p->Kw * sizeof(float) : 0), 256);
   }

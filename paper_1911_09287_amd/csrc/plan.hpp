@@ -77,6 +77,7 @@ struct bl_conv_plan_s {
   // workspace layout (bytes)
   int wg_chunks;        // bin slices of the weight-gradient inverse DFT
   int wg_bins;          // bins per slice (a multiple of 8)
+  int wg_groups;        // groups of 256 threads per block summing parts of a slice (1, 2 or 4)
   BlContractTiling ct[3];  // contraction tiling: forward, grad-input, grad-weight
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
   // small device tables (1-D chirps and filter spectra, weight-gradient
@@ -87,6 +88,9 @@ struct bl_conv_plan_s {
 
 // Frees a plan's device tables (null is a no-op).
 void bl_plan_tables_free(void* tables);
+
+// Taps of the weight-gradient inverse DFT as its kernels are instantiated.
+inline int wgrad_tmax(int T) { return T <= 9 ? T : T <= 16 ? 16 : T <= 32 ? 32 : 64; }
 
 // FFT row index of the r-th kept row: the top-left corner (u = 0..r_h) first,
 // then the bottom-left corner (u = Lh - r_h .. Lh - 1).

@@ -32,7 +32,7 @@ LIBRARY_NAMES = OrderedDict([
     ("contract_wgrad", r"k_cgemm\w*<\d+, \d+, false, true, true, (false|true)>"),
     ("contract (thin, any pass)", r"k_thin_"),
     ("contract_reduce", r"k_split_reduce"),
-    ("wgrad_idft", r"k_wgrad_wide<|k_wgrad_idft<"),
+    ("wgrad_idft", r"k_wgrad_wide<|k_wgrad_idft<|k_wgrad_tile<"),
     ("wgrad_reduce", r"k_wgrad_reduce"),
 ])
 MARKER = "spin_kernel"

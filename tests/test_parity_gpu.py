@@ -272,13 +272,16 @@ def test_wgrad_paths(torch):
     """Each route of the weight-gradient inverse DFT: one pass over all bins
     for wide layers (taps padded to 16 or exact), bin slices whose weights fill
     the LDS cap (8 x 8 taps), channel-tiled slices for more than 256 output
-    channels, and a single slice written without partial sums."""
+    channels, a single slice written without partial sums, and 16 x 16
+    channel tiles over all bins (2 and 4 groups per tile, ragged tiles)."""
     cases = [
         synth.Layer("wg_wide_k3", 2, 2, 128, 128, 8, 8, 3, (1, 1, 1, 1), "blur"),
         synth.Layer("wg_wide_k4", 2, 2, 128, 128, 8, 8, 4, (2, 1, 2, 1), "blur"),
         synth.Layer("wg_lds_cap_k8", 2, 1, 256, 256, 32, 32, 8, (0, 0, 0, 0), "blur"),
         synth.Layer("wg_tiled_f384", 2, 2, 16, 384, 12, 12, 3, (1, 1, 1, 1), "blur"),
         synth.Layer("wg_single_slice", 1, 2, 4, 300, 20, 1, 3, (1, 1), "walk"),
+        synth.Layer("wg_tile_ng2", 2, 2, 256, 256, 8, 8, 3, (1, 1, 1, 1), "blur"),
+        synth.Layer("wg_tile_ng4_ragged", 2, 2, 200, 260, 6, 6, 4, (2, 1, 2, 1), "blur"),
     ]
     for i, layer in enumerate(cases):
         for c in (0.0, 0.5):
