@@ -631,19 +631,6 @@ __global__ __launch_bounds__(64 * kWaves1k) void k_bluestein1k(const void* __res
   }
 }
 
-int g_cu_count[64];
-
-int device_cus() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (g_cu_count[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    g_cu_count[dev] = n;
-  }
-  return g_cu_count[dev];
-}
-
 template <int M, int MODE, typename S>
 bl_status_t launch_m(BlueArgs& a, const void* in, void* out, const char* name, double bytes, hipStream_t s) {
   // algorithmic arithmetic: two M-point complex FFTs (5 M log2 M flops each, the

@@ -76,6 +76,8 @@ long float_key(float x);  // bit pattern of x, for keys
 // Allows kernel `kern` up to `bytes` of dynamic LDS on the current device
 // (hipFuncAttributeMaxDynamicSharedMemorySize), once per kernel and device.
 bl_status_t lds_opt_in(const void* kern, int bytes);
+// Compute units of the current device (256 if the query fails).
+int device_cus();
 
 // ---- stage launchers --------------------------------------------------------
 // Real planes [P][Hin][Win] placed at (oi, oj) of the grid -> kept spectrum

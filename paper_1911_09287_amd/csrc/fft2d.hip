@@ -4,13 +4,15 @@
 //   row pass    one thread per input row: the real 2MW-point DFT of the padded
 //               row is one MW-point complex DFT of z[q] = x[2q] + i x[2q+1],
 //               split by conjugate symmetry; only columns v < V are kept.
-//   column pass one thread per (plane, kept column): the 2MH-point DFT over the
-//               padded rows is two MH-point DFTs (even and odd rows) and one
-//               radix-2 butterfly; only kept rows are written, bin-major.
+//   column pass per (plane, kept column): the 2MH-point DFT over the padded
+//               rows is two MH-point DFTs (even and odd rows) and one radix-2
+//               butterfly, on one thread or split over a lane pair (one DFT
+//               per thread, butterfly across the pair); only kept rows are
+//               written, bin-major.
 // Inverse (kept bins -> real window), the mirror image:
-//   column pass one thread per (plane, kept column): zero-filled 2MH-point
-//               inverse DFT as two MH-point inverse DFTs (decimation in
-//               frequency); only the rows of the output window are kept.
+//   column pass per (plane, kept column): zero-filled 2MH-point inverse DFT
+//               as two MH-point inverse DFTs (decimation in frequency), on one
+//               thread or one per thread of a lane pair.
 //   row pass    one thread per output row: the Hermitian (c2r) 2MW-point
 //               inverse as one MW-point complex inverse DFT whose real and
 //               imaginary parts are the even and odd samples; the imaginary
@@ -120,6 +122,12 @@ __device__ __forceinline__ float2 root(int k) {
   return make_float2(c, INV ? s : -s);
 }
 
+// Value of the other lane of an even/odd lane pair (DPP quad permutation 1 0 3 2).
+__device__ __forceinline__ float swap_pair(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float2 swap_pair(float2 a) { return make_float2(swap_pair(a.x), swap_pair(a.y)); }
+
 struct Fft2Args {
   int Hin, Win;    // forward: input plane; inverse: output window (OH, OW)
   int oi, oj;      // forward: placement offset; inverse: crop origin
@@ -158,7 +166,7 @@ __device__ inline unsigned plane_group(unsigned b, unsigned nb, unsigned K) {
 // LDS layout (complex spectra, column-major per plane): S[p * PS + v * (LH + 1) + i],
 // so a column thread reads its LH rows at fixed offsets.
 // S: stored-spectrum element of the output (float2 or bfloat16 pairs)
-template <int MH, int MW, typename S>
+template <int MH, int MW, typename S, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, S* __restrict__ out,
                                                        Fft2Args g) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
@@ -176,15 +184,24 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
     for (int j = 0; j < g.oj; ++j) xr[j] = 0.f;
     for (int j = g.oj + g.Win; j < LW; ++j) xr[j] = 0.f;
   }
-  // coalesced copy of the block's rows into their grid columns
+  // coalesced copy of the block's rows into their grid columns: every load of
+  // a thread is issued before the first is used (at most 256 rows of at most
+  // LW floats, so NV4 float4 per thread), the last index repeated past the end
   const float4* src = reinterpret_cast<const float4*>(in + (size_t)p0 * g.Hin * g.Win);
   const unsigned n4 = (unsigned)nrows * g.q4;
-  for (unsigned e = tid; e < n4; e += blockDim.x) {
-    const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
-    const unsigned j4 = e - row * g.q4;
-    const float4 v = src[e];
-    float* xr = xs + row * LW1 + g.oj + 4 * j4;
-    xr[0] = v.x; xr[1] = v.y; xr[2] = v.z; xr[3] = v.w;
+  constexpr int NV4 = (LW + 3) / 4;
+  float4 v4[NV4];
+#pragma unroll
+  for (int it = 0; it < NV4; ++it) v4[it] = src[min((unsigned)(tid + it * kThreads), n4 - 1)];
+#pragma unroll
+  for (int it = 0; it < NV4; ++it) {
+    const unsigned e = (unsigned)(tid + it * kThreads);
+    if (e < n4) {
+      const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
+      const unsigned j4 = e - row * g.q4;
+      float* xr = xs + row * LW1 + g.oj + 4 * j4;
+      xr[0] = v4[it].x; xr[1] = v4[it].y; xr[2] = v4[it].z; xr[3] = v4[it].w;
+    }
   }
   __syncthreads();
 
@@ -220,35 +237,64 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
   }
   __syncthreads();
 
-  // column pass: thread = (kept column, plane), planes fastest
-  for (int e = tid; e < np * g.V; e += blockDim.x) {
-    const int p = e % np, v = e / np;
-    float2* tc = T + p * g.PS + v * LH1;
-    for (int i = 0; i < g.oi; ++i) tc[i] = make_float2(0.f, 0.f);
-    for (int i = g.oi + g.Hin; i < LH; ++i) tc[i] = make_float2(0.f, 0.f);
-    float2 ev[MH], od[MH];
-#pragma unroll
-    for (int q = 0; q < MH; ++q) {
-      ev[q] = tc[2 * q];
-      od[q] = tc[2 * q + 1];
-    }
-    float2 E[MH], O[MH];
-    dft_odd<MH, false>(ev, E);
-    dft_odd<MH, false>(od, O);
-    S* dst = out + (p0 + p) + (unsigned)v * g.P;
+  if constexpr (SPLIT) {
+    // column pass: two threads per (kept column, plane), planes fastest after
+    // the pair: thread h of a pair takes the padded rows of parity h, the odd
+    // half is twiddled, and the pair swaps halves to write rows k (h = 0) and
+    // k + MH (h = 1).  A pair's lanes are active together (the count is even).
     const unsigned rs = (unsigned)g.V * g.P;
+    for (int e = tid; e < 2 * np * g.V; e += kThreads) {
+      const int h = e & 1, c = e >> 1;
+      const int p = c % np, v = c / np;
+      const float2* tc = T + p * g.PS + v * LH1;
+      float2 z[MH];
 #pragma unroll
-    for (int k = 0; k < MH; ++k) {
-      const float2 t = cmul(root<LH, false>(k), O[k]);
-      const int r_lo = row_slot(k, g.r_h, g.R, LH);
-      const int r_hi = row_slot(k + MH, g.r_h, g.R, LH);
-      if (r_lo >= 0) spec_put(dst, (unsigned)r_lo * rs, cadd(E[k], t));
-      if (r_hi >= 0) spec_put(dst, (unsigned)r_hi * rs, csub(E[k], t));
+      for (int q = 0; q < MH; ++q) {
+        const int i = 2 * q + h;
+        z[q] = (i >= g.oi && i < g.oi + g.Hin) ? tc[i] : make_float2(0.f, 0.f);
+      }
+      float2 D[MH];
+      dft_odd<MH, false>(z, D);
+      S* dst = out + (p0 + p) + (unsigned)v * g.P;
+#pragma unroll
+      for (int k = 0; k < MH; ++k) {
+        const float2 mine = h ? cmul(root<LH, false>(k), D[k]) : D[k];
+        const float2 other = swap_pair(mine);
+        const int r = row_slot(k + h * MH, g.r_h, g.R, LH);
+        if (r >= 0) spec_put(dst, (unsigned)r * rs, h ? csub(other, mine) : cadd(mine, other));
+      }
+    }
+  } else {
+    // column pass: thread = (kept column, plane), planes fastest
+    for (int e = tid; e < np * g.V; e += kThreads) {
+      const int p = e % np, v = e / np;
+      float2* tc = T + p * g.PS + v * LH1;
+      for (int i = 0; i < g.oi; ++i) tc[i] = make_float2(0.f, 0.f);
+      for (int i = g.oi + g.Hin; i < LH; ++i) tc[i] = make_float2(0.f, 0.f);
+      float2 ev[MH], od[MH];
+#pragma unroll
+      for (int q = 0; q < MH; ++q) {
+        ev[q] = tc[2 * q];
+        od[q] = tc[2 * q + 1];
+      }
+      float2 E[MH], O[MH];
+      dft_odd<MH, false>(ev, E);
+      dft_odd<MH, false>(od, O);
+      S* dst = out + (p0 + p) + (unsigned)v * g.P;
+      const unsigned rs = (unsigned)g.V * g.P;
+#pragma unroll
+      for (int k = 0; k < MH; ++k) {
+        const float2 t = cmul(root<LH, false>(k), O[k]);
+        const int r_lo = row_slot(k, g.r_h, g.R, LH);
+        const int r_hi = row_slot(k + MH, g.r_h, g.R, LH);
+        if (r_lo >= 0) spec_put(dst, (unsigned)r_lo * rs, cadd(E[k], t));
+        if (r_hi >= 0) spec_put(dst, (unsigned)r_hi * rs, csub(E[k], t));
+      }
     }
   }
 }
 
-template <int MH, int MW>
+template <int MH, int MW, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
                                                        Fft2Args g) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
@@ -260,29 +306,61 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
 
-  // column pass: thread = (kept column, plane), planes fastest
-  for (int e = tid; e < np * g.V; e += blockDim.x) {
-    const int p = e % np, v = e / np;
-    const float2* src = in + (p0 + p) + (unsigned)v * g.P;
-    const unsigned rs = (unsigned)g.V * g.P;
-    float2 a[MH], b[MH];
+  if constexpr (SPLIT) {
+    // column pass: two threads per (kept column, plane), planes fastest after
+    // the pair: thread h of a pair loads the kept rows k + h MH, the pair swaps
+    // them, and thread h forms the even (h = 0) or twiddled odd (h = 1) half and
+    // inverts it into the padded rows of parity h.  A pair's lanes are active
+    // together (the count is even).
+    for (int e = tid; e < 2 * np * g.V; e += kThreads) {
+      const int h = e & 1, c = e >> 1;
+      const int p = c % np, v = c / np;
+      const float2* src = in + (p0 + p) + (unsigned)v * g.P;
+      const unsigned rs = (unsigned)g.V * g.P;
+      float2 mine[MH];
 #pragma unroll
-    for (int k = 0; k < MH; ++k) {
-      const int r0 = row_slot(k, g.r_h, g.R, LH);
-      const int r1 = row_slot(k + MH, g.r_h, g.R, LH);
-      const float2 lo = r0 >= 0 ? src[r0 * rs] : make_float2(0.f, 0.f);
-      const float2 hi = r1 >= 0 ? src[r1 * rs] : make_float2(0.f, 0.f);
-      a[k] = cadd(lo, hi);
-      b[k] = cmul(root<LH, true>(k), csub(lo, hi));
+      for (int k = 0; k < MH; ++k) {
+        const int r = row_slot(k + h * MH, g.r_h, g.R, LH);
+        mine[k] = r >= 0 ? src[(unsigned)r * rs] : make_float2(0.f, 0.f);
+      }
+      float2 z[MH];
+#pragma unroll
+      for (int k = 0; k < MH; ++k) {
+        const float2 other = swap_pair(mine[k]);
+        const float2 lo = h ? other : mine[k], hi = h ? mine[k] : other;
+        z[k] = h ? cmul(root<LH, true>(k), csub(lo, hi)) : cadd(lo, hi);
+      }
+      float2 x[MH];
+      dft_odd<MH, true>(z, x);
+      float2* zc = Zs + p * g.PS + v * LH1;
+#pragma unroll
+      for (int q = 0; q < MH; ++q) zc[2 * q + h] = x[q];
     }
-    float2 xe[MH], xo[MH];
-    dft_odd<MH, true>(a, xe);
-    dft_odd<MH, true>(b, xo);
-    float2* zc = Zs + p * g.PS + v * LH1;
+  } else {
+    // column pass: thread = (kept column, plane), planes fastest
+    for (int e = tid; e < np * g.V; e += kThreads) {
+      const int p = e % np, v = e / np;
+      const float2* src = in + (p0 + p) + (unsigned)v * g.P;
+      const unsigned rs = (unsigned)g.V * g.P;
+      float2 a[MH], b[MH];
 #pragma unroll
-    for (int q = 0; q < MH; ++q) {
-      zc[2 * q] = xe[q];
-      zc[2 * q + 1] = xo[q];
+      for (int k = 0; k < MH; ++k) {
+        const int r0 = row_slot(k, g.r_h, g.R, LH);
+        const int r1 = row_slot(k + MH, g.r_h, g.R, LH);
+        const float2 lo = r0 >= 0 ? src[r0 * rs] : make_float2(0.f, 0.f);
+        const float2 hi = r1 >= 0 ? src[r1 * rs] : make_float2(0.f, 0.f);
+        a[k] = cadd(lo, hi);
+        b[k] = cmul(root<LH, true>(k), csub(lo, hi));
+      }
+      float2 xe[MH], xo[MH];
+      dft_odd<MH, true>(a, xe);
+      dft_odd<MH, true>(b, xo);
+      float2* zc = Zs + p * g.PS + v * LH1;
+#pragma unroll
+      for (int q = 0; q < MH; ++q) {
+        zc[2 * q] = xe[q];
+        zc[2 * q + 1] = xo[q];
+      }
     }
   }
   __syncthreads();
@@ -335,6 +413,16 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
 // ceil(2^32 / d) for d > 1 (d = 1 is handled by the kernels directly).
 unsigned magic_for(unsigned d) { return d > 1 ? (unsigned)((0x100000000ull + d - 1) / d) : 0u; }
 
+// Column pass on lane pairs (one MH-point DFT per thread).  Always for the
+// longest columns (MH >= 17), where two DFTs per thread hold too many registers
+// for four waves per SIMD; for the forward on 18-point columns when the pairs
+// of a block's G planes x V kept columns fit one pass of its threads.  On
+// shorter columns, and for the inverse below 34 points, one thread per column
+// measured faster.
+bool column_split(bool fwd, int MH, int G, int V) {
+  return MH >= 17 || (fwd && MH >= 9 && 2L * G * V <= kThreads);
+}
+
 // Plane groups whose runs of G elements of `elem` bytes fill a 128-byte line.
 unsigned line_groups(int G, int elem) { return (unsigned)std::max(1, (128 + G * elem - 1) / (G * elem)); }
 
@@ -342,7 +430,8 @@ template <int MH, int MW>
 bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                          int oj, hipStream_t s) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
-  if (Win % 4 != 0 || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
+  if (Win % 4 != 0 || oj + Win > LW || oi + Hin > LH || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L)
+    return BL_ERR_UNSUPPORTED;
   Fft2Args g{Hin, Win, oi, oj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)(Win / 4), 0, 1u, 1.0f};
   g.magic = magic_for(g.q4);
   g.PS = (p->V * (LH + 1)) | 1;
@@ -366,13 +455,22 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, lo
   // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
   // complex LH-point column FFTs (5 LH log2 LH) per plane
   const double flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
+  const bool split = column_split(true, MH, G, p->V);
   return timed_launch("spec_fwd_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    if (p->bf16)
-      hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0,
-                            e1, 0, in, static_cast<unsigned*>(out), g);
-    else
-      hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0,
-                            e1, 0, in, static_cast<float2*>(out), g);
+    const dim3 grid((unsigned)blocks), block(kThreads);
+    if (p->bf16) {
+      unsigned* o = static_cast<unsigned*>(out);
+      if (split)
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, true>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+      else
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, false>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+    } else {
+      float2* o = static_cast<float2*>(out);
+      if (split)
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, true>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+      else
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, false>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+    }
   });
 }
 
@@ -399,8 +497,13 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
   const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
+  const bool split = column_split(false, MH, G, p->V);
   return timed_launch("spec_inv_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL((k_fft2_inv<MH, MW>), dim3((unsigned)blocks), dim3(kThreads), lds_for(G), s, e0, e1, 0, in, out, g);
+    const dim3 grid((unsigned)blocks), block(kThreads);
+    if (split)
+      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true>), grid, block, lds_for(G), s, e0, e1, 0, in, out, g);
+    else
+      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false>), grid, block, lds_for(G), s, e0, e1, 0, in, out, g);
   });
 }
 

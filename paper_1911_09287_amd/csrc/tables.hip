@@ -62,6 +62,18 @@ bl_status_t lds_opt_in(const void* kern, int bytes) {
   return BL_OK;
 }
 
+int device_cus() {
+  static int count[64];  // per device; written once with the same value
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (count[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    count[dev] = n;
+  }
+  return count[dev];
+}
+
 long float_key(float x) {
   unsigned u;
   std::memcpy(&u, &x, sizeof u);
