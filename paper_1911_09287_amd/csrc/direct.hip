@@ -189,13 +189,18 @@ __global__ __launch_bounds__(kThreads) void k_spec_inv(const float2* __restrict_
 
 // ---------------------------------------------------------------------------
 // spec_filt: w [F][C][Kh][Kw] -> W[b][c][f] at the kept bins (origin placement).
-// One thread per (c, f) pair; blockIdx.y strides over chunks of bins.
+// One thread per (c, f) pair, consecutive threads on consecutive f (so the
+// stores of a bin are contiguous); the grid is (pair blocks) x (bin chunks),
+// numbered so that consecutive pair blocks run on one XCD: the taps of
+// neighbouring channels c share cache lines, which are then fetched into one
+// L2 rather than several.
 // ---------------------------------------------------------------------------
 
 struct FiltGeom {
   int F, C, Kh, Kw;
   int Lh, Lw, r_h, R, V;
   int bins_per_block;
+  int xblocks;  // blocks of 256 (c, f) pairs
 };
 
 template <int KH, int KW, typename S>
@@ -206,6 +211,24 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
   extern __shared__ float2 smem[];
   float2* twh = smem;
   float2* tww = twh + g.Lh;
+  // logical block: consecutive ids on one XCD (the hardware deals blocks to
+  // the 8 XCDs in turn); pair block = id % xblocks, bin chunk = id / xblocks
+  const unsigned nb = gridDim.x;
+  unsigned id = blockIdx.x;
+  if (nb % 8 == 0) id = (id % 8) * (nb / 8) + id / 8;
+  const unsigned xblocks = (unsigned)g.xblocks;
+  const unsigned bx = id % xblocks, by = id / xblocks;
+  const long CF = (long)g.C * g.F;
+  const long q = (long)bx * blockDim.x + threadIdx.x;  // q = c * F + f
+  const bool live = q < CF;
+  const int c = live ? (int)(q / g.F) : 0, f = live ? (int)(q % g.F) : 0;
+  // the taps are loaded before the roots are staged, so both loads overlap
+  float tap[KH][KW];
+  const float* wp = w + ((size_t)f * g.C + c) * KH * KW;
+#pragma unroll
+  for (int a = 0; a < KH; ++a)
+#pragma unroll
+    for (int b = 0; b < KW; ++b) tap[a][b] = wp[a * KW + b];
   if (roots) {
     for (int k = threadIdx.x; k < g.Lh + g.Lw; k += blockDim.x) smem[k] = roots[k];
   } else {
@@ -213,18 +236,9 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
     fill_roots(tww, g.Lw, -1.0);
   }
   __syncthreads();
-  const long CF = (long)g.C * g.F;
-  const long q = (long)blockIdx.x * blockDim.x + threadIdx.x;  // q = c * F + f
-  if (q >= CF) return;
-  const int c = (int)(q / g.F), f = (int)(q % g.F);
-  float tap[KH][KW];
-  const float* wp = w + ((size_t)f * g.C + c) * KH * KW;
-#pragma unroll
-  for (int a = 0; a < KH; ++a)
-#pragma unroll
-    for (int b = 0; b < KW; ++b) tap[a][b] = wp[a * KW + b];
+  if (!live) return;
   const int B = g.R * g.V;
-  const int b0 = blockIdx.y * g.bins_per_block;
+  const int b0 = (int)by * g.bins_per_block;
   const int b1 = min(B, b0 + g.bins_per_block);
   // twiddle indices (u a) mod Lh and (v b) mod Lw, advanced bin by bin
   int r = b0 / g.V, v = b0 - (b0 / g.V) * g.V;
@@ -724,7 +738,7 @@ void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
 }
 
 bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s, bool use_table) {
-  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0};
+  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
   const float2* roots = nullptr;
   if (use_table) {
     const std::vector<long> key{3, p->Lh, p->Lw};
@@ -739,7 +753,9 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
   g.bins_per_block = (B + chunks - 1) / chunks;
   chunks = (B + g.bins_per_block - 1) / g.bins_per_block;
   const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
-  dim3 grid((unsigned)xblocks, (unsigned)chunks);
+  g.xblocks = (int)xblocks;
+  if ((double)xblocks * chunks >= 2147483647.0) return BL_ERR_UNSUPPORTED;
+  dim3 grid((unsigned)(xblocks * chunks));
   const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * (p->bf16 ? 4 : 8);
 #define X(a, b)                                                                                             \
   if (p->Kh == a && p->Kw == b)                                                                             \
