@@ -464,7 +464,7 @@ __global__ __launch_bounds__(64 * NW) void k_wgrad_wide(const float2* __restrict
   }
 }
 
-// Layers with many channel pairs (at least 128 tiles of 16 x 16): a block
+// Layers of 128 to 511 tiles of 16 x 16 channel pairs: a block
 // takes a tile of 16 input channels x 16 filters and all kept bins; its NG
 // groups of 256 threads (one pair (c, f) per thread) each sum a contiguous
 // part of the bins, reading DW[bin][c][f] as runs of 16 filters (128 bytes)
