@@ -59,9 +59,15 @@ typedef short shortx4 __attribute__((ext_vector_type(4)));
 // BF16: operands stored as bfloat16 pairs (32-bit words, real part in the low
 // half), multiplied on the bf16 matrix cores with fp32 accumulation; else
 // complex64 on the fp32 ones.
-template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16>
-__global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, const void* __restrict__ B_,
-                                               float2* __restrict__ O, CgemmArgs g) {
+// KS: groups of 4 waves sharing the tile (fp32 only): group q takes the
+// k-stages q, q + KS, ... through its own LDS buffers, and the groups' sums are
+// added through LDS in group order at the end.  Used when the launch has no
+// more tiles than compute units, so that each SIMD runs KS waves instead of one.
+template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16, int KS>
+__global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void* __restrict__ A_,
+                                                                   const void* __restrict__ B_,
+                                                                   float2* __restrict__ O, CgemmArgs g) {
+  static_assert(KS == 1 || !BF16, "the in-block k split is built for the fp32 operands");
   using S = std::conditional_t<BF16, unsigned, float2>;  // stored operand element
   using V = std::conditional_t<BF16, uint2, float4>;     // two consecutive elements
   const S* A = static_cast<const S*>(A_);
@@ -74,8 +80,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
   constexpr int BV = BN / 32;  // 16-byte B loads per thread per stage
   constexpr int SA = BM + 4, SB = BN + 4;  // padded row lengths
   constexpr int PA = plane_floats<BM>(), PB = plane_floats<BN>();
-  __shared__ float As[BF16 ? 1 : 2][BF16 ? 1 : 2 * PA];
-  __shared__ float Bs[BF16 ? 1 : 2][BF16 ? 1 : 2 * PB];
+  __shared__ float As[KS][BF16 ? 1 : 2][BF16 ? 1 : 2 * PA];
+  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : 2 * PB];
   // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
   // the (even, odd) real-k entries of the 2x2 block column the lane reads.
   // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
@@ -97,7 +103,7 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
   const int m0 = tm * BM, n0 = tn * BN;
   const S* Ab = A + bin * g.bA;
   const S* Bb = Bm + bin * g.bB;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x & 255, grp = KS == 1 ? 0 : (int)(threadIdx.x >> 8), lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
 
   // B operand of this lane: real column jcol = lane % 32 of a 32-wide block is
@@ -198,8 +204,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
     if constexpr (BF16) {
       store16(buf, k0, ra, rb);
     } else {
-      float* a0 = As[buf];
-      float* a1 = As[buf] + PA;
+      float* a0 = As[grp][buf];
+      float* a1 = As[grp][buf] + PA;
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         int m, k;
@@ -213,8 +219,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
           *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(r.y, r.w);
         }
       }
-      float* b0 = Bs[buf];
-      float* b1 = Bs[buf] + PB;
+      float* b0 = Bs[grp][buf];
+      float* b1 = Bs[grp][buf] + PB;
 #pragma unroll
       for (int q = 0; q < BV; ++q) {
         int k, n;
@@ -266,8 +272,8 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
       return;
     }
     // all fragments of the stage first, so the LDS reads overlap the MFMAs
-    const float* ap = As[buf] + a_part * PA + wm + jcol;
-    const float* bp = Bs[buf] + b_src * PB + wn + (jcol >> 1);
+    const float* ap = As[grp][buf] + a_part * PA + wm + jcol;
+    const float* bp = Bs[grp][buf] + b_src * PB + wn + (jcol >> 1);
     float av[kBK][MI], bv[kBK][NJ];
 #pragma unroll
     for (int s = 0; s < kBK; ++s) {
@@ -292,22 +298,51 @@ __global__ __launch_bounds__(256, 2) void k_cgemm(const void* __restrict__ A_, c
   // clamped for the load (a repeated, cached read) and zero-filled by the
   // store; with an odd number of stages the last pair's second stage is such
   // an all-zero stage (its MFMAs add nothing).
+  // Group grp's local stage t is stage KS t + grp of the k range (the groups
+  // loop the same number of times: a stage past the last is zero-filled).
   const int nst = (kend - kbeg + kBK - 1) / kBK;
-  auto kof = [&](int st) { return kbeg + min(st, nst - 1) * kBK; };
+  const int nst_l = (nst + KS - 1) / KS;
+  auto kof = [&](int t) { return kbeg + min(KS * t + grp, nst - 1) * kBK; };
+  auto k0of = [&](int t) { return kbeg + (KS * t + grp) * kBK; };
   V ra0[AV], rb0[BV], ra1[AV], rb1[BV];
   load(kof(0), ra0, rb0);
   load(kof(1), ra1, rb1);
-  store(0, kbeg, ra0, rb0);
+  store(0, k0of(0), ra0, rb0);
   __syncthreads();
-  for (int cs = 0; cs < nst; cs += 2) {
+  for (int cs = 0; cs < nst_l; cs += 2) {
     load(kof(cs + 2), ra0, rb0);
     compute(0);
-    store(1, kbeg + (cs + 1) * kBK, ra1, rb1);
+    store(1, k0of(cs + 1), ra1, rb1);
     __syncthreads();
     load(kof(cs + 3), ra1, rb1);
     compute(1);
-    store(0, kbeg + (cs + 2) * kBK, ra0, rb0);
+    store(0, k0of(cs + 2), ra0, rb0);
     __syncthreads();
+  }
+  if constexpr (KS > 1) {
+    // groups 1.. leave their sums in the (now idle) operand buffers; group 0
+    // adds them in group order and stores the tile
+    constexpr int kAcc = 256 * MI * NJ * 16;  // floats per group
+    static_assert((KS - 1) * kAcc <= KS * 2 * 2 * PA, "reduction buffer");
+    float* red = &As[0][0][0];
+    if (grp > 0) {
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) red[(grp - 1) * kAcc + ((i * NJ + j) * 16 + v) * 256 + tid] = acc[i][j][v];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int q = 1; q < KS; ++q)
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(q - 1) * kAcc + ((i * NJ + j) * 16 + v) * 256 + tid];
   }
 
   // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
@@ -397,9 +432,11 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
 #define BL_GO(BMV, BNV, AK, BN_, CJ)                                                                        \
   st = timed_launch(name, bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                               \
     if (p->bf16)                                                                                             \
-      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, true>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
+      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, true, 1>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
+    else if (t.ks == 2)                                                                                      \
+      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, false, 2>), grid, dim3(512), 0, s, e0, e1, 0, A, Bm, dst, g); \
     else                                                                                                     \
-      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, false>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
+      hipExtLaunchKernelGGL((k_cgemm<BMV, BNV, AK, BN_, CJ, false, 1>), grid, dim3(256), 0, s, e0, e1, 0, A, Bm, dst, g); \
   })
 #define BL_SHAPES(AK, BN_, CJ)                       \
   if (BM == 128 && BN == 64) BL_GO(128, 64, AK, BN_, CJ); \

@@ -26,13 +26,14 @@ constexpr long kWgradSliceLds = 48 * 1024;
 
 struct BlContractTiling {
   int bm, bn, splits;
+  int ks;  // groups of 4 waves per block splitting the tile's k range (fp32 tiles, 1 or 2)
 };
 inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
   // constants fitted to measured launches of the tiles on an MI355X: the
   // matrix cores reach about 60% (1 or 4 MFMA chains per wave) or 50%
   // (2 chains) of their rate inside a tile
   const double kCUs = 256, kClock = 2.4e9, kStart = 0.3e-6, kHbm = 5.0e12, kPass = 4e-6;
-  BlContractTiling best{64, 64, 1};
+  BlContractTiling best{64, 64, 1, 1};
   double best_t = 1e30;
   const int shapes[4][2] = {{128, 64}, {64, 64}, {128, 32}, {64, 32}};
   for (const auto& sh : shapes) {
@@ -49,9 +50,13 @@ inline BlContractTiling bl_contract_tiling(long M, long N, long K, long bins) {
       const double mfma = chains * 64.0 * kper / kClock / (chains == 2 ? 0.5 : 0.6);
       double t = per_cu * (mfma + kStart);
       if (splits > 1) t += kPass + 8.0 * bins * M * N * (splits + 1) / kHbm;
-      if (t < best_t * 0.98) best_t = t, best = BlContractTiling{bm, bn, splits};
+      if (t < best_t * 0.98) best_t = t, best = BlContractTiling{bm, bn, splits, 1};
     }
   }
+  // no more tiles than compute units: one wave per SIMD would run each tile,
+  // so two groups of four waves split its k range instead
+  const long tiles = bins * ((M + best.bm - 1) / best.bm) * ((N + best.bn - 1) / best.bn) * best.splits;
+  if (tiles <= (long)kCUs && best.bm == 64) best.ks = 2;
   return best;
 }
 
