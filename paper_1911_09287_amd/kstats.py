@@ -27,9 +27,9 @@ LIBRARY_NAMES = OrderedDict([
     ("spec_fwd_direct", r"k_spec_fwd<"),
     ("spec_inv_direct", r"k_spec_inv\b"),
     ("spec_filt", r"k_spec_filt<"),
-    ("contract_fwd", r"k_cgemm\w*<\d+, \d+, true, true, true, (false|true)>"),
-    ("contract_dgrad", r"k_cgemm\w*<\d+, \d+, true, false, false, (false|true)>"),
-    ("contract_wgrad", r"k_cgemm\w*<\d+, \d+, false, true, true, (false|true)>"),
+    ("contract_fwd", r"k_cgemm\w*<\d+, \d+, true, true, true, (false|true)(, \d+)?>"),
+    ("contract_dgrad", r"k_cgemm\w*<\d+, \d+, true, false, false, (false|true)(, \d+)?>"),
+    ("contract_wgrad", r"k_cgemm\w*<\d+, \d+, false, true, true, (false|true)(, \d+)?>"),
     ("contract (thin, any pass)", r"k_thin_"),
     ("contract_reduce", r"k_split_reduce"),
     ("wgrad_idft", r"k_wgrad_wide<|k_wgrad_idft<|k_wgrad_tile<"),
