@@ -128,6 +128,9 @@ __device__ __forceinline__ float swap_pair(float x) {
 }
 __device__ __forceinline__ float2 swap_pair(float2 a) { return make_float2(swap_pair(a.x), swap_pair(a.y)); }
 
+// Flag in Fft2Args::K of the inverse: the output window's rows are whole float4s.
+constexpr unsigned kInvVec4 = 0x80000000u;
+
 struct Fft2Args {
   int Hin, Win;    // forward: input plane; inverse: output window (OH, OW)
   int oi, oj;      // forward: placement offset; inverse: crop origin
@@ -303,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   float* ys = reinterpret_cast<float*>(sm);  // output staging: G*OH grid rows of LW1 floats; aliases Zs
   const int tid = threadIdx.x;
   const int OH = g.Hin, OW = g.Win;
-  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K) * (unsigned)g.G;
+  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K & ~kInvVec4) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
 
   if constexpr (SPLIT) {
@@ -400,13 +403,25 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
     for (int j = 0; j < LW; ++j) yr[j] = yv[j];
   }
   __syncthreads();
-  // coalesced copy of the cropped window (planes contiguous in HBM)
+  // coalesced copy of the cropped window (planes contiguous in HBM): 16-byte
+  // stores when the window's rows are whole float4s (q4 = OW / 4), else floats
+  // (q4 = OW)
   float* dst = out + (size_t)p0 * OH * OW;
-  const unsigned n = (unsigned)nrows * OW;
-  for (unsigned e = tid; e < n; e += blockDim.x) {
-    const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
-    const unsigned j = e - row * g.q4;
-    dst[e] = ys[row * LW1 + g.oj + j];
+  if (g.K & kInvVec4) {
+    float4* dst4 = reinterpret_cast<float4*>(dst);
+    const unsigned n4 = (unsigned)nrows * g.q4;
+    for (unsigned e = tid; e < n4; e += blockDim.x) {
+      const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
+      const float* yr = ys + row * LW1 + g.oj + 4 * (e - row * g.q4);
+      dst4[e] = make_float4(yr[0], yr[1], yr[2], yr[3]);
+    }
+  } else {
+    const unsigned n = (unsigned)nrows * OW;
+    for (unsigned e = tid; e < n; e += blockDim.x) {
+      const unsigned row = g.q4 == 1 ? e : __umulhi(e, g.magic);
+      const unsigned j = e - row * g.q4;
+      dst[e] = ys[row * LW1 + g.oj + j];
+    }
   }
 }
 
@@ -479,7 +494,8 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
                          int cj, hipStream_t s) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if ((double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
-  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)OW, 0, 1u,
+  const bool vec4 = OW % 4 == 0;
+  Fft2Args g{OH, OW, ci, cj, p->r_h, p->R, p->V, (unsigned)P, 0, 0, (unsigned)(vec4 ? OW / 4 : OW), 0, 1u,
              1.0f / ((float)p->Lh * (float)p->Lw)};
   g.magic = magic_for(g.q4);
   g.PS = (p->V * (LH + 1)) | 1;
@@ -493,7 +509,7 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   while (G > 1 && lds_for(G) > kMaxLds) --G;
   if (OH > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
   g.G = G;
-  g.K = line_groups(G, 8);
+  g.K = line_groups(G, 8) | (vec4 ? kInvVec4 : 0u);
   const long blocks = (P + G - 1) / G;
   const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
   const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
