@@ -87,15 +87,6 @@ __device__ __forceinline__ int pidx(int n) { return n + (n >> 4); }
 template <int M>
 constexpr int padded() { return M + M / 16; }
 
-// Orders the LDS accesses of one wave: everything a wave wrote before this
-// point is seen by its later reads (LDS executes a wave's accesses in order;
-// the fences keep the compiler from moving accesses across).
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // One Stockham autosort pass of radix R over M points, done by one wave (lane
 // = 0..63) or by a whole block (NT threads; then it synchronises the block).
 // load(i) returns element i of the input sequence and store(i, v) takes

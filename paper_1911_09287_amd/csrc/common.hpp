@@ -35,6 +35,15 @@ __device__ __forceinline__ float2 spec_get(const float2* o, size_t i) { return o
 __device__ __forceinline__ float2 spec_get(const unsigned* o, size_t i) { return spec_unpack(o[i]); }
 constexpr size_t kMaxLds = 64 * 1024;
 
+// Orders the LDS accesses of one wave: everything a wave wrote before this
+// point is seen by its later reads (LDS executes a wave's accesses in order;
+// the fences keep the compiler from moving accesses across).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---- per-kernel timing (bl_profile_*) -------------------------------------
 // Reserve a timing slot for one launch; -1 when profiling is off or full.
 int prof_slot(const char* name, double bytes, double flops);

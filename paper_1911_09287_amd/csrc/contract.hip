@@ -334,19 +334,52 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
           for (int v = 0; v < 16; ++v) red[(grp - 1) * kAcc + ((i * NJ + j) * 16 + v) * 256 + tid] = acc[i][j][v];
     }
     __syncthreads();
-    if (grp > 0) return;
+    if (grp == 0) {
 #pragma unroll
-    for (int q = 1; q < KS; ++q)
+      for (int q = 1; q < KS; ++q)
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(q - 1) * kAcc + ((i * NJ + j) * 16 + v) * 256 + tid];
+    }
+    __syncthreads();  // the sums are read before the store staging below reuses the buffers
+    if (grp > 0) return;
+  }
+
+  // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
+  float* Of = reinterpret_cast<float*>(O + blockIdx.z * g.split_stride + bin * g.bO);
+  if constexpr (!BF16) {
+    if (g.ldo % 2 == 0 && g.N % 2 == 0) {
+      // through the idle operand buffers, 16 rows of a block at a time (rows
+      // padded to 40 floats: the two half-waves' rows land on disjoint banks),
+      // so that each lane stores 16 bytes: two complex columns of one row
+      float* st = &As[0][0][0] + wave * (16 * 40);
+      static_assert(4 * 16 * 40 <= KS * 2 * 2 * PA, "store staging");
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(q - 1) * kAcc + ((i * NJ + j) * 16 + v) * 256 + tid];
+          for (int hv = 0; hv < 2; ++hv) {  // VGPRs 8 hv .. 8 hv + 7: rows 16 hv .. 16 hv + 15
+#pragma unroll
+            for (int v = 0; v < 8; ++v)
+              st[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 40 + jcol] = acc[i][j][8 * hv + v];
+            wave_sync();
+#pragma unroll
+            for (int it = 0; it < 2; ++it) {
+              const int idx = it * 64 + lane, row = idx >> 3, c4 = idx & 7;
+              const int m = m0 + wm + 32 * i + 16 * hv + row;
+              const int n = n0 + wn + 16 * j + 2 * c4;
+              const float4 val = *reinterpret_cast<const float4*>(st + row * 40 + 4 * c4);
+              if (m < g.M && n < g.N) *reinterpret_cast<float4*>(Of + ((unsigned)m * g.ldo + n) * 2) = val;
+            }
+            wave_sync();
+          }
+      return;
+    }
   }
-
-  // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
-  float* Of = reinterpret_cast<float*>(O + blockIdx.z * g.split_stride + bin * g.bO);
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
