@@ -150,17 +150,21 @@ def profile_steps(torch, blconv, layers, steps):
     """The same steps again with the library stamping every kernel's own start
     and end (two HIP events per launch on the stream it runs on).  The events
     add gaps between kernels (the step takes longer), not time inside them.
-    Returns (all records, records per layer)."""
+    Marker kernels bracket the pass, as they do the timed steps, so that a
+    profiler's trace of the same pass can be compared.  Returns (all records,
+    records per layer)."""
     prof = blconv.Profile(capacity=64 * steps * len(layers))
     lib = blconv.load()
     bounds = []
     torch.cuda.synchronize()
+    torch.cuda._sleep(1000)  # marker kernels bracket the pass in a profiler's trace
     with prof:
         for _ in range(steps):
             for i, L in enumerate(layers):
                 a = lib.bl_profile_count()
                 L.step()
                 bounds.append((i, a, lib.bl_profile_count()))
+    torch.cuda._sleep(1000)
     torch.cuda.synchronize()
     recs = prof.records()
     prof.release()

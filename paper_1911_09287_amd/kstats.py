@@ -2,9 +2,11 @@
 
 Measurement tool (not used by the library).  Input: the ``*_kernel_trace.csv``
 of ``rocprofv3 --kernel-trace`` run on ``bench.py``.  The benchmark launches a
-short spin kernel just before and just after each group of timed steps; this
-tool keeps the dispatches between the first two such markers (the headline
-workload's timed steps) and prints, per library kernel name (the names the
+short spin kernel just before and just after each group of timed steps and
+each pass with per-kernel events; this tool keeps the dispatches between the
+markers of one such group (segment 0: the headline workload's timed steps;
+segment 1: its pass with per-kernel events, from which the benchmark's
+roofline durations come) and prints, per library kernel name (the names the
 library's per-kernel timing reports, each covering one or more template
 instantiations), the dispatch count and the average, minimum and maximum
 duration, then the same per kernel symbol.  The output is a Markdown table.
@@ -49,7 +51,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("trace")
     ap.add_argument("--segment", type=int, default=0,
-                    help="which marked group of timed steps (0 = the first: the headline)")
+                    help="which marked group (0: the headline's timed steps; 1: its pass with kernel events)")
     a = ap.parse_args()
     rows = sorted(csv.DictReader(open(a.trace)), key=lambda r: int(r["Start_Timestamp"]))
     marks = [i for i, r in enumerate(rows) if MARKER in r["Kernel_Name"]]
