@@ -13,11 +13,12 @@
 // loads (16-byte vectors, two complex values each) run two stages ahead of
 // the MFMAs through two register sets, and LDS is double buffered.  4 waves
 // in a 2x2 grid; a wave owns BM/2 rows x BN/2 complex columns.  Operands are
-// staged in LDS as separate real and imaginary planes, k-major, with rows
-// padded by 4 floats and planes offset by half the banks, so that the MFMA
-// operand fetches (one 32-bit read per lane) and the stores are free of bank
-// conflicts.  Blocks are numbered so that consecutive tiles (which share
-// operand rows) run on the same XCD and its L2.
+// staged in LDS as separate real and imaginary planes (B also as its negated
+// imaginary plane, so that each lane reads its block entry as is), k-major,
+// with rows padded by 4 floats and planes offset by half or a quarter of the
+// banks, so that the MFMA operand fetches (one 32-bit read per lane) and the
+// stores are free of bank conflicts.  Blocks are numbered so that consecutive
+// tiles (which share operand rows) run on the same XCD and its L2.
 //
 // With bfloat16 storage of the spectra the operands arrive as 32-bit (re, im)
 // pairs (8-byte vectors, two values each) and run on v_mfma_f32_32x32x8_bf16,
@@ -81,7 +82,9 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   constexpr int SA = BM + 4, SB = BN + 4;  // padded row lengths
   constexpr int PA = plane_floats<BM>(), PB = plane_floats<BN>();
   __shared__ float As[KS][BF16 ? 1 : 2][BF16 ? 1 : 2 * PA];
-  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : 2 * PB];
+  // B planes: re at 0, im at PB (half the banks away), -im at 2 PB + 16 (a
+  // quarter of the banks away from both), so that no lane negates a value
+  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : 3 * PB + 16];
   // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
   // the (even, odd) real-k entries of the 2x2 block column the lane reads.
   // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
@@ -111,10 +114,9 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   const int a_part = lane >> 5;
   const int jcol = lane & 31;
   const int bcol = jcol & 1;
-  const int b_src = (a_part == bcol) ? 0 : 1;  // br on the block diagonal, bi off it
-  float b_sign = 1.f;
-  if (CONJ && a_part == 0 && bcol == 1) b_sign = -1.f;
-  if (!CONJ && a_part == 1 && bcol == 0) b_sign = -1.f;
+  // br on the block diagonal, +bi or -bi off it
+  const bool neg = CONJ ? (a_part == 0 && bcol == 1) : (a_part == 1 && bcol == 0);
+  const int b_poff = (a_part == bcol) ? 0 : neg ? 2 * PB + 16 : PB;
 
   floatx16 acc[MI][NJ];
 #pragma unroll
@@ -140,22 +142,39 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     if (B_NC) { k = e / (BN / 2); n = (e - k * (BN / 2)) * 2; }
     else { n = e >> 3; k = (e & 7) * 2; }
   };
+  // per-thread load geometry, fixed over the k loop: per stage each offset
+  // is one add and one select (no branch)
+  unsigned a_base[AV], b_base[BV];
+  int a_kk[AV], b_kk[BV];
+  bool a_in[AV], b_in[BV];
+#pragma unroll
+  for (int q = 0; q < AV; ++q) {
+    int m, k;
+    a_pos(q, m, k);
+    a_in[q] = m0 + m < g.M;
+    a_kk[q] = k;
+    a_base[q] = (unsigned)(m0 + m) * g.sAm + (unsigned)k * g.sAk;
+  }
+#pragma unroll
+  for (int q = 0; q < BV; ++q) {
+    int k, n;
+    b_pos(q, k, n);
+    b_in[q] = n0 + n < g.N;
+    b_kk[q] = k;
+    b_base[q] = (unsigned)k * g.sBk + (unsigned)(n0 + n) * g.sBn;
+  }
   auto load = [&](int k0, V* ra, V* rb) {
+    const int lim = kend - k0;
+    const unsigned ka = (unsigned)k0 * g.sAk, kb = (unsigned)k0 * g.sBk;
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
-      int m, k;
-      a_pos(q, m, k);
-      const bool in = (m0 + m < g.M) && (k0 + k < kend);
-      const unsigned off = in ? (unsigned)(m0 + m) * g.sAm + (unsigned)(k0 + k) * g.sAk : 0u;
-      ra[q] = *reinterpret_cast<const V*>(Ab + off);
+      const bool in = a_in[q] & (a_kk[q] < lim);
+      ra[q] = *reinterpret_cast<const V*>(Ab + (in ? a_base[q] + ka : 0u));
     }
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
-      int k, n;
-      b_pos(q, k, n);
-      const bool in = (n0 + n < g.N) && (k0 + k < kend);
-      const unsigned off = in ? (unsigned)(k0 + k) * g.sBk + (unsigned)(n0 + n) * g.sBn : 0u;
-      rb[q] = *reinterpret_cast<const V*>(Bb + off);
+      const bool in = b_in[q] & (b_kk[q] < lim);
+      rb[q] = *reinterpret_cast<const V*>(Bb + (in ? b_base[q] + kb : 0u));
     }
   };
   // the two forms of a stored value w = (br, bi): conj block [[br, -bi], [bi, br]],
@@ -221,6 +240,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
       }
       float* b0 = Bs[grp][buf];
       float* b1 = Bs[grp][buf] + PB;
+      float* b2 = Bs[grp][buf] + 2 * PB + 16;
 #pragma unroll
       for (int q = 0; q < BV; ++q) {
         int k, n;
@@ -229,9 +249,10 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
         if (B_NC) {
           *reinterpret_cast<float2*>(b0 + k * SB + n) = make_float2(r.x, r.z);
           *reinterpret_cast<float2*>(b1 + k * SB + n) = make_float2(r.y, r.w);
+          *reinterpret_cast<float2*>(b2 + k * SB + n) = make_float2(-r.y, -r.w);
         } else {
-          b0[k * SB + n] = r.x; b1[k * SB + n] = r.y;
-          b0[(k + 1) * SB + n] = r.z; b1[(k + 1) * SB + n] = r.w;
+          b0[k * SB + n] = r.x; b1[k * SB + n] = r.y; b2[k * SB + n] = -r.y;
+          b0[(k + 1) * SB + n] = r.z; b1[(k + 1) * SB + n] = r.w; b2[(k + 1) * SB + n] = -r.w;
         }
       }
     }
@@ -273,7 +294,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     }
     // all fragments of the stage first, so the LDS reads overlap the MFMAs
     const float* ap = As[grp][buf] + a_part * PA + wm + jcol;
-    const float* bp = Bs[grp][buf] + b_src * PB + wn + (jcol >> 1);
+    const float* bp = Bs[grp][buf] + b_poff + wn + (jcol >> 1);
     float av[kBK][MI], bv[kBK][NJ];
 #pragma unroll
     for (int s = 0; s < kBK; ++s) {
@@ -288,7 +309,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[s][i], b_sign * bv[s][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[s][i], bv[s][j], acc[i][j], 0, 0, 0);
   };
 
   // stage st sits in LDS buffer st % 2; register set st % 2 receives stage
