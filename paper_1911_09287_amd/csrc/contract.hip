@@ -15,10 +15,10 @@
 // in a 2x2 grid; a wave owns BM/2 rows x BN/2 complex columns.  Operands are
 // staged in LDS as separate real and imaginary planes (B also as its negated
 // imaginary plane, so that each lane reads its block entry as is), k-major,
-// with rows padded by 4 floats and planes offset by half or a quarter of the
-// banks, so that the MFMA operand fetches (one 32-bit read per lane) and the
-// stores are free of bank conflicts.  Blocks are numbered so that consecutive
-// tiles (which share operand rows) run on the same XCD and its L2.
+// with padded rows and planes offset by half or a quarter of the banks, so
+// that the MFMA operand fetches (one 32-bit read per lane) are free of bank
+// conflicts.  Blocks are numbered so that consecutive tiles (which share
+// operand rows) run on the same XCD and its L2.
 //
 // With bfloat16 storage of the spectra the operands arrive as 32-bit (re, im)
 // pairs (8-byte vectors, two values each) and run on v_mfma_f32_32x32x8_bf16,
@@ -49,10 +49,11 @@ struct CgemmArgs {
 
 constexpr int kBK = 16;  // complex k per stage
 
-// LDS plane of R rows of W floats: padded rows, plane size = 32 (mod 64) floats.
+// LDS plane of kBK rows of W floats: the smallest size of at least the rows
+// that is 32 (mod 64) floats, so that consecutive planes sit half the banks apart.
 template <int W>
 constexpr int plane_floats() {
-  return ((kBK * (W + 4) + 63) / 64) * 64 + 32;
+  return kBK * W + ((32 - kBK * W % 64) + 64) % 64;
 }
 
 typedef short shortx4 __attribute__((ext_vector_type(4)));
@@ -79,12 +80,15 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   constexpr int NJ = WN / 16;  // 16-complex-column MFMA blocks per wave
   constexpr int AV = BM / 32;  // 16-byte A loads per thread per stage
   constexpr int BV = BN / 32;  // 16-byte B loads per thread per stage
-  constexpr int SA = BM + 4, SB = BN + 4;  // padded row lengths
-  constexpr int PA = plane_floats<BM>(), PB = plane_floats<BN>();
-  __shared__ float As[KS][BF16 ? 1 : 2][BF16 ? 1 : 2 * PA];
+  // rows padded by 2 floats: the 64 x 32 tile's buffers then take 30 KB, so
+  // that five blocks fit one CU's LDS
+  constexpr int SA = BM + 2, SB = BN + 2;
+  constexpr int PA = plane_floats<SA>(), PB = plane_floats<SB>();
+  constexpr int ABUF = PA + kBK * SA, BBUF = 2 * PB + 16 + kBK * SB;  // floats per stage buffer
+  __shared__ float As[KS][BF16 ? 1 : 2][BF16 ? 1 : ABUF];
   // B planes: re at 0, im at PB (half the banks away), -im at 2 PB + 16 (a
   // quarter of the banks away from both), so that no lane negates a value
-  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : 3 * PB + 16];
+  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : BBUF];
   // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
   // the (even, odd) real-k entries of the 2x2 block column the lane reads.
   // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
@@ -344,7 +348,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     // groups 1.. leave their sums in the (now idle) operand buffers; group 0
     // adds them in group order and stores the tile
     constexpr int kAcc = 256 * MI * NJ * 16;  // floats per group
-    static_assert((KS - 1) * kAcc <= KS * 2 * 2 * PA, "reduction buffer");
+    static_assert((KS - 1) * kAcc <= KS * 2 * ABUF, "reduction buffer");
     float* red = &As[0][0][0];
     if (grp > 0) {
 #pragma unroll
@@ -377,7 +381,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
       // padded to 40 floats: the two half-waves' rows land on disjoint banks),
       // so that each lane stores 16 bytes: two complex columns of one row
       float* st = &As[0][0][0] + wave * (16 * 40);
-      static_assert(4 * 16 * 40 <= KS * 2 * 2 * PA, "store staging");
+      static_assert(4 * 16 * 40 <= KS * 2 * ABUF, "store staging");
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
