@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay per-layer HIP graphs instead of launching every kernel from the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate-backward", action="store_true",
+                    help="backward as the two calls (grad-input, grad-weight) instead of the combined one")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--table", default=None, help="also write a per-config/per-c table (JSON lines) here")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -80,8 +82,9 @@ def parse():
 class Layer:
     """Device state of one layer: plan, inputs, outputs and workspace."""
 
-    def __init__(self, torch, blconv, layer, arrays, c, dev, desc_flags=0):
+    def __init__(self, torch, blconv, layer, arrays, c, dev, desc_flags=0, separate_backward=False):
         self.layer = layer
+        self.separate_backward = separate_backward
         self.plan = blconv.plan_for_layer(layer, c, None, desc_flags)
         x, w, dy = arrays
         self.x, self.w, self.dy = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
@@ -94,8 +97,13 @@ class Layer:
     def step(self):
         b = self.blconv
         self.plan.forward(self.x, self.w, self.y, self.ws)
-        self.plan.backward_input(self.dy, self.w, self.dx, self.ws, flags=b.BL_REUSE_W)
-        self.plan.backward_weight(self.x, self.dy, self.dw, self.ws, flags=b.BL_REUSE_X | b.BL_REUSE_DY)
+        if self.separate_backward:
+            self.plan.backward_input(self.dy, self.w, self.dx, self.ws, flags=b.BL_REUSE_W)
+            self.plan.backward_weight(self.x, self.dy, self.dw, self.ws, flags=b.BL_REUSE_X | b.BL_REUSE_DY)
+            return
+        # both gradients in one call: the grad-input and grad-weight
+        # contractions share one launch where their tiles agree
+        self.plan.backward(self.dy, None, None, self.dx, self.dw, self.ws, flags=b.BL_REUSE_W | b.BL_REUSE_X)
 
 
 def capture(torch, layers):
@@ -214,7 +222,8 @@ def roofline(agg):
 
 KERNEL_SOURCES = {"spec_fwd_1d": "bluestein.hip", "spec_inv_1d": "bluestein.hip", "spec_fwd_2d": "fft2d.hip",
                   "spec_inv_2d": "fft2d.hip", "contract_fwd": "contract.hip", "contract_dgrad": "contract.hip",
-                  "contract_wgrad": "contract.hip", "wgrad_idft": "direct.hip", "spec_filt": "direct.hip"}
+                  "contract_wgrad": "contract.hip", "contract_bwd": "contract.hip", "wgrad_idft": "direct.hip",
+                  "spec_filt": "direct.hip"}
 
 
 def measured_traffic(kernel, workload):
@@ -302,7 +311,7 @@ def main():
         return cf, arr, sum(3 * L.direct_flops() for L in cf.layers)
 
     def build(cf, arr, c, desc_flags=0):
-        return [Layer(torch, blconv, L, a, c, dev, desc_flags) for L, a in zip(cf.layers, arr)]
+        return [Layer(torch, blconv, L, a, c, dev, desc_flags, args.separate_backward) for L, a in zip(cf.layers, arr)]
 
     def graphs_for(Ls):
         if not args.graph:
@@ -400,6 +409,7 @@ def main():
         "extra_workload": extra,
         "wall_s_timed": wall,
         "launch": "hip_graph per layer" if args.graph else "eager",
+        "backward": "two calls (grad-input, grad-weight)" if args.separate_backward else "one call (both gradients)",
     }
     print(json.dumps(out), flush=True)
 

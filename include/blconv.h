@@ -132,13 +132,14 @@ typedef struct bl_conv_plan_s* bl_conv_plan_t;
 /* Flags of the compute calls (map reuse, Sec. 3.2.3).  Every compute call
  * leaves in the workspace the spectra it computed: forward the input spectrum
  * X and the filter spectrum W, backward_input the output-gradient spectrum DY
- * and W, backward_weight X and DY.  A REUSE flag skips recomputing that
+ * and W, backward_weight X and DY, backward all three.  A REUSE flag skips
+ * recomputing that
  * spectrum and reads the copy in the workspace instead; the caller asserts that
  * the tensor it came from has not changed since, which the library cannot
  * check.  The tensor pointer may then be NULL. */
-#define BL_REUSE_X  0x1u  /* forward, backward_weight: reuse X */
-#define BL_REUSE_W  0x2u  /* forward, backward_input: reuse W */
-#define BL_REUSE_DY 0x4u  /* backward_weight: reuse DY */
+#define BL_REUSE_X  0x1u  /* forward, backward_weight, backward: reuse X */
+#define BL_REUSE_W  0x2u  /* forward, backward_input, backward: reuse W */
+#define BL_REUSE_DY 0x4u  /* backward_weight, backward: reuse DY */
 
 /* Build a plan: geometry, the number of peeled layers t for rate c, the kept
  * bin set and the workspace layout.  Host only.  BL_ERR_UNSUPPORTED for
@@ -187,6 +188,18 @@ bl_status_t bl_conv_backward_input(bl_conv_plan_t plan, const float* dy, const f
  * cropped to the K x K filter support.  Writes X and DY to ws. */
 bl_status_t bl_conv_backward_weight(bl_conv_plan_t plan, const float* x, const float* dy, float* dw,
                                     void* ws, unsigned flags, void* stream);
+
+/* Both gradients of one layer (Sec. 3.2.3): dx as bl_conv_backward_input and
+ * dw as bl_conv_backward_weight compute them, from one output-gradient
+ * spectrum DY.  The two per-bin contractions run as one launch when both use
+ * the tiled kernel with one tile shape, no k split and sums of the same length
+ * (C_out = N: their tiles then share the GPU), else one after the other;
+ * either way every output element is the same sum, in the same order, as in
+ * the separate calls with the same tile shape.  Writes DY, W and X to ws; flags: any of BL_REUSE_X, BL_REUSE_W,
+ * BL_REUSE_DY (the tensor may then be NULL).  dx, dw and ws may not be NULL;
+ * errors as the other compute calls. */
+bl_status_t bl_conv_backward(bl_conv_plan_t plan, const float* dy, const float* w, const float* x, float* dx,
+                             float* dw, void* ws, unsigned flags, void* stream);
 
 /* Forward pass that allocates nothing, for callers that cannot allocate
  * device memory: code under HIP graph capture, tight serving loops, harnesses

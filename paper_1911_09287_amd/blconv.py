@@ -34,7 +34,7 @@ EXPORTED = (
     "bl_conv_backward_input", "bl_conv_backward_weight", "bl_status_string", "bl_profile_begin",
     "bl_profile_end", "bl_profile_count", "bl_profile_get", "bl_profile_release", "bl_conv_input_energy",
     "bl_conv_rate_for_energy", "bl_conv_zero_smallest", "bl_conv_fine_band_for_energy", "bl_conv_zero_bins",
-    "bl_conv_forward_noalloc",
+    "bl_conv_forward_noalloc", "bl_conv_backward",
 )
 
 
@@ -80,6 +80,7 @@ def load():
     for name in ("bl_conv_forward", "bl_conv_backward_input", "bl_conv_backward_weight"):
         getattr(lib, name).argtypes = [P, P, P, P, P, U, P]
     lib.bl_conv_forward_noalloc.argtypes = [P, P, P, P, P]
+    lib.bl_conv_backward.argtypes = [P, P, P, P, P, P, P, U, P]
     lib.bl_conv_input_energy.argtypes = [P, P, P, U, P, P]
     lib.bl_conv_rate_for_energy.argtypes = [P, P, S, D, ctypes.POINTER(I), ctypes.POINTER(D), ctypes.POINTER(D)]
     lib.bl_conv_zero_smallest.argtypes = [P, P, P, U, ctypes.c_longlong, U, P]
@@ -237,6 +238,13 @@ class Plan:
     def backward_weight(self, x, dy, dw, ws, flags=0, stream=None):
         _check("bl_conv_backward_weight", self._lib.bl_conv_backward_weight(
             self._h, self._ptr(x, self.x_shape(), "x"), self._ptr(dy, self.y_shape(), "dy"),
+            self._ptr(dw, self.w_shape(), "dw"), self._ws(ws), flags, self._stream(stream)))
+
+    def backward(self, dy, w, x, dx, dw, ws, flags=0, stream=None):
+        """Both gradients (bl_conv_backward)."""
+        _check("bl_conv_backward", self._lib.bl_conv_backward(
+            self._h, self._ptr(dy, self.y_shape(), "dy"), self._ptr(w, self.w_shape(), "w"),
+            self._ptr(x, self.x_shape(), "x"), self._ptr(dx, self.x_shape(), "dx"),
             self._ptr(dw, self.w_shape(), "dw"), self._ws(ws), flags, self._stream(stream)))
 
     def input_energy(self, x, ws, energy=None, flags=0, stream=None):

@@ -142,6 +142,34 @@ extern "C" bl_status_t bl_conv_backward_weight(bl_conv_plan_t p, const float* x,
   return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
 }
 
+extern "C" bl_status_t bl_conv_backward(bl_conv_plan_t p, const float* dy, const float* w, const float* x,
+                                        float* dx, float* dw, void* ws, unsigned flags, void* stream) {
+  if (!p || !dx || !dw || !ws) return BL_ERR_INVALID_ARG;
+  if (flags & ~(BL_REUSE_X | BL_REUSE_W | BL_REUSE_DY)) return BL_ERR_INVALID_ARG;
+  if ((!(flags & BL_REUSE_DY) && !dy) || (!(flags & BL_REUSE_W) && !w) || (!(flags & BL_REUSE_X) && !x))
+    return BL_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* X = spec_at(ws, p->off_X);
+  void* Wf = spec_at(ws, p->off_W);
+  void* DY = spec_at(ws, p->off_DY);
+  float2* T = ws_at(ws, p->off_T);
+  float2* DW = ws_at(ws, p->off_DW);
+  if (!(flags & BL_REUSE_DY))
+    BL_TRY(launch_spec_fwd(p, dy, DY, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s));
+  if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
+  if (!(flags & BL_REUSE_X))
+    BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  const bl_status_t st = launch_contract_bwd_pair(p, DY, Wf, T, X, DW, s);
+  if (st == BL_ERR_UNSUPPORTED) {
+    BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, ws_at(ws, p->off_CPart), s));
+    BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, ws_at(ws, p->off_CPart), s));
+  } else if (st != BL_OK) {
+    return st;
+  }
+  BL_TRY(launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
+  return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
+}
+
 // ---------------------------------------------------------------------------
 // Forward pass without any allocation: the spectra live in a fixed static
 // device array instead of a caller workspace.

@@ -115,6 +115,12 @@ bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const void*
 bool contract_is_thin(const bl_conv_plan_s* p, Contract which);
 bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                  float2* O, hipStream_t s);
+// Grad-input (DX = DY W) and grad-weight (DW = X^T conj(DY)) contractions in
+// one launch when both run on the tiled kernel with one tile shape, no k split
+// and the same number of k stages; BL_ERR_UNSUPPORTED (nothing enqueued)
+// otherwise.
+bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, const void* W, float2* DX,
+                                     const void* X, float2* DW, hipStream_t s);
 // Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
 // generic one (any strides and sizes).
 bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,

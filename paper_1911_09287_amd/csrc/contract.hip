@@ -65,10 +65,29 @@ typedef short shortx4 __attribute__((ext_vector_type(4)));
 // k-stages q, q + KS, ... through its own LDS buffers, and the groups' sums are
 // added through LDS in group order at the end.  Used when the launch has no
 // more tiles than compute units, so that each SIMD runs KS waves instead of one.
+// LDS layout of one tile's stage buffers (floats).
+template <int BM, int BN, bool BF16, int KS>
+struct CgemmLds {
+  // rows padded by 2 floats: the 64 x 32 tile's buffers then take 30 KB, so
+  // that five blocks fit one CU's LDS
+  static constexpr int SA = BM + 2, SB = BN + 2;
+  static constexpr int PA = plane_floats<SA>(), PB = plane_floats<SB>();
+  static constexpr int ABUF = PA + kBK * SA, BBUF = 2 * PB + 16 + kBK * SB;  // floats per stage buffer
+  // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
+  // the (even, odd) real-k entries of the 2x2 block column the lane reads.
+  // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
+  // in disjoint banks; the form planes are 16 (mod 64) words apart.
+  static constexpr int SA16 = BM + 16, SB16 = BN + 16;
+  static constexpr int PB16 = ((kBK * SB16 + 63) / 64) * 64 + 16;
+  static constexpr int floats = BF16 ? 2 * kBK * SA16 + 2 * 2 * PB16 : KS * 2 * (ABUF + BBUF);
+};
+
+// One output tile: tile id (bin-major over the launch's tiles) and k-split kz,
+// with the stage buffers in smem (CgemmLds floats, 16-byte aligned).
 template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16, int KS>
-__global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void* __restrict__ A_,
-                                                                   const void* __restrict__ B_,
-                                                                   float2* __restrict__ O, CgemmArgs g) {
+__device__ __forceinline__ void cgemm_tile(const void* __restrict__ A_, const void* __restrict__ B_,
+                                           float2* __restrict__ O, const CgemmArgs& g, unsigned id, int kz,
+                                           float* smem) {
   static_assert(KS == 1 || !BF16, "the in-block k split is built for the fp32 operands");
   using S = std::conditional_t<BF16, unsigned, float2>;  // stored operand element
   using V = std::conditional_t<BF16, uint2, float4>;     // two consecutive elements
@@ -80,31 +99,21 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   constexpr int NJ = WN / 16;  // 16-complex-column MFMA blocks per wave
   constexpr int AV = BM / 32;  // 16-byte A loads per thread per stage
   constexpr int BV = BN / 32;  // 16-byte B loads per thread per stage
-  // rows padded by 2 floats: the 64 x 32 tile's buffers then take 30 KB, so
-  // that five blocks fit one CU's LDS
-  constexpr int SA = BM + 2, SB = BN + 2;
-  constexpr int PA = plane_floats<SA>(), PB = plane_floats<SB>();
-  constexpr int ABUF = PA + kBK * SA, BBUF = 2 * PB + 16 + kBK * SB;  // floats per stage buffer
-  __shared__ float As[KS][BF16 ? 1 : 2][BF16 ? 1 : ABUF];
-  // B planes: re at 0, im at PB (half the banks away), -im at 2 PB + 16 (a
-  // quarter of the banks away from both), so that no lane negates a value
-  __shared__ float Bs[KS][BF16 ? 1 : 2][BF16 ? 1 : BBUF];
-  // bf16 operands: A as packed (re, im) pairs [k][m]; B in two forms [form][k][n],
-  // the (even, odd) real-k entries of the 2x2 block column the lane reads.
-  // Row strides of 16 (mod 32) words put the two half-waves' rows (k and k + 2)
-  // in disjoint banks; the form planes are 16 (mod 64) words apart.
-  constexpr int SA16 = BM + 16, SB16 = BN + 16;
-  constexpr int PB16 = ((kBK * SB16 + 63) / 64) * 64 + 16;
-  __shared__ unsigned As16[BF16 ? 2 : 1][BF16 ? kBK * SA16 : 1];
-  __shared__ unsigned Bs16[BF16 ? 2 : 1][BF16 ? 2 * PB16 : 1];
+  using L = CgemmLds<BM, BN, BF16, KS>;
+  constexpr int SA = L::SA, SB = L::SB, PA = L::PA, PB = L::PB, ABUF = L::ABUF, BBUF = L::BBUF;
+  constexpr int SA16 = L::SA16, SB16 = L::SB16, PB16 = L::PB16;
+  // fp32: A buffers [group][stage buffer] of ABUF floats, then B buffers of
+  // BBUF; B planes: re at 0, im at PB (half the banks away), -im at 2 PB + 16
+  // (a quarter of the banks away from both), so that no lane negates a value.
+  // bf16: A buffers [2][kBK SA16] words, then B buffers [2][2 PB16].
+  auto As = [&](int gq, int b) { return smem + (gq * 2 + b) * ABUF; };
+  auto Bs = [&](int gq, int b) { return smem + KS * 2 * ABUF + (gq * 2 + b) * BBUF; };
+  auto As16 = [&](int b) { return reinterpret_cast<unsigned*>(smem) + b * kBK * SA16; };
+  auto Bs16 = [&](int b) { return reinterpret_cast<unsigned*>(smem) + 2 * kBK * SA16 + b * 2 * PB16; };
 
-  // XCD-aware numbering: the hardware deals blocks to the 8 XCDs in turn
-  const unsigned nb = gridDim.x * gridDim.y;
-  unsigned id = blockIdx.x + blockIdx.y * gridDim.x;
-  if (nb % 8 == 0) id = (id % 8) * (nb / 8) + id / 8;
   const int bin = id / g.tiles;
   const int tile = id - bin * g.tiles;
-  const int kbeg = blockIdx.z * g.kper;
+  const int kbeg = kz * g.kper;
   const int kend = min(g.K, kbeg + g.kper);
   const int tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
@@ -194,7 +203,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   // consecutive columns of rows 4q + {0, 1, 2, 3}) stay conflict-free.
   auto swz = [](int k) { return 8 * ((k >> 2) & 3); };
   auto store16 = [&](int buf, int k0, const V* ra, const V* rb) {
-    unsigned* a16 = As16[buf];
+    unsigned* a16 = As16(buf);
 #pragma unroll
     for (int q = 0; q < AV; ++q) {
       int m, k;
@@ -209,7 +218,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
         a16[k * SA16 + ms + 1] = r.y;  // m even: (m + 1) ^ swz = ms + 1
       }
     }
-    unsigned* b16 = Bs16[buf];
+    unsigned* b16 = Bs16(buf);
 #pragma unroll
     for (int q = 0; q < BV; ++q) {
       int k, n;
@@ -227,8 +236,8 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     if constexpr (BF16) {
       store16(buf, k0, ra, rb);
     } else {
-      float* a0 = As[grp][buf];
-      float* a1 = As[grp][buf] + PA;
+      float* a0 = As(grp, buf);
+      float* a1 = As(grp, buf) + PA;
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         int m, k;
@@ -242,9 +251,9 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
           *reinterpret_cast<float2*>(a1 + k * SA + m) = make_float2(r.y, r.w);
         }
       }
-      float* b0 = Bs[grp][buf];
-      float* b1 = Bs[grp][buf] + PB;
-      float* b2 = Bs[grp][buf] + 2 * PB + 16;
+      float* b0 = Bs(grp, buf);
+      float* b1 = Bs(grp, buf) + PB;
+      float* b2 = Bs(grp, buf) + 2 * PB + 16;
 #pragma unroll
       for (int q = 0; q < BV; ++q) {
         int k, n;
@@ -265,8 +274,8 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     // v_mfma_f32_32x32x8_bf16: lane l supplies real k = 4 (l / 32) .. + 3 of its
     // row (A) or column (B), i.e. complex k = 2 (l / 32) and 2 (l / 32) + 1 of
     // the four complex k an instruction consumes
-    const unsigned* a16 = As16[buf];
-    const unsigned* b16 = Bs16[buf] + bcol * PB16;
+    const unsigned* a16 = As16(buf);
+    const unsigned* b16 = Bs16(buf) + bcol * PB16;
 #pragma unroll
     for (int q = 0; q < kBK / 4; ++q) {
       const int kc = 4 * q + 2 * a_part;
@@ -297,8 +306,8 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
       return;
     }
     // all fragments of the stage first, so the LDS reads overlap the MFMAs
-    const float* ap = As[grp][buf] + a_part * PA + wm + jcol;
-    const float* bp = Bs[grp][buf] + b_poff + wn + (jcol >> 1);
+    const float* ap = As(grp, buf) + a_part * PA + wm + jcol;
+    const float* bp = Bs(grp, buf) + b_poff + wn + (jcol >> 1);
     float av[kBK][MI], bv[kBK][NJ];
 #pragma unroll
     for (int s = 0; s < kBK; ++s) {
@@ -349,7 +358,7 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     // adds them in group order and stores the tile
     constexpr int kAcc = 256 * MI * NJ * 16;  // floats per group
     static_assert((KS - 1) * kAcc <= KS * 2 * ABUF, "reduction buffer");
-    float* red = &As[0][0][0];
+    float* red = smem;
     if (grp > 0) {
 #pragma unroll
       for (int i = 0; i < MI; ++i)
@@ -374,13 +383,13 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
   }
 
   // D[i][j] of a 32x32 block: VGPR v holds row 8 (v / 4) + 4 (lane / 32) + v % 4, real column lane % 32.
-  float* Of = reinterpret_cast<float*>(O + blockIdx.z * g.split_stride + bin * g.bO);
+  float* Of = reinterpret_cast<float*>(O + kz * g.split_stride + bin * g.bO);
   if constexpr (!BF16) {
     if (g.ldo % 2 == 0 && g.N % 2 == 0) {
       // through the idle operand buffers, 16 rows of a block at a time (rows
       // padded to 40 floats: the two half-waves' rows land on disjoint banks),
       // so that each lane stores 16 bytes: two complex columns of one row
-      float* st = &As[0][0][0] + wave * (16 * 40);
+      float* st = smem + wave * (16 * 40);
       static_assert(4 * 16 * 40 <= KS * 2 * ABUF, "store staging");
 #pragma unroll
       for (int i = 0; i < MI; ++i)
@@ -418,6 +427,39 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
     }
 }
 
+// XCD-aware numbering of a launch's nb blocks: the hardware deals blocks to
+// the 8 XCDs in turn, so consecutive logical ids (tiles of one bin, which
+// share operand rows) land on one XCD and its L2.
+__device__ __forceinline__ unsigned xcd_block_id(unsigned raw, unsigned nb) {
+  return nb % 8 == 0 ? (raw % 8) * (nb / 8) + raw / 8 : raw;
+}
+
+template <int BM, int BN, bool A_KC, bool B_NC, bool CONJ, bool BF16, int KS>
+__global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void* __restrict__ A_,
+                                                                   const void* __restrict__ B_,
+                                                                   float2* __restrict__ O, CgemmArgs g) {
+  __shared__ __align__(16) float smem[CgemmLds<BM, BN, BF16, KS>::floats];
+  const unsigned id = xcd_block_id(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+  cgemm_tile<BM, BN, A_KC, B_NC, CONJ, BF16, KS>(A_, B_, O, g, id, blockIdx.z, smem);
+}
+
+// The grad-input and grad-weight contractions of a layer in one launch (both
+// need only the stored spectra): logical blocks [0, n1) take grad-input tiles
+// (DX = DY W), the rest grad-weight tiles (DW = X^T conj(DY)), one tile shape.
+// One launch instead of two, and the two passes' tiles share the CUs.
+template <int BM, int BN, bool BF16>
+__global__ __launch_bounds__(256, 2) void k_cgemm_bwd(const void* __restrict__ A1, const void* __restrict__ B1,
+                                                     float2* __restrict__ O1, CgemmArgs g1,
+                                                     const void* __restrict__ A2, const void* __restrict__ B2,
+                                                     float2* __restrict__ O2, CgemmArgs g2, unsigned n1) {
+  __shared__ __align__(16) float smem[CgemmLds<BM, BN, BF16, 1>::floats];
+  const unsigned id = xcd_block_id(blockIdx.x, gridDim.x);
+  if (id < n1)
+    cgemm_tile<BM, BN, true, false, false, BF16, 1>(A1, B1, O1, g1, id, 0, smem);
+  else
+    cgemm_tile<BM, BN, false, true, true, BF16, 1>(A2, B2, O2, g2, id - n1, 0, smem);
+}
+
 // out[i] = sum over k-splits of part[s][i], in split order.
 __global__ __launch_bounds__(256) void k_split_reduce(const float4* __restrict__ part, float4* __restrict__ out,
                                                       unsigned long long n4, int splits) {
@@ -431,13 +473,10 @@ __global__ __launch_bounds__(256) void k_split_reduce(const float4* __restrict__
   out[i] = acc;
 }
 
-}  // namespace
-
-// Tiled path: needs 16-byte aligned pairs of complex values along the
-// contiguous dimension of each operand; returns BL_ERR_UNSUPPORTED otherwise.
-bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
-                                  float2* O, float2* part, hipStream_t s) {
-  CgemmArgs g{};
+// Operand geometry of one pass for the tiled kernel; false when its 16-byte
+// pairs do not align or a bin's matrices need 64-bit offsets.
+bool tiled_args(const bl_conv_plan_s* p, Contract which, CgemmArgs& g) {
+  g = CgemmArgs{};
   const unsigned long long B = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
   bool a_kc = true, b_nc = true;
   switch (which) {
@@ -463,9 +502,33 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   // alignment of every 2-complex vector: even strides, even sizes along the vector
   const bool a_ok = (g.bA % 2 == 0) && (a_kc ? (g.sAm % 2 == 0 && g.K % 2 == 0) : (g.sAk % 2 == 0 && g.M % 2 == 0));
   const bool b_ok = (g.bB % 2 == 0) && (b_nc ? (g.sBk % 2 == 0 && g.N % 2 == 0) : (g.sBn % 2 == 0 && g.K % 2 == 0));
-  if (!a_ok || !b_ok || B > 65535) return BL_ERR_UNSUPPORTED;
+  if (!a_ok || !b_ok || B > 65535) return false;
   const long most = std::max<long>({(long)g.M * g.K, (long)g.K * g.N, (long)g.M * g.N});
-  if (2 * most >= 2147483647L) return BL_ERR_UNSUPPORTED;  // 32-bit offsets within a bin
+  return 2 * most < 2147483647L;  // 32-bit offsets within a bin
+}
+
+double pass_bytes(const bl_conv_plan_s* p, const CgemmArgs& g) {
+  const double ob = p->bf16 ? 4.0 : 8.0;  // bytes per stored operand element
+  return (double)p->kept * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
+}
+
+// Tile counts of a pass on BM x BN tiles, one k range.
+void whole_k_tiles(CgemmArgs& g, int BM, int BN) {
+  g.tiles_n = (g.N + BN - 1) / BN;
+  g.tiles = ((g.M + BM - 1) / BM) * g.tiles_n;
+  g.kper = (g.K + kBK - 1) / kBK * kBK;
+  g.split_stride = 0;
+}
+
+}  // namespace
+
+// Tiled path: needs 16-byte aligned pairs of complex values along the
+// contiguous dimension of each operand; returns BL_ERR_UNSUPPORTED otherwise.
+bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
+                                  float2* O, float2* part, hipStream_t s) {
+  CgemmArgs g;
+  if (!tiled_args(p, which, g)) return BL_ERR_UNSUPPORTED;
+  const unsigned long long B = p->kept;
   const BlContractTiling& t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
   const int BM = t.bm, BN = t.bn;
   const int tiles_m = (g.M + BM - 1) / BM;
@@ -482,8 +545,7 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   // (tile, bin) pairs as a 2-D grid; the kernel renumbers them per XCD
   dim3 grid((unsigned)g.tiles, (unsigned)B, (unsigned)splits);
   const double flops = 8.0 * B * g.M * g.N * g.K;
-  const double ob = p->bf16 ? 4.0 : 8.0;  // bytes per stored operand element
-  const double bytes = B * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
+  const double bytes = pass_bytes(p, g);
   const char* name = which == Contract::Forward ? "contract_fwd"
                      : which == Contract::GradInput ? "contract_dgrad" : "contract_wgrad";
   bl_status_t st = BL_ERR_UNSUPPORTED;
@@ -517,6 +579,44 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
     hipExtLaunchKernelGGL(k_split_reduce, dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0,
                        reinterpret_cast<const float4*>(part), reinterpret_cast<float4*>(O), n4, splits);
   });
+}
+
+bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, const void* W, float2* DX,
+                                     const void* X, float2* DW, hipStream_t s) {
+  if (contract_is_thin(p, Contract::GradInput) || contract_is_thin(p, Contract::GradWeight)) return BL_ERR_UNSUPPORTED;
+  const BlContractTiling &t1 = p->ct[1], &t2 = p->ct[2];
+  if (t1.bm != t2.bm || t1.bn != t2.bn || t1.splits != 1 || t2.splits != 1) return BL_ERR_UNSUPPORTED;
+  CgemmArgs g1, g2;
+  if (!tiled_args(p, Contract::GradInput, g1) || !tiled_args(p, Contract::GradWeight, g2)) return BL_ERR_UNSUPPORTED;
+  // tiles of both passes must take about the same time: with unequal k
+  // lengths the long tiles end up sharing CUs with short ones and finish last
+  // (measured: a 4-fold k ratio made the launch 70 % slower than two)
+  if ((g1.K + kBK - 1) / kBK != (g2.K + kBK - 1) / kBK) return BL_ERR_UNSUPPORTED;
+  const int BM = t1.bm, BN = t1.bn;
+  whole_k_tiles(g1, BM, BN);
+  whole_k_tiles(g2, BM, BN);
+  const unsigned long long n1 = (unsigned long long)g1.tiles * p->kept, n2 = (unsigned long long)g2.tiles * p->kept;
+  if (n1 + n2 >= 2147483647ULL) return BL_ERR_UNSUPPORTED;
+  const double flops = 8.0 * p->kept * ((double)g1.M * g1.N * g1.K + (double)g2.M * g2.N * g2.K);
+  const double bytes = pass_bytes(p, g1) + pass_bytes(p, g2);
+  const dim3 grid((unsigned)(n1 + n2));
+  const unsigned n1u = (unsigned)n1;
+  bl_status_t st = BL_ERR_UNSUPPORTED;
+#define BL_GO(BMV, BNV)                                                                                         \
+  st = timed_launch("contract_bwd", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                       \
+    if (p->bf16)                                                                                                \
+      hipExtLaunchKernelGGL((k_cgemm_bwd<BMV, BNV, true>), grid, dim3(256), 0, s, e0, e1, 0, DY, W, DX, g1, X, DY, \
+                            DW, g2, n1u);                                                                       \
+    else                                                                                                        \
+      hipExtLaunchKernelGGL((k_cgemm_bwd<BMV, BNV, false>), grid, dim3(256), 0, s, e0, e1, 0, DY, W, DX, g1, X,   \
+                            DY, DW, g2, n1u);                                                                   \
+  })
+  if (BM == 128 && BN == 64) BL_GO(128, 64);
+  else if (BM == 64 && BN == 64) BL_GO(64, 64);
+  else if (BM == 128 && BN == 32) BL_GO(128, 32);
+  else if (BM == 64 && BN == 32) BL_GO(64, 32);
+#undef BL_GO
+  return st;
 }
 
 }  // namespace blc

@@ -32,6 +32,7 @@ LIBRARY_NAMES = OrderedDict([
     ("contract_fwd", r"k_cgemm\w*<\d+, \d+, true, true, true, (false|true)(, \d+)?>"),
     ("contract_dgrad", r"k_cgemm\w*<\d+, \d+, true, false, false, (false|true)(, \d+)?>"),
     ("contract_wgrad", r"k_cgemm\w*<\d+, \d+, false, true, true, (false|true)(, \d+)?>"),
+    ("contract_bwd", r"k_cgemm_bwd<"),
     ("contract (thin, any pass)", r"k_thin_"),
     ("contract_reduce", r"k_split_reduce"),
     ("wgrad_idft", r"k_wgrad_wide<|k_wgrad_idft<|k_wgrad_tile<"),

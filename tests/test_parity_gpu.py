@@ -337,6 +337,60 @@ def test_contraction_shapes(torch):
         assert max(errs) <= TOL, errs
 
 
+def test_combined_backward(torch):
+    """bl_conv_backward (both gradients from one DY spectrum; the two
+    contractions in one launch where their tiles and sum lengths agree)
+    against the oracle, equal run to run and with or without reuse flags, and
+    within rounding of the separate backward calls: the ResNet stack at
+    c = 0.5 (one launch on the 128-channel layer, where C_out = N, two on the
+    others), a ragged layer, a 1-D layer and a bfloat16 plan (one launch)."""
+    # (layer, rate, plan flags, workload (config, layer) or None for random inputs)
+    cases = [(synth.WORKLOADS[3].layers[i], 0.5, 0, (3, i)) for i in range(4)]
+    cases += [(synth.Layer("ragged", 2, 70, 66, 130, 6, 6, 3, (1, 1, 1, 1), "blur"), 0.0, 0, None),
+              (synth.WORKLOADS[2].layers[1], 0.5, 0, (2, 1)),
+              (synth.Layer("bf_pair", 2, 64, 32, 64, 12, 12, 3, (1, 1, 1, 1), "blur"), 0.5,
+               blconv.BL_DESC_BF16_SPECTRA, None)]
+    dev = torch.device("cuda:0")
+    for i, (layer, c, flags, src) in enumerate(cases):
+        say(f"[backward] {layer.name} c={c} desc_flags={flags}")
+        x, w, dy = synth.layer_inputs(*src) if src else synth.random_inputs(layer, 2100 + i)
+        plan = blconv.plan_for_layer(layer, c, None, flags)
+        ws = plan.workspace(dev)
+        ws.fill_(0xFF)
+        xt, wt, dyt = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        outs = []
+        for reuse in (False, True, True):
+            dx = torch.full(plan.x_shape(), float("nan"), device=dev)
+            dw = torch.full(plan.w_shape(), float("nan"), device=dev)
+            if reuse:
+                plan.backward(None, None, None, dx, dw, ws,
+                              flags=blconv.BL_REUSE_X | blconv.BL_REUSE_W | blconv.BL_REUSE_DY)
+            else:
+                plan.backward(dyt, wt, xt, dx, dw, ws)
+            torch.cuda.synchronize()
+            outs.append((dx.cpu().numpy(), dw.cpu().numpy()))
+        for a, b in zip(outs[0], outs[1]):
+            assert np.array_equal(a, b)
+        for a, b in zip(outs[1], outs[2]):
+            assert np.array_equal(a, b)
+        sdx = torch.full(plan.x_shape(), float("nan"), device=dev)
+        sdw = torch.full(plan.w_shape(), float("nan"), device=dev)
+        plan.backward_input(dyt, wt, sdx, ws)
+        plan.backward_weight(xt, dyt, sdw, ws)
+        torch.cuda.synchronize()
+        sep = (sdx.cpu().numpy(), sdw.cpu().numpy())
+        rounding = bo.round_bf16 if flags else None
+        spatial = (layer.H,) if layer.ndim == 1 else (layer.H, layer.W)
+        ref = (bo.backward_input(dy, w, spatial, layer.pad, c, None, rounding),
+               bo.backward_weight(x, dy, layer.K, layer.pad, c, None, rounding))
+        errs = [err(a, b) for a, b in zip(outs[0], ref)]
+        gaps = [rel(a, b) for a, b in zip(outs[0], sep)]
+        say(f"    err vs oracle dx={errs[0]:.2e} dw={errs[1]:.2e}; vs separate calls {gaps}")
+        assert all(np.isfinite(a).all() for a in outs[0])
+        assert max(errs) <= (BF16_TOL if flags else TOL), errs
+        assert max(gaps) <= 1e-5, gaps
+
+
 def test_thin_contractions(torch):
     """Layers where a contraction size (batch, input or output channels) is at
     most 8, which run the memory-bound vector-ALU contraction: lanes over
@@ -684,27 +738,31 @@ def test_graph_replays_match_eager(torch):
         y = torch.empty(plan.y_shape(), device=dev)
         dx = torch.empty(plan.x_shape(), device=dev)
         dw = torch.empty(plan.w_shape(), device=dev)
+        dx2 = torch.empty(plan.x_shape(), device=dev)
+        dw2 = torch.empty(plan.w_shape(), device=dev)
 
         def step():
             plan.forward(x, w, y, ws)
             plan.backward_input(dy, w, dx, ws, flags=blconv.BL_REUSE_W)
             plan.backward_weight(x, dy, dw, ws, flags=blconv.BL_REUSE_X | blconv.BL_REUSE_DY)
+            plan.backward(dy, None, None, dx2, dw2, ws, flags=blconv.BL_REUSE_W | blconv.BL_REUSE_X)
 
         step()
         torch.cuda.synchronize()
-        ref = (y.clone(), dx.clone(), dw.clone())
+        outs = (y, dx, dw, dx2, dw2)
+        ref = tuple(t.clone() for t in outs)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             step()
         torch.cuda.synchronize()
         for r in range(3):
-            for t in (y, dx, dw):
+            for t in outs:
                 t.fill_(float("nan"))
             ws.fill_(0xFF)
             g.replay()
             oy, odx, odw, _, _ = gpu_passes(torch, other, 0.5, ox, ow, ody, poison=False)
             torch.cuda.synchronize()
-            for name, got, want in zip(("y", "dx", "dw"), (y, dx, dw), ref):
+            for name, got, want in zip(("y", "dx", "dw", "dx (backward)", "dw (backward)"), outs, ref):
                 assert torch.equal(got, want), (layer.name, r, name)
 
 

@@ -168,6 +168,7 @@ def test_null_arguments_are_rejected_without_gpu():
     assert lib.bl_conv_forward(None, None, None, None, None, 0, None) == 1
     assert lib.bl_conv_backward_input(None, None, None, None, None, 0, None) == 1
     assert lib.bl_conv_backward_weight(None, None, None, None, None, 0, None) == 1
+    assert lib.bl_conv_backward(None, None, None, None, None, None, None, 0, None) == 1
     p = blconv.Plan(2, 1, 1, 1, (8, 8), 3, (1, 1, 1, 1), 0.5)
     h = p._h
     assert lib.bl_conv_forward(h, None, None, None, None, 0, None) == 1
@@ -175,6 +176,12 @@ def test_null_arguments_are_rejected_without_gpu():
     assert lib.bl_conv_forward(h, 8, 8, 8, 8, 0x4, None) == 1
     assert lib.bl_conv_backward_input(h, 8, 8, 8, 8, 0x1, None) == 1
     assert lib.bl_conv_backward_weight(h, 8, 8, 8, 8, 0x2, None) == 1
+    assert lib.bl_conv_backward(h, 8, 8, 8, 8, 8, 8, 0x8, None) == 1
+    # a tensor missing without its reuse flag
+    assert lib.bl_conv_backward(h, None, 8, 8, 8, 8, 8, 0x3, None) == 1
+    assert lib.bl_conv_backward(h, 8, None, 8, 8, 8, 8, 0x5, None) == 1
+    assert lib.bl_conv_backward(h, 8, 8, None, 8, 8, 8, 0x6, None) == 1
+    assert lib.bl_conv_backward(h, 8, 8, 8, None, 8, 8, 0x7, None) == 1
     # fine-grained top compression: argument checks happen before any HIP call
     ws8 = ctypes.c_void_p(8)
     assert lib.bl_conv_zero_smallest(None, None, ws8, 0, 1, 0, None) == 1
