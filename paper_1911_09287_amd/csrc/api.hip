@@ -99,8 +99,18 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   void* X = spec_at(ws, p->off_X);
   void* Wf = spec_at(ws, p->off_W);
   float2* T = ws_at(ws, p->off_T);
+  const bool small = p->fused_fwd && small_fwd_eligible(p);
+  if (!(flags & (BL_REUSE_W | BL_REUSE_X)) && !small && p->Lh > 1) {
+    // input and filter transforms in one launch where the 2-D fast path has it
+    const bl_status_t st = launch_fft2_fwd_filt(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, w, Wf, s);
+    if (st == BL_OK) {
+      BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, ws_at(ws, p->off_CPart), s));
+      return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
+    }
+    if (st != BL_ERR_UNSUPPORTED) return st;
+  }
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
-  if (p->fused_fwd && !(flags & BL_REUSE_X) && small_fwd_eligible(p)) {
+  if (small && !(flags & BL_REUSE_X)) {
     const bl_status_t st = launch_small_fwd(p, x, static_cast<const float2*>(Wf), y, static_cast<float2*>(X), s);
     if (st != BL_ERR_UNSUPPORTED) return st;
   }

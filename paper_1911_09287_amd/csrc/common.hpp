@@ -103,6 +103,12 @@ bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* ou
 // use_table = false are computed by each block (no table, no allocation).
 bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s,
                              bool use_table = true);
+// The 2-D input transform of a forward pass (as launch_spec_fwd on the fast
+// 2-D path) and the filter transform w -> wout (as launch_spec_filt) in one
+// launch; BL_ERR_UNSUPPORTED (nothing enqueued) where either has no such path
+// (only 3 x 3 filters are compiled for it).
+bl_status_t launch_fft2_fwd_filt(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
+                                 int oi, int oj, const float* w, void* wout, hipStream_t s);
 // DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats.
 bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s);
 

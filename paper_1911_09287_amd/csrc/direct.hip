@@ -17,20 +17,10 @@
 #include <cmath>
 
 #include "common.hpp"
+#include "filt.hpp"
 
 namespace blc {
 namespace {
-
-// e^{sign * 2 pi i k / L}, evaluated in double and rounded once to fp32.
-__device__ inline float2 unit_root(int k, int L, double sign) {
-  double s, c;
-  sincospi(2.0 * (double)k / (double)L, &s, &c);
-  return make_float2((float)c, (float)(sign * s));
-}
-
-__device__ inline void fill_roots(float2* tab, int L, double sign) {
-  for (int k = threadIdx.x; k < L; k += blockDim.x) tab[k] = unit_root(k, L, sign);
-}
 
 
 // ---------------------------------------------------------------------------
@@ -196,92 +186,11 @@ __global__ __launch_bounds__(kThreads) void k_spec_inv(const float2* __restrict_
 // L2 rather than several.
 // ---------------------------------------------------------------------------
 
-struct FiltGeom {
-  int F, C, Kh, Kw;
-  int Lh, Lw, r_h, R, V;
-  int bins_per_block;
-  int xblocks;  // blocks of 256 (c, f) pairs
-};
-
 template <int KH, int KW, typename S>
 __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict__ w, const float2* __restrict__ roots,
                                                         S* __restrict__ out, FiltGeom g) {
-  // roots: e^{-2 pi i k / Lh} (k < Lh) then e^{-2 pi i k / Lw} (k < Lw), from
-  // a table built once per plan, or (roots == nullptr) computed here
   extern __shared__ float2 smem[];
-  float2* twh = smem;
-  float2* tww = twh + g.Lh;
-  // logical block: consecutive ids on one XCD (the hardware deals blocks to
-  // the 8 XCDs in turn); pair block = id % xblocks, bin chunk = id / xblocks
-  const unsigned nb = gridDim.x;
-  unsigned id = blockIdx.x;
-  if (nb % 8 == 0) id = (id % 8) * (nb / 8) + id / 8;
-  const unsigned xblocks = (unsigned)g.xblocks;
-  const unsigned bx = id % xblocks, by = id / xblocks;
-  const long CF = (long)g.C * g.F;
-  const long q = (long)bx * blockDim.x + threadIdx.x;  // q = c * F + f
-  const bool live = q < CF;
-  const int c = live ? (int)(q / g.F) : 0, f = live ? (int)(q % g.F) : 0;
-  // the taps are loaded before the roots are staged, so both loads overlap
-  float tap[KH][KW];
-  const float* wp = w + ((size_t)f * g.C + c) * KH * KW;
-#pragma unroll
-  for (int a = 0; a < KH; ++a)
-#pragma unroll
-    for (int b = 0; b < KW; ++b) tap[a][b] = wp[a * KW + b];
-  if (roots) {
-    for (int k = threadIdx.x; k < g.Lh + g.Lw; k += blockDim.x) smem[k] = roots[k];
-  } else {
-    fill_roots(twh, g.Lh, -1.0);
-    fill_roots(tww, g.Lw, -1.0);
-  }
-  __syncthreads();
-  if (!live) return;
-  const int B = g.R * g.V;
-  const int b0 = (int)by * g.bins_per_block;
-  const int b1 = min(B, b0 + g.bins_per_block);
-  // twiddle indices (u a) mod Lh and (v b) mod Lw, advanced bin by bin
-  int r = b0 / g.V, v = b0 - (b0 / g.V) * g.V;
-  int ih[KH], iw[KW];
-  auto row_start = [&]() {
-    const int u = kept_row_d(r, g.r_h, g.Lh, g.R);
-#pragma unroll
-    for (int a = 0; a < KH; ++a) ih[a] = (int)(((long)u * a) % g.Lh);
-  };
-  row_start();
-#pragma unroll
-  for (int b = 0; b < KW; ++b) iw[b] = (int)(((long)v * b) % g.Lw);
-  for (int bin = b0; bin < b1; ++bin) {
-    float re = 0.f, im = 0.f;
-#pragma unroll
-    for (int a = 0; a < KH; ++a) {
-      // row sum over columns: sum_b tap[a][b] e^{-2 pi i v b / Lw}
-      float rr = 0.f, ri = 0.f;
-#pragma unroll
-      for (int b = 0; b < KW; ++b) {
-        const float2 t = tww[iw[b]];
-        rr = fmaf(tap[a][b], t.x, rr);
-        ri = fmaf(tap[a][b], t.y, ri);
-      }
-      const float2 t = twh[ih[a]];
-      re = fmaf(rr, t.x, fmaf(-ri, t.y, re));
-      im = fmaf(rr, t.y, fmaf(ri, t.x, im));
-    }
-    spec_put(out, (size_t)bin * CF + q, make_float2(re, im));
-    if (++v == g.V) {
-      v = 0;
-      ++r;
-      row_start();
-#pragma unroll
-      for (int b = 0; b < KW; ++b) iw[b] = 0;
-    } else {
-#pragma unroll
-      for (int b = 0; b < KW; ++b) {
-        iw[b] += b;
-        if (iw[b] >= g.Lw) iw[b] -= g.Lw;
-      }
-    }
-  }
+  spec_filt_block<KH, KW, S>(w, roots, out, g, blockIdx.x, gridDim.x, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -722,9 +631,6 @@ bl_status_t launch_spec_inv_direct(const bl_conv_plan_s* p, const float2* in, fl
   });
 }
 
-#define BL_FILT_CASES(X) \
-  X(1, 1) X(1, 2) X(1, 3) X(1, 4) X(1, 5) X(1, 6) X(1, 7) X(1, 8) \
-  X(2, 2) X(3, 3) X(4, 4) X(5, 5) X(6, 6) X(7, 7) X(8, 8)
 
 // e^{-2 pi i k / Lh} for k < Lh, then e^{-2 pi i k / Lw} for k < Lw, in double precision.
 void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
@@ -737,14 +643,15 @@ void host_filt_roots(const bl_conv_plan_s* p, std::vector<float2>& out) {
     }
 }
 
-bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s, bool use_table) {
-  FiltGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
-  const float2* roots = nullptr;
-  if (use_table) {
-    const std::vector<long> key{3, p->Lh, p->Lw};
-    const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_filt_roots(p, h); }, &roots);
-    if (ts != BL_OK) return ts;
-  }
+bl_status_t filt_setup(const bl_conv_plan_s* p, bool use_table, FiltGeom& g, const float2** roots, long* blocks,
+                       size_t* lds, double* bytes) {
+  g = FiltGeom{p->Cout, p->Cin, p->Kh, p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0};
+  *roots = nullptr;
+  bool known = false;
+#define X(a, b) known = known || (p->Kh == a && p->Kw == b);
+  BL_FILT_CASES(X)
+#undef X
+  if (!known) return BL_ERR_UNSUPPORTED;
   const long CF = (long)p->Cin * p->Cout;
   const int B = p->R * p->V;
   const long xblocks = (CF + kThreads - 1) / kThreads;
@@ -752,11 +659,27 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
   int chunks = (int)std::max<long>(1, std::min<long>(B, (1024 + xblocks - 1) / xblocks));
   g.bins_per_block = (B + chunks - 1) / chunks;
   chunks = (B + g.bins_per_block - 1) / g.bins_per_block;
-  const size_t lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
   g.xblocks = (int)xblocks;
   if ((double)xblocks * chunks >= 2147483647.0) return BL_ERR_UNSUPPORTED;
-  dim3 grid((unsigned)(xblocks * chunks));
-  const double bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * (p->bf16 ? 4 : 8);
+  *blocks = xblocks * chunks;
+  *lds = (size_t)(p->Lh + p->Lw) * sizeof(float2);
+  *bytes = (double)CF * p->Kh * p->Kw * 4 + (double)CF * B * (p->bf16 ? 4 : 8);
+  if (use_table) {
+    const std::vector<long> key{3, p->Lh, p->Lw};
+    return plan_table(p, key, [&](std::vector<float2>& h) { host_filt_roots(p, h); }, roots);
+  }
+  return BL_OK;
+}
+
+bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out, hipStream_t s, bool use_table) {
+  FiltGeom g;
+  const float2* roots;
+  long blocks;
+  size_t lds;
+  double bytes;
+  const bl_status_t st = filt_setup(p, use_table, g, &roots, &blocks, &lds, &bytes);
+  if (st != BL_OK) return st;
+  const dim3 grid((unsigned)blocks);
 #define X(a, b)                                                                                             \
   if (p->Kh == a && p->Kw == b)                                                                             \
     return timed_launch("spec_filt", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {                    \

@@ -24,6 +24,7 @@
 #include <cmath>
 
 #include "common.hpp"
+#include "filt.hpp"
 
 namespace blc {
 namespace {
@@ -169,15 +170,15 @@ __device__ inline unsigned plane_group(unsigned b, unsigned nb, unsigned K) {
 // LDS layout (complex spectra, column-major per plane): S[p * PS + v * (LH + 1) + i],
 // so a column thread reads its LH rows at fixed offsets.
 // S: stored-spectrum element of the output (float2 or bfloat16 pairs)
+// One block (id of nb) of the forward transform; sm: the launch's LDS.
 template <int MH, int MW, typename S, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, S* __restrict__ out,
-                                                       Fft2Args g) {
+__device__ __forceinline__ void fft2_fwd_block(const float* __restrict__ in, S* __restrict__ out, const Fft2Args& g,
+                                               unsigned id, unsigned nb, float2* sm) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
-  extern __shared__ float2 sm[];
   float* xs = reinterpret_cast<float*>(sm);  // staging: G*Hin padded grid rows of LW1 floats
   float2* T = sm;                            // row spectra, column-major; aliases xs
   const int tid = threadIdx.x;
-  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K) * (unsigned)g.G;
+  const unsigned p0 = plane_group(id, nb, g.K) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
   const int nrows = np * g.Hin;
 
@@ -295,6 +296,30 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__
       }
     }
   }
+}
+
+template <int MH, int MW, typename S, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_fft2_fwd(const float* __restrict__ in, S* __restrict__ out,
+                                                       Fft2Args g) {
+  extern __shared__ float2 sm[];
+  fft2_fwd_block<MH, MW, S, SPLIT>(in, out, g, blockIdx.x, gridDim.x, sm);
+}
+
+// The input transform and the filter transform of a forward pass in one
+// launch (they are independent): blocks [0, nx) transform planes of x, the
+// rest compute filter-spectrum chunks.  The filter transform is a short,
+// latency-bound kernel; beside the input transform its blocks fill the CUs
+// that the transform's last blocks leave idle, and one launch is saved.
+template <int MH, int MW, typename S, bool SPLIT, int KH, int KW>
+__global__ __launch_bounds__(kThreads) void k_fft2_fwd_filt(const float* __restrict__ in, S* __restrict__ out,
+                                                            Fft2Args g, const float* __restrict__ w,
+                                                            const float2* __restrict__ roots, S* __restrict__ wout,
+                                                            FiltGeom fg, unsigned nx) {
+  extern __shared__ float2 sm[];
+  if (blockIdx.x < nx)
+    fft2_fwd_block<MH, MW, S, SPLIT>(in, out, g, blockIdx.x, nx, sm);
+  else
+    spec_filt_block<KH, KW, S>(w, roots, wout, fg, blockIdx.x - nx, gridDim.x - nx, sm);
 }
 
 template <int MH, int MW, bool SPLIT>
@@ -441,9 +466,17 @@ bool column_split(bool fwd, int MH, int G, int V) {
 // Plane groups whose runs of G elements of `elem` bytes fill a 128-byte line.
 unsigned line_groups(int G, int elem) { return (unsigned)std::max(1, (128 + G * elem - 1) / (G * elem)); }
 
+// Launch geometry of the forward transform.
+struct FwdSetup {
+  Fft2Args g;
+  long blocks;
+  size_t lds;
+  double bytes, flops;
+  bool split;
+};
+
 template <int MH, int MW>
-bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
-                         int oj, hipStream_t s) {
+bl_status_t fwd_setup(const bl_conv_plan_s* p, long P, int Hin, int Win, int oi, int oj, FwdSetup& f) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if (Win % 4 != 0 || oj + Win > LW || oi + Hin > LH || (double)p->kept * P >= 2147483647.0 || P >= 2147483647L)
     return BL_ERR_UNSUPPORTED;
@@ -465,26 +498,39 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, lo
   // (1.2x) and cost time for runs of 64 bytes, so it is kept to the shorter runs
   const int run = G * (p->bf16 ? 4 : 8);
   g.K = run < 64 ? line_groups(G, p->bf16 ? 4 : 8) : 1u;
-  const long blocks = (P + G - 1) / G;
-  const double bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
+  f.g = g;
+  f.blocks = (P + G - 1) / G;
+  f.lds = lds_for(G);
+  f.bytes = (double)P * Hin * Win * 4 + (double)P * p->kept * (p->bf16 ? 4 : 8);
   // conventional FFT counts: Hin real LW-point row FFTs (2.5 LW log2 LW) and V
   // complex LH-point column FFTs (5 LH log2 LH) per plane
-  const double flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
-  const bool split = column_split(true, MH, G, p->V);
-  return timed_launch("spec_fwd_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    const dim3 grid((unsigned)blocks), block(kThreads);
+  f.flops = (double)P * (Hin * 2.5 * LW * std::log2((double)LW) + p->V * 5.0 * LH * std::log2((double)LH));
+  f.split = column_split(true, MH, G, p->V);
+  return BL_OK;
+}
+
+template <int MH, int MW>
+bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
+                         int oj, hipStream_t s) {
+  FwdSetup f;
+  const bl_status_t fs = fwd_setup<MH, MW>(p, P, Hin, Win, oi, oj, f);
+  if (fs != BL_OK) return fs;
+  const Fft2Args g = f.g;
+  const size_t lds = f.lds;
+  return timed_launch("spec_fwd_2d", f.bytes, f.flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    const dim3 grid((unsigned)f.blocks), block(kThreads);
     if (p->bf16) {
       unsigned* o = static_cast<unsigned*>(out);
-      if (split)
-        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, true>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+      if (f.split)
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, true>), grid, block, lds, s, e0, e1, 0, in, o, g);
       else
-        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, false>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, unsigned, false>), grid, block, lds, s, e0, e1, 0, in, o, g);
     } else {
       float2* o = static_cast<float2*>(out);
-      if (split)
-        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, true>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+      if (f.split)
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, true>), grid, block, lds, s, e0, e1, 0, in, o, g);
       else
-        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, false>), grid, block, lds_for(G), s, e0, e1, 0, in, o, g);
+        hipExtLaunchKernelGGL((k_fft2_fwd<MH, MW, float2, false>), grid, block, lds, s, e0, e1, 0, in, o, g);
     }
   });
 }
@@ -523,6 +569,49 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   });
 }
 
+// The forward transform of x beside the filter transform (3 x 3 filters).
+template <int MH, int MW>
+bl_status_t launch_fwd_filt_t(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
+                              int oj, const float* w, void* wout, hipStream_t s) {
+  if (p->Kh != 3 || p->Kw != 3) return BL_ERR_UNSUPPORTED;
+  FwdSetup f;
+  bl_status_t st = fwd_setup<MH, MW>(p, P, Hin, Win, oi, oj, f);
+  if (st != BL_OK) return st;
+  FiltGeom fg;
+  const float2* roots;
+  long fblocks;
+  size_t flds;
+  double fbytes;
+  st = filt_setup(p, true, fg, &roots, &fblocks, &flds, &fbytes);
+  if (st != BL_OK) return st;
+  if (f.blocks + fblocks >= 2147483647L) return BL_ERR_UNSUPPORTED;
+  const dim3 grid((unsigned)(f.blocks + fblocks)), block(kThreads);
+  const size_t lds = std::max(f.lds, flds);
+  const unsigned nx = (unsigned)f.blocks;
+  const Fft2Args g = f.g;
+  return timed_launch("spec_fwd_filt_2d", f.bytes + fbytes, f.flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    if (p->bf16) {
+      unsigned* o = static_cast<unsigned*>(out);
+      unsigned* wo = static_cast<unsigned*>(wout);
+      if (f.split)
+        hipExtLaunchKernelGGL((k_fft2_fwd_filt<MH, MW, unsigned, true, 3, 3>), grid, block, lds, s, e0, e1, 0, in, o, g,
+                              w, roots, wo, fg, nx);
+      else
+        hipExtLaunchKernelGGL((k_fft2_fwd_filt<MH, MW, unsigned, false, 3, 3>), grid, block, lds, s, e0, e1, 0, in, o,
+                              g, w, roots, wo, fg, nx);
+    } else {
+      float2* o = static_cast<float2*>(out);
+      float2* wo = static_cast<float2*>(wout);
+      if (f.split)
+        hipExtLaunchKernelGGL((k_fft2_fwd_filt<MH, MW, float2, true, 3, 3>), grid, block, lds, s, e0, e1, 0, in, o, g,
+                              w, roots, wo, fg, nx);
+      else
+        hipExtLaunchKernelGGL((k_fft2_fwd_filt<MH, MW, float2, false, 3, 3>), grid, block, lds, s, e0, e1, 0, in, o,
+                              g, w, roots, wo, fg, nx);
+    }
+  });
+}
+
 #define BL_FFT2_GRIDS(X) X(3, 3) X(5, 5) X(9, 9) X(17, 17) X(29, 29)
 
 }  // namespace
@@ -531,6 +620,16 @@ bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out,
                             int oj, hipStream_t s) {
 #define X(a, b) \
   if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_fwd_t<a, b>(p, in, out, P, Hin, Win, oi, oj, s);
+  BL_FFT2_GRIDS(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+bl_status_t launch_fft2_fwd_filt(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
+                                 int oi, int oj, const float* w, void* wout, hipStream_t s) {
+#define X(a, b)                         \
+  if (p->Lh == 2 * a && p->Lw == 2 * b) \
+    return launch_fwd_filt_t<a, b>(p, in, out, P, Hin, Win, oi, oj, w, wout, s);
   BL_FFT2_GRIDS(X)
 #undef X
   return BL_ERR_UNSUPPORTED;

@@ -23,6 +23,7 @@ from collections import OrderedDict
 # library kernel name -> pattern of the kernel symbols launched under it
 LIBRARY_NAMES = OrderedDict([
     ("spec_fwd_2d", r"k_fft2_fwd<"),
+    ("spec_fwd_filt_2d", r"k_fft2_fwd_filt<"),
     ("spec_inv_2d", r"k_fft2_inv<"),
     ("spec_fwd_1d", r"k_bluestein1k<[02],"),
     ("spec_inv_1d", r"k_bluestein1k<[13],"),
