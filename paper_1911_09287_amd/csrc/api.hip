@@ -59,7 +59,18 @@ bl_status_t launch_contract(const bl_conv_plan_s* p, Contract which, const void*
 }
 
 bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                            int cj, hipStream_t s) {
+                            int cj, hipStream_t s, int nsplit, float2* tmp) {
+  if (nsplit > 1) {
+    const size_t n = (size_t)p->kept * P;
+    if (p->Lh > 1) {
+      const bl_status_t st = launch_fft2_inv(p, in, out, P, OH, OW, ci, cj, s, nsplit, n);
+      if (st != BL_ERR_UNSUPPORTED) return st;
+    }
+    if (!tmp) return BL_ERR_INVALID_ARG;
+    const bl_status_t st = launch_split_reduce(in, tmp, n, nsplit, s);
+    if (st != BL_OK) return st;
+    in = tmp;
+  }
   if (p->Lh == 1) {
     bl_status_t st = launch_bluestein_inv(p, in, out, P, OW, cj, s);
     if (st != BL_ERR_UNSUPPORTED) return st;
@@ -169,15 +180,20 @@ extern "C" bl_status_t bl_conv_backward(bl_conv_plan_t p, const float* dy, const
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
   if (!(flags & BL_REUSE_X))
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  const bl_status_t st = launch_contract_bwd_pair(p, DY, Wf, T, X, DW, s);
+  // the paired launch writes a pass that it splits along k as partial spectra
+  // (contraction-partials area), which the inverse transform adds
+  float2* CP = ws_at(ws, p->off_CPart);
+  int s1 = p->bp_s1, s2 = p->bp_s2;
+  const bl_status_t st = launch_contract_bwd_pair(p, DY, Wf, s1 > 1 ? CP : T, X, s2 > 1 ? CP : DW, s);
   if (st == BL_ERR_UNSUPPORTED) {
-    BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, ws_at(ws, p->off_CPart), s));
-    BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, ws_at(ws, p->off_CPart), s));
+    s1 = s2 = 1;
+    BL_TRY(launch_contract(p, Contract::GradInput, DY, Wf, T, CP, s));
+    BL_TRY(launch_contract(p, Contract::GradWeight, X, DY, DW, CP, s));
   } else if (st != BL_OK) {
     return st;
   }
-  BL_TRY(launch_spec_inv(p, T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  return launch_wgrad_idft(p, DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s);
+  BL_TRY(launch_spec_inv(p, s1 > 1 ? CP : T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s, s1, T));
+  return launch_wgrad_idft(p, s2 > 1 ? CP : DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s, s2, DW);
 }
 
 // ---------------------------------------------------------------------------

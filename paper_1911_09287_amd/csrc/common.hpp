@@ -95,9 +95,12 @@ int device_cus();
 bl_status_t launch_spec_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
                             int oi, int oj, hipStream_t s);
 // Kept spectrum in[b * P + p] -> real planes [P][OH][OW] holding the grid
-// window that starts at (ci, cj), scaled by 1 / (Lh Lw).
+// window that starts at (ci, cj), scaled by 1 / (Lh Lw).  With nsplit > 1 the
+// spectrum is the sum of nsplit partial spectra kept * P complex values apart
+// (added in order while loading on the fast 2-D path, else first summed into
+// tmp, which then holds the spectrum).
 bl_status_t launch_spec_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                            int cj, hipStream_t s);
+                            int cj, hipStream_t s, int nsplit = 1, float2* tmp = nullptr);
 // Filter w [F][C][Kh][Kw] -> W[b][c][f] (stored-spectrum type).  The roots of
 // unity come from the plan's device table (built on first use), or with
 // use_table = false are computed by each block (no table, no allocation).
@@ -109,8 +112,13 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
 // (only 3 x 3 filters are compiled for it).
 bl_status_t launch_fft2_fwd_filt(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win,
                                  int oi, int oj, const float* w, void* wout, hipStream_t s);
-// DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats.
-bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s);
+// DW[b][c][f] -> dw [F][C][Kh][Kw]; `part` holds wg_chunks x Kh Kw x C F floats
+// (times bp_s2 when the plan pairs the backward contractions).  With nsplit > 1
+// DW is the sum of nsplit partial spectra kept * C * F complex values apart
+// (their bin slices summed with the others on the sliced path, else first
+// summed into tmp, which then holds the spectrum).
+bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s,
+                              int nsplit = 1, float2* tmp = nullptr);
 
 // Operands A and Bm are stored spectra (complex64 or bfloat16 pairs); the
 // output O and the split-k partials are complex64.
@@ -122,11 +130,14 @@ bool contract_is_thin(const bl_conv_plan_s* p, Contract which);
 bl_status_t launch_contract_thin(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                  float2* O, hipStream_t s);
 // Grad-input (DX = DY W) and grad-weight (DW = X^T conj(DY)) contractions in
-// one launch when both run on the tiled kernel with one tile shape, no k split
-// and the same number of k stages; BL_ERR_UNSUPPORTED (nothing enqueued)
-// otherwise.
+// one launch where the plan pairs them (bp_s1, bp_s2 >= 1): a pass split
+// s > 1 ways along k writes s partial spectra, kept * M * N complex values
+// apart, to DX or DW, for the inverse transform to add; BL_ERR_UNSUPPORTED
+// (nothing enqueued) otherwise.
 bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, const void* W, float2* DX,
                                      const void* X, float2* DW, hipStream_t s);
+// out[i] = sum over s < splits of part[s n + i] in order s = 0, 1, ... (n even).
+bl_status_t launch_split_reduce(const float2* part, float2* out, unsigned long long n, int splits, hipStream_t s);
 // Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
 // generic one (any strides and sizes).
 bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
@@ -157,6 +168,6 @@ bl_status_t launch_small_fwd(const bl_conv_plan_s* p, const float* x, const floa
 bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out, long P, int Hin, int Win, int oi,
                             int oj, hipStream_t s);
 bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                            int cj, hipStream_t s);
+                            int cj, hipStream_t s, int nsplit = 1, size_t pstride = 0);
 
 }  // namespace blc

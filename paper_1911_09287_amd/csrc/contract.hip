@@ -444,20 +444,25 @@ __global__ __launch_bounds__(256 * KS, KS == 1 ? 2 : 1) void k_cgemm(const void*
 }
 
 // The grad-input and grad-weight contractions of a layer in one launch (both
-// need only the stored spectra): logical blocks [0, n1) take grad-input tiles
-// (DX = DY W), the rest grad-weight tiles (DW = X^T conj(DY)), one tile shape.
-// One launch instead of two, and the two passes' tiles share the CUs.
+// need only the stored spectra): logical blocks [0, s1 t1) take grad-input
+// tiles (DX = DY W), the rest grad-weight tiles (DW = X^T conj(DY)), one tile
+// shape; t1, t2 = tiles x bins of a pass, s1, s2 its k ranges (a pass split
+// along k writes partial sums, split_stride apart).  One launch instead of
+// two, and the two passes' tiles, of equal k length, share the CUs.
 template <int BM, int BN, bool BF16>
 __global__ __launch_bounds__(256, 2) void k_cgemm_bwd(const void* __restrict__ A1, const void* __restrict__ B1,
                                                      float2* __restrict__ O1, CgemmArgs g1,
                                                      const void* __restrict__ A2, const void* __restrict__ B2,
-                                                     float2* __restrict__ O2, CgemmArgs g2, unsigned n1) {
+                                                     float2* __restrict__ O2, CgemmArgs g2, unsigned t1, unsigned s1,
+                                                     unsigned t2) {
   __shared__ __align__(16) float smem[CgemmLds<BM, BN, BF16, 1>::floats];
   const unsigned id = xcd_block_id(blockIdx.x, gridDim.x);
-  if (id < n1)
-    cgemm_tile<BM, BN, true, false, false, BF16, 1>(A1, B1, O1, g1, id, 0, smem);
-  else
-    cgemm_tile<BM, BN, false, true, true, BF16, 1>(A2, B2, O2, g2, id - n1, 0, smem);
+  if (id < t1 * s1) {
+    cgemm_tile<BM, BN, true, false, false, BF16, 1>(A1, B1, O1, g1, id % t1, id / t1, smem);
+  } else {
+    const unsigned j = id - t1 * s1;
+    cgemm_tile<BM, BN, false, true, true, BF16, 1>(A2, B2, O2, g2, j % t2, j / t2, smem);
+  }
 }
 
 // out[i] = sum over k-splits of part[s][i], in split order.
@@ -512,12 +517,15 @@ double pass_bytes(const bl_conv_plan_s* p, const CgemmArgs& g) {
   return (double)p->kept * (ob * ((double)g.M * g.K + (double)g.K * g.N) + 8.0 * g.M * g.N);
 }
 
-// Tile counts of a pass on BM x BN tiles, one k range.
-void whole_k_tiles(CgemmArgs& g, int BM, int BN) {
+// Tile counts of a pass on BM x BN tiles and `splits` k ranges of whole
+// stages (partial outputs split_stride = bins x M x N apart); returns the
+// number of k ranges that hold stages.
+int split_k_tiles(CgemmArgs& g, int BM, int BN, int splits, unsigned long long bins) {
   g.tiles_n = (g.N + BN - 1) / BN;
   g.tiles = ((g.M + BM - 1) / BM) * g.tiles_n;
-  g.kper = (g.K + kBK - 1) / kBK * kBK;
-  g.split_stride = 0;
+  g.kper = ((g.K + splits - 1) / splits + kBK - 1) / kBK * kBK;
+  g.split_stride = bins * (unsigned long long)g.M * g.N;
+  return (g.K + g.kper - 1) / g.kper;
 }
 
 }  // namespace
@@ -583,33 +591,33 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
 
 bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, const void* W, float2* DX,
                                      const void* X, float2* DW, hipStream_t s) {
+  if (p->bp_s1 < 1 || p->bp_s2 < 1) return BL_ERR_UNSUPPORTED;
   if (contract_is_thin(p, Contract::GradInput) || contract_is_thin(p, Contract::GradWeight)) return BL_ERR_UNSUPPORTED;
-  const BlContractTiling &t1 = p->ct[1], &t2 = p->ct[2];
-  if (t1.bm != t2.bm || t1.bn != t2.bn || t1.splits != 1 || t2.splits != 1) return BL_ERR_UNSUPPORTED;
   CgemmArgs g1, g2;
   if (!tiled_args(p, Contract::GradInput, g1) || !tiled_args(p, Contract::GradWeight, g2)) return BL_ERR_UNSUPPORTED;
-  // tiles of both passes must take about the same time: with unequal k
-  // lengths the long tiles end up sharing CUs with short ones and finish last
-  // (measured: a 4-fold k ratio made the launch 70 % slower than two)
-  if ((g1.K + kBK - 1) / kBK != (g2.K + kBK - 1) / kBK) return BL_ERR_UNSUPPORTED;
-  const int BM = t1.bm, BN = t1.bn;
-  whole_k_tiles(g1, BM, BN);
-  whole_k_tiles(g2, BM, BN);
-  const unsigned long long n1 = (unsigned long long)g1.tiles * p->kept, n2 = (unsigned long long)g2.tiles * p->kept;
-  if (n1 + n2 >= 2147483647ULL) return BL_ERR_UNSUPPORTED;
+  // the plan split the pass with more k stages so that both passes' tiles take
+  // about the same time: with unequal k lengths the long tiles end up sharing
+  // CUs with short ones and finish last (a 4-fold ratio made the launch 70 %
+  // slower than two launches; split 4 ways it is 17 % faster)
+  const int BM = p->ct[1].bm, BN = p->ct[1].bn;
+  const unsigned long long B = p->kept;
+  if (split_k_tiles(g1, BM, BN, p->bp_s1, B) != p->bp_s1 || split_k_tiles(g2, BM, BN, p->bp_s2, B) != p->bp_s2)
+    return BL_ERR_UNSUPPORTED;
+  const unsigned long long n1 = (unsigned long long)g1.tiles * B, n2 = (unsigned long long)g2.tiles * B;
+  if (n1 * p->bp_s1 + n2 * p->bp_s2 >= 2147483647ULL) return BL_ERR_UNSUPPORTED;
   const double flops = 8.0 * p->kept * ((double)g1.M * g1.N * g1.K + (double)g2.M * g2.N * g2.K);
   const double bytes = pass_bytes(p, g1) + pass_bytes(p, g2);
-  const dim3 grid((unsigned)(n1 + n2));
-  const unsigned n1u = (unsigned)n1;
+  const dim3 grid((unsigned)(n1 * p->bp_s1 + n2 * p->bp_s2));
+  const unsigned t1 = (unsigned)n1, s1 = (unsigned)p->bp_s1, t2 = (unsigned)n2;
   bl_status_t st = BL_ERR_UNSUPPORTED;
 #define BL_GO(BMV, BNV)                                                                                         \
   st = timed_launch("contract_bwd", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {                       \
     if (p->bf16)                                                                                                \
       hipExtLaunchKernelGGL((k_cgemm_bwd<BMV, BNV, true>), grid, dim3(256), 0, s, e0, e1, 0, DY, W, DX, g1, X, DY, \
-                            DW, g2, n1u);                                                                       \
+                            DW, g2, t1, s1, t2);                                                                \
     else                                                                                                        \
       hipExtLaunchKernelGGL((k_cgemm_bwd<BMV, BNV, false>), grid, dim3(256), 0, s, e0, e1, 0, DY, W, DX, g1, X,   \
-                            DY, DW, g2, n1u);                                                                   \
+                            DY, DW, g2, t1, s1, t2);                                                            \
   })
   if (BM == 128 && BN == 64) BL_GO(128, 64);
   else if (BM == 64 && BN == 64) BL_GO(64, 64);
@@ -617,6 +625,16 @@ bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, co
   else if (BM == 64 && BN == 32) BL_GO(64, 32);
 #undef BL_GO
   return st;
+}
+
+bl_status_t launch_split_reduce(const float2* part, float2* out, unsigned long long n, int splits, hipStream_t s) {
+  if (n % 2 != 0) return BL_ERR_UNSUPPORTED;  // summed as pairs of complex values
+  const unsigned long long n4 = n / 2;
+  const unsigned long long blocks = (n4 + 255) / 256;
+  return timed_launch("contract_reduce", 8.0 * n * (splits + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_split_reduce, dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0,
+                          reinterpret_cast<const float4*>(part), reinterpret_cast<float4*>(out), n4, splits);
+  });
 }
 
 }  // namespace blc

@@ -213,6 +213,8 @@ struct WgradGeom {
   int Lh, Lw, r_h, R, V;
   int bins_per_chunk, chunks;
   int tiles_f;  // 16-filter tiles along F (k_wgrad_tile)
+  int nsplit;   // k_wgrad_idft: partial spectra of DW (their slices are more slices; 0 or 1: one)
+  unsigned long long pstride;  // complex values between two partial spectra
 };
 
 template <int TMAX, int TC>
@@ -223,8 +225,11 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
   extern __shared__ float2 E[];  // bins_per_chunk x TMAX, zero beyond T (no branches in the bin loop)
   __shared__ float res[TC > 1 ? TF * TC * TMAX : 1];
   const int B = g.R * g.V;
-  const int b0 = blockIdx.y * g.bins_per_chunk;
+  // slice blockIdx.y: bin chunk blockIdx.y % chunks of partial spectrum blockIdx.y / chunks
+  const int sp = blockIdx.y / g.chunks;
+  const int b0 = (blockIdx.y - sp * g.chunks) * g.bins_per_chunk;
   const int nb = min(g.bins_per_chunk, B - b0);
+  DW += (size_t)sp * g.pstride;
   // copy this slice of the table, four loads of a thread in flight together
   const float2* Es = Et + (size_t)b0 * g.T;
   for (int e0 = threadIdx.x; e0 < nb * TMAX; e0 += 4 * kThreads) {
@@ -265,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
       for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
     }
   }
-  if (g.chunks > 1) {
+  if (gridDim.y > 1) {
     if (valid) {
 #pragma unroll
       for (int t = 0; t < TMAX; ++t)
@@ -307,13 +312,14 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restri
   const int t = (int)(e / Q);
   const size_t stride = (size_t)g.T * Q;
   const float* src = part + e;
+  const int slices = g.chunks * max(1, g.nsplit);
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   int k = 0;
-  for (; k + 8 <= g.chunks; k += 8) {
+  for (; k + 8 <= slices; k += 8) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) s[i] += src[(size_t)(k + i) * stride];
   }
-  for (int i = 0; k < g.chunks; ++k, ++i) s[i] += src[(size_t)k * stride];
+  for (int i = 0; k < slices; ++k, ++i) s[i] += src[(size_t)k * stride];
   const float tot = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
   const int c = (int)(q / g.F), f = (int)(q % g.F);
   dw[((size_t)f * g.C + c) * g.T + t] = tot;
@@ -695,11 +701,28 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
   return BL_ERR_UNSUPPORTED;
 }
 
-bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s) {
+bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s,
+                              int nsplit, float2* tmp) {
   WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0,
-              (p->Cout + 15) / 16};
+              (p->Cout + 15) / 16, 1, 0};
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept;
+  const int tmax_w = g.T <= 9 ? g.T : 16;
+  const bool wide = (Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && g.T <= 16 &&
+                    (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds && Q < 2147483647L;
+  if (nsplit > 1) {
+    // partial spectra: more slices of the sliced path (whose partial-sum area
+    // the plan sized for them), else summed into tmp first
+    if (p->wg_groups == 0 && !wide && p->wg_chunks > 1 && nsplit <= std::max(1, p->bp_s2)) {
+      g.nsplit = nsplit;
+      g.pstride = (unsigned long long)B * Q;
+    } else {
+      if (!tmp) return BL_ERR_INVALID_ARG;
+      const bl_status_t st = launch_split_reduce(DW, tmp, (unsigned long long)B * Q, nsplit, s);
+      if (st != BL_OK) return st;
+      DW = tmp;
+    }
+  }
   // one pass over all bins when there are at least 256 blocks of 64 pairs,
   // or few bins (at most 256: a sixteenth per wave), and taps and table fit
   // (rows of at most 256 output channels: wider rows write dw better from the
@@ -737,10 +760,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
 #undef BL_WG
     return st;
   }
-  const int tmax_w = g.T <= 9 ? g.T : 16;
-  if ((Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && g.T <= 16 &&
-      (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds &&
-      Q < 2147483647L) {
+  if (wide) {
     const size_t lds = (size_t)B * tmax_w * sizeof(float2);
     const long blocks = (Q + 63) / 64;
     // at most one block per CU: 16 waves per block, each over a sixteenth of
@@ -765,16 +785,16 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
     }
 #undef BL_WIDE
   }
-  g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices
+  g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices (per partial spectrum)
   g.bins_per_chunk = p->wg_bins;
-  if (g.chunks > 65535) return BL_ERR_UNSUPPORTED;
+  if ((long)g.chunks * g.nsplit > 65535) return BL_ERR_UNSUPPORTED;
   const int tmax = g.T <= 9 ? g.T : g.T <= 16 ? 16 : g.T <= 32 ? 32 : 64;  // as instantiated below
   const size_t lds = (size_t)g.bins_per_chunk * tmax * sizeof(float2);
   if ((long)lds > kWgradSliceLds) return BL_ERR_UNSUPPORTED;
   const int TC = chan_tile(g.T, p->Cout), TF = kThreads / TC;
   const long xblocks = TC == 1 ? (Q + kThreads - 1) / kThreads : (long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF);
-  dim3 grid((unsigned)xblocks, (unsigned)g.chunks);
-  const double bytes = (double)Q * B * 8 + (double)Q * g.T * 4;
+  dim3 grid((unsigned)xblocks, (unsigned)(g.chunks * g.nsplit));
+  const double bytes = (double)Q * B * 8 * g.nsplit + (double)Q * g.T * 4;
   bl_status_t st;
   auto go = [&](auto kern) {
     return timed_launch("wgrad_idft", bytes, 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
@@ -792,9 +812,10 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
       else if (g.T <= 32) st = go(k_wgrad_idft<32, 1>);
       else st = go(k_wgrad_idft<64, 1>);
   }
-  if (st != BL_OK || g.chunks == 1) return st;
+  if (st != BL_OK || g.chunks * g.nsplit == 1) return st;
   const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
-  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {
+  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks * g.nsplit + 1), 0.0, s,
+                      [&](hipEvent_t e0, hipEvent_t e1) {
     hipExtLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, e0, e1, 0, part, dw, g);
   });
 }

@@ -143,7 +143,20 @@ struct Fft2Args {
   unsigned magic;  // ceil(2^32 / q4) for q4 > 1: e / q4 == umulhi(e, magic) for the block's e
   unsigned K;      // plane groups per 128-byte line of a bin row (plane_group)
   float scale;     // inverse: 1 / (Lh Lw)
+  unsigned nsplit;               // inverse: partial spectra to add (0 or 1: one spectrum)
+  unsigned long long pstride;    // inverse: complex values between two partial spectra
 };
+
+// A kept bin of the inverse's input: with PARTS the sum of its nsplit partial
+// spectra in order, else one load (a separate instantiation, so that the
+// common case keeps its code).
+template <bool PARTS>
+__device__ __forceinline__ float2 load_parts(const float2* q, const Fft2Args& g) {
+  float2 v = q[0];
+  if constexpr (PARTS)
+    for (unsigned s = 1; s < g.nsplit; ++s) v = cadd(v, q[(size_t)s * g.pstride]);
+  return v;
+}
 
 // Index of kept row u (or -1): the top-left corner rows 0..r_h, then the
 // bottom-left corner rows Lh - (R - r_h - 1) .. Lh - 1.
@@ -322,7 +335,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd_filt(const float* __restr
     spec_filt_block<KH, KW, S>(w, roots, wout, fg, blockIdx.x - nx, gridDim.x - nx, sm);
 }
 
-template <int MH, int MW, bool SPLIT>
+template <int MH, int MW, bool SPLIT, bool PARTS>
 __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
                                                        Fft2Args g) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
@@ -349,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
 #pragma unroll
       for (int k = 0; k < MH; ++k) {
         const int r = row_slot(k + h * MH, g.r_h, g.R, LH);
-        mine[k] = r >= 0 ? src[(unsigned)r * rs] : make_float2(0.f, 0.f);
+        mine[k] = r >= 0 ? load_parts<PARTS>(src + (unsigned)r * rs, g) : make_float2(0.f, 0.f);
       }
       float2 z[MH];
 #pragma unroll
@@ -375,8 +388,8 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
       for (int k = 0; k < MH; ++k) {
         const int r0 = row_slot(k, g.r_h, g.R, LH);
         const int r1 = row_slot(k + MH, g.r_h, g.R, LH);
-        const float2 lo = r0 >= 0 ? src[r0 * rs] : make_float2(0.f, 0.f);
-        const float2 hi = r1 >= 0 ? src[r1 * rs] : make_float2(0.f, 0.f);
+        const float2 lo = r0 >= 0 ? load_parts<PARTS>(src + r0 * rs, g) : make_float2(0.f, 0.f);
+        const float2 hi = r1 >= 0 ? load_parts<PARTS>(src + r1 * rs, g) : make_float2(0.f, 0.f);
         a[k] = cadd(lo, hi);
         b[k] = cmul(root<LH, true>(k), csub(lo, hi));
       }
@@ -537,7 +550,7 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, lo
 
 template <int MH, int MW>
 bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                         int cj, hipStream_t s) {
+                         int cj, hipStream_t s, int nsplit, size_t pstride) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if ((double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
   const bool vec4 = OW % 4 == 0;
@@ -545,6 +558,8 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
              1.0f / ((float)p->Lh * (float)p->Lw)};
   g.magic = magic_for(g.q4);
   g.PS = (p->V * (LH + 1)) | 1;
+  g.nsplit = (unsigned)std::max(1, nsplit);
+  g.pstride = pstride;
   int G = std::max(1, kThreads / OH);
   G = (int)std::min<long>(G, P);
   auto lds_for = [&](int gg) {
@@ -557,15 +572,22 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   g.G = G;
   g.K = line_groups(G, 8) | (vec4 ? kInvVec4 : 0u);
   const long blocks = (P + G - 1) / G;
-  const double bytes = (double)P * p->kept * 8 + (double)P * OH * OW * 4;
+  const double bytes = (double)P * p->kept * 8 * g.nsplit + (double)P * OH * OW * 4;
   const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
   const bool split = column_split(false, MH, G, p->V);
   return timed_launch("spec_inv_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
     const dim3 grid((unsigned)blocks), block(kThreads);
-    if (split)
-      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true>), grid, block, lds_for(G), s, e0, e1, 0, in, out, g);
-    else
-      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false>), grid, block, lds_for(G), s, e0, e1, 0, in, out, g);
+    const size_t lds = lds_for(G);
+    if (g.nsplit > 1) {
+      if (split)
+        hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true, true>), grid, block, lds, s, e0, e1, 0, in, out, g);
+      else
+        hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false, true>), grid, block, lds, s, e0, e1, 0, in, out, g);
+    } else if (split) {
+      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true, false>), grid, block, lds, s, e0, e1, 0, in, out, g);
+    } else {
+      hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false, false>), grid, block, lds, s, e0, e1, 0, in, out, g);
+    }
   });
 }
 
@@ -636,9 +658,9 @@ bl_status_t launch_fft2_fwd_filt(const bl_conv_plan_s* p, const float* in, void*
 }
 
 bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                            int cj, hipStream_t s) {
+                            int cj, hipStream_t s, int nsplit, size_t pstride) {
 #define X(a, b) \
-  if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_inv_t<a, b>(p, in, out, P, OH, OW, ci, cj, s);
+  if (p->Lh == 2 * a && p->Lw == 2 * b) return launch_inv_t<a, b>(p, in, out, P, OH, OW, ci, cj, s, nsplit, pstride);
   BL_FFT2_GRIDS(X)
 #undef X
   return BL_ERR_UNSUPPORTED;

@@ -113,6 +113,27 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
   p->off_DY = o; o = align_up(o + B * p->N * p->Cout * sb, 256);
   p->off_T = o;  o = align_up(o + B * p->N * (size_t)std::max(p->Cin, p->Cout) * cb, 256);
   p->off_DW = o; o = align_up(o + B * p->Cin * p->Cout * cb, 256);
+  // contraction tiling of the three passes, and the paired backward launch:
+  // one tile shape and no k split of their own; the pass with more k stages is
+  // split (2 to 4 ways) to the other's length
+  {
+    const long Bk = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
+    p->ct[0] = bl_contract_tiling(N, Co, Ci, Bk);
+    p->ct[1] = bl_contract_tiling(N, Ci, Co, Bk);
+    p->ct[2] = bl_contract_tiling(Ci, Co, N, Bk);
+    p->bp_s1 = p->bp_s2 = 0;
+    const BlContractTiling &t1 = p->ct[1], &t2 = p->ct[2];
+    if (t1.bm == t2.bm && t1.bn == t2.bn && t1.splits == 1 && t2.splits == 1) {
+      const long st1 = (Co + 15) / 16, st2 = (N + 15) / 16;  // k stages: grad-input sums C_out, grad-weight N
+      if (st1 == st2) {
+        p->bp_s1 = p->bp_s2 = 1;
+      } else if (st1 > st2 && st1 % st2 == 0 && st1 / st2 <= 4) {
+        p->bp_s1 = (int)(st1 / st2), p->bp_s2 = 1;
+      } else if (st2 > st1 && st2 % st1 == 0 && st2 / st1 <= 4) {
+        p->bp_s1 = 1, p->bp_s2 = (int)(st2 / st1);
+      }
+    }
+  }
   // partial sums of the weight-gradient inverse DFT over bin slices: enough
   // slices for ~1024 blocks of 256 (c, f) pairs, at least 16 bins per slice,
   // whole batches of 8 bins, and a slice's weights [bins][taps, padded as the
@@ -143,18 +164,20 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
                       (long)ng * 256 * tm * 4 <= 64 * 1024) ? ng : 0;
     }
     p->off_Part = o;
-    o = align_up(o + (chunks > 1 ? (size_t)chunks * Q * p->Kh * p->Kw * sizeof(float) : 0), 256);
+    // (k-split partial spectra of a paired backward launch count as more slices)
+    o = align_up(o + (chunks > 1 ? (size_t)std::max(1, p->bp_s2) * chunks * Q * p->Kh * p->Kw * sizeof(float) : 0),
+                 256);
   }
-  // split-k partial tiles of the contraction (largest of the three passes)
+  // split-k partial tiles of the contraction (largest of the three passes and
+  // of the paired backward launch)
   {
     const long Bk = p->kept, N = p->N, Ci = p->Cin, Co = p->Cout;
-    p->ct[0] = bl_contract_tiling(N, Co, Ci, Bk);
-    p->ct[1] = bl_contract_tiling(N, Ci, Co, Bk);
-    p->ct[2] = bl_contract_tiling(Ci, Co, N, Bk);
     size_t need = 0;
     const long mn[3] = {N * Co, N * Ci, Ci * Co};
     for (int i = 0; i < 3; ++i)
       if (p->ct[i].splits > 1) need = std::max(need, (size_t)p->ct[i].splits * Bk * mn[i] * cb);
+    if (p->bp_s1 > 1) need = std::max(need, (size_t)p->bp_s1 * Bk * mn[1] * cb);
+    if (p->bp_s2 > 1) need = std::max(need, (size_t)p->bp_s2 * Bk * mn[2] * cb);
     p->off_CPart = o;
     o = align_up(o + need, 256);
   }

@@ -84,6 +84,11 @@ struct bl_conv_plan_s {
   int wg_bins;          // bins per slice (a multiple of 8)
   int wg_groups;        // groups of 256 threads per block summing parts of a slice (1, 2 or 4)
   BlContractTiling ct[3];  // contraction tiling: forward, grad-input, grad-weight
+  // paired backward contraction (one launch for grad-input and grad-weight):
+  // k-splits of the two passes (the longer split so that both have tiles of
+  // equal k length; partial sums in the contraction-partials area, added by
+  // the inverse transforms); 0 when the passes are not paired
+  int bp_s1, bp_s2;
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
   // small device tables (1-D chirps and filter spectra, weight-gradient
   // inverse-DFT weights), built on a plan's first call that needs them on

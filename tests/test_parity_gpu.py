@@ -339,15 +339,22 @@ def test_contraction_shapes(torch):
 
 def test_combined_backward(torch):
     """bl_conv_backward (both gradients from one DY spectrum; the two
-    contractions in one launch where their tiles and sum lengths agree)
-    against the oracle, equal run to run and with or without reuse flags, and
-    within rounding of the separate backward calls: the ResNet stack at
-    c = 0.5 (one launch on the 128-channel layer, where C_out = N, two on the
-    others), a ragged layer, a 1-D layer and a bfloat16 plan (one launch)."""
+    contractions in one launch where they share a tile shape, the pass with
+    the longer sum split along k into partial spectra that the inverse
+    transforms add) against the oracle, equal run to run and with or without
+    reuse flags, and within rounding of the separate backward calls.  The
+    ResNet stack at c = 0.5 covers the 64-channel layer (grad-weight split in
+    two, its partials added as more bin slices), the 128-channel layer (no
+    split), the 256-channel layer (different tiles: two launches) and the
+    512-channel layer (grad-input split in four, added by the 2-D inverse as
+    it loads); then a ragged layer, a 1-D layer (grad-input partials summed
+    before the chirp-z inverse), a layer whose grad-weight partials are summed
+    before the one-pass inverse DFT, and a bfloat16 plan."""
     # (layer, rate, plan flags, workload (config, layer) or None for random inputs)
     cases = [(synth.WORKLOADS[3].layers[i], 0.5, 0, (3, i)) for i in range(4)]
     cases += [(synth.Layer("ragged", 2, 70, 66, 130, 6, 6, 3, (1, 1, 1, 1), "blur"), 0.0, 0, None),
               (synth.WORKLOADS[2].layers[1], 0.5, 0, (2, 1)),
+              (synth.Layer("split_wide", 2, 128, 32, 32, 8, 8, 3, (1, 1, 1, 1), "blur"), 0.0, 0, None),
               (synth.Layer("bf_pair", 2, 64, 32, 64, 12, 12, 3, (1, 1, 1, 1), "blur"), 0.5,
                blconv.BL_DESC_BF16_SPECTRA, None)]
     dev = torch.device("cuda:0")
