@@ -599,7 +599,7 @@ bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, co
   // about the same time: with unequal k lengths the long tiles end up sharing
   // CUs with short ones and finish last (a 4-fold ratio made the launch 70 %
   // slower than two launches; split 4 ways it is 17 % faster)
-  const int BM = p->ct[1].bm, BN = p->ct[1].bn;
+  const int BM = p->bp_bm, BN = p->bp_bn;
   const unsigned long long B = p->kept;
   if (split_k_tiles(g1, BM, BN, p->bp_s1, B) != p->bp_s1 || split_k_tiles(g2, BM, BN, p->bp_s2, B) != p->bp_s2)
     return BL_ERR_UNSUPPORTED;

@@ -89,6 +89,7 @@ struct bl_conv_plan_s {
   // equal k length; partial sums in the contraction-partials area, added by
   // the inverse transforms); 0 when the passes are not paired
   int bp_s1, bp_s2;
+  int bp_bm, bp_bn;  // the paired launch's tile shape
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
   // small device tables (1-D chirps and filter spectra, weight-gradient
   // inverse-DFT weights), built on a plan's first call that needs them on
