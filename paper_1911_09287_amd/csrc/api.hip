@@ -110,14 +110,23 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   void* X = spec_at(ws, p->off_X);
   void* Wf = spec_at(ws, p->off_W);
   float2* T = ws_at(ws, p->off_T);
+  float2* CP = ws_at(ws, p->off_CPart);
+  // the contraction and the output inverse; a split contraction leaves
+  // partial spectra that the 2-D inverse adds as it loads them
+  auto contract_invert = [&]() -> bl_status_t {
+    if (p->fwd_split > 1 && p->Lh > 1) {
+      const bl_status_t st = launch_contract_tiled(p, Contract::Forward, X, Wf, T, CP, s, p->fwd_split);
+      if (st == BL_OK) return launch_spec_inv(p, CP, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s, p->fwd_split, T);
+      if (st != BL_ERR_UNSUPPORTED) return st;
+    }
+    BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, CP, s));
+    return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
+  };
   const bool small = p->fused_fwd && small_fwd_eligible(p);
   if (!(flags & (BL_REUSE_W | BL_REUSE_X)) && !small && p->Lh > 1) {
     // input and filter transforms in one launch where the 2-D fast path has it
     const bl_status_t st = launch_fft2_fwd_filt(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, w, Wf, s);
-    if (st == BL_OK) {
-      BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, ws_at(ws, p->off_CPart), s));
-      return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
-    }
+    if (st == BL_OK) return contract_invert();
     if (st != BL_ERR_UNSUPPORTED) return st;
   }
   if (!(flags & BL_REUSE_W)) BL_TRY(launch_spec_filt(p, w, Wf, s));
@@ -127,8 +136,7 @@ extern "C" bl_status_t bl_conv_forward(bl_conv_plan_t p, const float* x, const f
   }
   if (!(flags & BL_REUSE_X))
     BL_TRY(launch_spec_fwd(p, x, X, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s));
-  BL_TRY(launch_contract(p, Contract::Forward, X, Wf, T, ws_at(ws, p->off_CPart), s));
-  return launch_spec_inv(p, T, y, (long)p->N * p->Cout, p->Ho, p->Wo, 0, 0, s);
+  return contract_invert();
 }
 
 extern "C" bl_status_t bl_conv_backward_input(bl_conv_plan_t p, const float* dy, const float* w, float* dx,

@@ -140,8 +140,10 @@ bl_status_t launch_contract_bwd_pair(const bl_conv_plan_s* p, const void* DY, co
 bl_status_t launch_split_reduce(const float2* part, float2* out, unsigned long long n, int splits, hipStream_t s);
 // Tiled, double-buffered fp32-MFMA contraction (aligned operands) and the
 // generic one (any strides and sizes).
+// parts > 1: split k into exactly that many ranges and leave the partial
+// spectra in `part` (kept * M * N complex values apart) for the consumer to add.
 bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
-                                  float2* O, float2* part, hipStream_t s);
+                                  float2* O, float2* part, hipStream_t s, int parts = 0);
 bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
                                     float2* O, hipStream_t s);
 

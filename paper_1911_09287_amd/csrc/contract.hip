@@ -533,11 +533,12 @@ int split_k_tiles(CgemmArgs& g, int BM, int BN, int splits, unsigned long long b
 // Tiled path: needs 16-byte aligned pairs of complex values along the
 // contiguous dimension of each operand; returns BL_ERR_UNSUPPORTED otherwise.
 bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm,
-                                  float2* O, float2* part, hipStream_t s) {
+                                  float2* O, float2* part, hipStream_t s, int parts) {
   CgemmArgs g;
   if (!tiled_args(p, which, g)) return BL_ERR_UNSUPPORTED;
   const unsigned long long B = p->kept;
-  const BlContractTiling& t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
+  BlContractTiling t = p->ct[which == Contract::Forward ? 0 : which == Contract::GradInput ? 1 : 2];
+  if (parts > 1) t.splits = parts, t.ks = 1;
   const int BM = t.bm, BN = t.bn;
   const int tiles_m = (g.M + BM - 1) / BM;
   g.tiles_n = (g.N + BN - 1) / BN;
@@ -547,7 +548,8 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   g.kper = (g.K + splits - 1) / splits;
   g.kper = (g.kper + kBK - 1) / kBK * kBK;
   splits = (g.K + g.kper - 1) / g.kper;
-  if (total % 2 != 0) splits = 1, g.kper = g.K;  // the reduction works on pairs
+  if (parts > 1 && splits != parts) return BL_ERR_UNSUPPORTED;
+  if (parts <= 1 && total % 2 != 0) splits = 1, g.kper = g.K;  // the reduction works on pairs
   g.split_stride = total;
   float2* dst = splits > 1 ? part : O;
   // (tile, bin) pairs as a 2-D grid; the kernel renumbers them per XCD
@@ -580,7 +582,7 @@ bl_status_t launch_contract_tiled(const bl_conv_plan_s* p, Contract which, const
   }
 #undef BL_SHAPES
 #undef BL_GO
-  if (st != BL_OK || splits == 1) return st;
+  if (st != BL_OK || splits == 1 || parts > 1) return st;
   const unsigned long long n4 = total / 2;
   const unsigned long long blocks = (n4 + 255) / 256;
   return timed_launch("contract_reduce", 8.0 * total * (splits + 1), 0.0, s, [&](hipEvent_t e0, hipEvent_t e1) {

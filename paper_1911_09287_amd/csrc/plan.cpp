@@ -146,6 +146,21 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
         p->bp_s1 = p->bp_s2 = 0;
     }
   }
+  // a forward contraction with no more tiles than CUs (run with two wave
+  // groups per tile) is split along k instead, into up to 4 ranges of at least
+  // 8 stages and at most 768 tiles in all, when the 2-D inverse can add the
+  // partial spectra as it loads them (the 512-channel layer at c = 0.5: 192
+  // tiles of 32 stages become 768 of 8)
+  p->fwd_split = 1;
+  {
+    const BlContractTiling& t0 = p->ct[0];
+    const long tiles0 = (long)p->kept * ((p->N + t0.bm - 1) / t0.bm) * ((p->Cout + t0.bn - 1) / t0.bn);
+    const long st0 = (p->Cin + 15) / 16;
+    if (p->Lh > 1 && t0.splits == 1 && t0.ks == 2)
+      while (p->fwd_split < 4 && st0 % (2 * p->fwd_split) == 0 && st0 / (2 * p->fwd_split) >= 8 &&
+             tiles0 * 2 * p->fwd_split <= 768)
+        p->fwd_split *= 2;
+  }
   // partial sums of the weight-gradient inverse DFT over bin slices: enough
   // slices for ~1024 blocks of 256 (c, f) pairs, at least 16 bins per slice,
   // whole batches of 8 bins, and a slice's weights [bins][taps, padded as the
@@ -188,6 +203,7 @@ extern "C" bl_status_t bl_conv_plan_create(bl_conv_plan_t* out, const bl_conv_de
     const long mn[3] = {N * Co, N * Ci, Ci * Co};
     for (int i = 0; i < 3; ++i)
       if (p->ct[i].splits > 1) need = std::max(need, (size_t)p->ct[i].splits * Bk * mn[i] * cb);
+    if (p->fwd_split > 1) need = std::max(need, (size_t)p->fwd_split * Bk * mn[0] * cb);
     if (p->bp_s1 > 1) need = std::max(need, (size_t)p->bp_s1 * Bk * mn[1] * cb);
     if (p->bp_s2 > 1) need = std::max(need, (size_t)p->bp_s2 * Bk * mn[2] * cb);
     p->off_CPart = o;

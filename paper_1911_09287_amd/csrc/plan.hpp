@@ -90,6 +90,9 @@ struct bl_conv_plan_s {
   // the inverse transforms); 0 when the passes are not paired
   int bp_s1, bp_s2;
   int bp_bm, bp_bn;  // the paired launch's tile shape
+  // forward contraction split along k into partial spectra that the 2-D
+  // output inverse adds (1: not split), for launches of few tiles
+  int fwd_split;
   size_t off_X, off_W, off_DY, off_T, off_DW, off_Part, off_CPart, ws_bytes;
   // small device tables (1-D chirps and filter spectra, weight-gradient
   // inverse-DFT weights), built on a plan's first call that needs them on
