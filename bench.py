@@ -221,7 +221,7 @@ def roofline(agg):
 
 
 KERNEL_SOURCES = {"spec_fwd_1d": "bluestein.hip", "spec_inv_1d": "bluestein.hip", "spec_fwd_2d": "fft2d.hip",
-                  "spec_fwd_filt_2d": "fft2d.hip",
+                  "spec_fwd_filt_2d": "fft2d.hip", "spec_inv_wgrad_2d": "fft2d.hip",
                   "spec_inv_2d": "fft2d.hip", "contract_fwd": "contract.hip", "contract_dgrad": "contract.hip",
                   "contract_wgrad": "contract.hip", "contract_bwd": "contract.hip", "wgrad_idft": "direct.hip",
                   "spec_filt": "direct.hip"}

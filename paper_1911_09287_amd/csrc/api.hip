@@ -200,8 +200,17 @@ extern "C" bl_status_t bl_conv_backward(bl_conv_plan_t p, const float* dy, const
   } else if (st != BL_OK) {
     return st;
   }
-  BL_TRY(launch_spec_inv(p, s1 > 1 ? CP : T, dx, (long)p->N * p->Cin, p->Hi, p->Wi, p->pt, p->pl, s, s1, T));
-  return launch_wgrad_idft(p, s2 > 1 ? CP : DW, dw, reinterpret_cast<float*>(ws_at(ws, p->off_Part)), s, s2, DW);
+  float* part = reinterpret_cast<float*>(ws_at(ws, p->off_Part));
+  const long P = (long)p->N * p->Cin;
+  if (p->Lh > 1) {
+    // both inverses in one launch where the 2-D fast path and the sliced
+    // weight-gradient path allow it
+    const bl_status_t si = launch_fft2_inv_wgrad(p, s1 > 1 ? CP : T, dx, P, p->Hi, p->Wi, p->pt, p->pl, s1,
+                                                 (size_t)p->kept * P, s2 > 1 ? CP : DW, dw, part, s2, s);
+    if (si != BL_ERR_UNSUPPORTED) return si;
+  }
+  BL_TRY(launch_spec_inv(p, s1 > 1 ? CP : T, dx, P, p->Hi, p->Wi, p->pt, p->pl, s, s1, T));
+  return launch_wgrad_idft(p, s2 > 1 ? CP : DW, dw, part, s, s2, DW);
 }
 
 // ---------------------------------------------------------------------------

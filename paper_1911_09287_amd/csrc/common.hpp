@@ -171,5 +171,12 @@ bl_status_t launch_fft2_fwd(const bl_conv_plan_s* p, const float* in, void* out,
                             int oj, hipStream_t s);
 bl_status_t launch_fft2_inv(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
                             int cj, hipStream_t s, int nsplit = 1, size_t pstride = 0);
+// The input-gradient inverse (as launch_fft2_inv) and the weight-gradient
+// inverse DFT (as launch_wgrad_idft on its sliced path, wnsplit partial
+// spectra of DW) in one launch, then the slice sum; 3 x 3 filters;
+// BL_ERR_UNSUPPORTED (nothing enqueued) where either has no such path.
+bl_status_t launch_fft2_inv_wgrad(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW,
+                                  int ci, int cj, int nsplit, size_t pstride, const float2* DW, float* dw, float* part,
+                                  int wnsplit, hipStream_t s);
 
 }  // namespace blc

@@ -18,6 +18,7 @@
 
 #include "common.hpp"
 #include "filt.hpp"
+#include "wgrad.hpp"
 
 namespace blc {
 namespace {
@@ -201,104 +202,13 @@ __global__ __launch_bounds__(kThreads) void k_spec_filt(const float* __restrict_
 // plan.  Results do not depend on scheduling: every sum is taken in a fixed
 // order.
 // ---------------------------------------------------------------------------
-// Channel tile of the weight-gradient inverse DFT: TC input x 256 / TC output
-// channels.  Rows wider than 256 output channels take 32-channel spans of 8
-// input channels, so that the gradient rows dw[f][c0 .. c0 + 8][taps] are
-// written 8 x taps floats at a time; otherwise a block spans whole rows of
-// one input channel.
-inline int chan_tile(int taps, int F) { return (taps <= 16 && F > 256) ? 8 : 1; }
-
-struct WgradGeom {
-  int F, C, Kh, Kw, T;
-  int Lh, Lw, r_h, R, V;
-  int bins_per_chunk, chunks;
-  int tiles_f;  // 16-filter tiles along F (k_wgrad_tile)
-  int nsplit;   // k_wgrad_idft: partial spectra of DW (their slices are more slices; 0 or 1: one)
-  unsigned long long pstride;  // complex values between two partial spectra
-};
-
 template <int TMAX, int TC>
 __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restrict__ DW, const float2* __restrict__ Et,
                                                          float* __restrict__ dw, float* __restrict__ part,
                                                          WgradGeom g) {
-  constexpr int TF = kThreads / TC;
   extern __shared__ float2 E[];  // bins_per_chunk x TMAX, zero beyond T (no branches in the bin loop)
-  __shared__ float res[TC > 1 ? TF * TC * TMAX : 1];
-  const int B = g.R * g.V;
-  // slice blockIdx.y: bin chunk blockIdx.y % chunks of partial spectrum blockIdx.y / chunks
-  const int sp = blockIdx.y / g.chunks;
-  const int b0 = (blockIdx.y - sp * g.chunks) * g.bins_per_chunk;
-  const int nb = min(g.bins_per_chunk, B - b0);
-  DW += (size_t)sp * g.pstride;
-  // copy this slice of the table, four loads of a thread in flight together
-  const float2* Es = Et + (size_t)b0 * g.T;
-  for (int e0 = threadIdx.x; e0 < nb * TMAX; e0 += 4 * kThreads) {
-    float2 v[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int e = e0 + k * kThreads, bb = e / TMAX, t = e - bb * TMAX;
-      v[k] = (e < nb * TMAX && t < g.T) ? Es[bb * g.T + t] : make_float2(0.f, 0.f);
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (e0 + k * kThreads < nb * TMAX) E[e0 + k * kThreads] = v[k];
-  }
-  __syncthreads();
-  const long Q = (long)g.C * g.F;
-  // TC == 1: 256 consecutive pairs q = c F + f per block; else a TC x TF tile
-  const int tiles_f = (g.F + TF - 1) / TF;
-  const int c0 = (blockIdx.x / tiles_f) * TC, f0 = (blockIdx.x % tiles_f) * TF;
-  const int tc = threadIdx.x / TF, tf = threadIdx.x - (threadIdx.x / TF) * TF;
-  const long q1 = (long)blockIdx.x * kThreads + threadIdx.x;
-  const int c = TC == 1 ? (int)(q1 / g.F) : c0 + tc, f = TC == 1 ? (int)(q1 % g.F) : f0 + tf;
-  const bool valid = TC == 1 ? q1 < Q : (c < g.C && f < g.F);
-  float acc[TMAX];
-#pragma unroll
-  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
-  const float2* src = DW + (size_t)b0 * Q + (valid ? (long)c * g.F + f : 0);
-  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
-  for (int bb = 0; bb < nb; bb += 8) {
-    float2 d[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, nb - 1) * Q];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const bool in = bb + j < nb;
-      const float2 dj = in ? d[j] : make_float2(0.f, 0.f);
-      const float2* Eb = E + min(bb + j, nb - 1) * TMAX;
-#pragma unroll
-      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
-    }
-  }
-  if (gridDim.y > 1) {
-    if (valid) {
-#pragma unroll
-      for (int t = 0; t < TMAX; ++t)
-        if (t < g.T) part[((size_t)blockIdx.y * g.T + t) * Q + (size_t)c * g.F + f] = acc[t];
-    }
-    return;
-  }
-  if (TC == 1) {
-    if (valid) {
-      float* o = dw + ((size_t)f * g.C + c) * g.T;
-#pragma unroll
-      for (int t = 0; t < TMAX; ++t)
-        if (t < g.T) o[t] = acc[t];
-    }
-    return;
-  }
-  // transpose through LDS: res[tf][tc][t], then each output row f gets its
-  // TC x T contiguous floats
-#pragma unroll
-  for (int t = 0; t < TMAX; ++t)
-    if (t < g.T) res[(tf * TC + tc) * g.T + t] = acc[t];
-  __syncthreads();
-  const int seg = TC * g.T;
-  for (int e = threadIdx.x; e < TF * seg; e += kThreads) {
-    const int ef = e / seg, r = e - ef * seg;
-    const int oc = c0 + r / g.T, of = f0 + ef;
-    if (oc < g.C && of < g.F) dw[((size_t)of * g.C + c0) * g.T + r] = res[e];
-  }
+  __shared__ float res[wgrad_res_floats<TMAX, TC>()];
+  wgrad_idft_block<TMAX, TC>(DW, Et, dw, part, g, blockIdx.x, blockIdx.y, gridDim.y > 1, E, res);
 }
 
 // One thread per (q, t): sums the slices in a fixed order (eight independent
@@ -701,6 +611,56 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
   return BL_ERR_UNSUPPORTED;
 }
 
+namespace {
+// The one-pass wide path applies (see launch_wgrad_idft).
+bool wgrad_wide(const bl_conv_plan_s* p) {
+  const long Q = (long)p->Cin * p->Cout;
+  const int B = (int)p->kept, T = p->Kh * p->Kw;
+  const int tmax_w = T <= 9 ? T : 16;
+  return (Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && T <= 16 &&
+         (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds && Q < 2147483647L;
+}
+
+bl_status_t wgrad_table(const bl_conv_plan_s* p, const float2** Et) {
+  const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
+  return plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, Et);
+}
+}  // namespace
+
+bool wgrad_sliced_setup(const bl_conv_plan_s* p, int nsplit, WgradGeom& g, long* xblocks, int* slices, size_t* lds,
+                        int* tc, const float2** Et) {
+  g = WgradGeom{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0,
+                (p->Cout + 15) / 16, 1, 0};
+  if (g.T > 64 || p->wg_groups > 0 || wgrad_wide(p)) return false;
+  const long Q = (long)p->Cin * p->Cout;
+  if (nsplit > 1) {
+    if (p->wg_chunks <= 1 || nsplit > std::max(1, p->bp_s2)) return false;  // partial-sum area sized for these
+    g.nsplit = nsplit;
+    g.pstride = (unsigned long long)p->kept * Q;
+  }
+  g.chunks = p->wg_chunks;  // the workspace holds partial sums for this many slices (per partial spectrum)
+  g.bins_per_chunk = p->wg_bins;
+  if ((long)g.chunks * g.nsplit > 65535) return false;
+  const int tmax = g.T <= 9 ? g.T : g.T <= 16 ? 16 : g.T <= 32 ? 32 : 64;  // as instantiated
+  *lds = (size_t)g.bins_per_chunk * tmax * sizeof(float2);
+  if ((long)*lds > kWgradSliceLds) return false;
+  const int TC = chan_tile(g.T, p->Cout), TF = kThreads / TC;
+  *tc = TC;
+  *xblocks = TC == 1 ? (Q + kThreads - 1) / kThreads : (long)((p->Cin + TC - 1) / TC) * ((p->Cout + TF - 1) / TF);
+  *slices = g.chunks * g.nsplit;
+  return wgrad_table(p, Et) == BL_OK;
+}
+
+bl_status_t launch_wgrad_reduce(const bl_conv_plan_s* p, const float* part, float* dw, const WgradGeom& g,
+                                hipStream_t s) {
+  const long Q = (long)p->Cin * p->Cout;
+  const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
+  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks * g.nsplit + 1), 0.0, s,
+                      [&](hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, e0, e1, 0, part, dw, g);
+  });
+}
+
 bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* dw, float* part, hipStream_t s,
                               int nsplit, float2* tmp) {
   WgradGeom g{p->Cout, p->Cin, p->Kh, p->Kw, p->Kh * p->Kw, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0,
@@ -708,8 +668,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept;
   const int tmax_w = g.T <= 9 ? g.T : 16;
-  const bool wide = (Q / 64 >= 256 || B <= 256) && p->Cout <= 256 && g.T <= 16 &&
-                    (long)(B * tmax_w * sizeof(float2)) <= kWgradSliceLds && Q < 2147483647L;
+  const bool wide = wgrad_wide(p);
   if (nsplit > 1) {
     // partial spectra: more slices of the sliced path (whose partial-sum area
     // the plan sized for them), else summed into tmp first
@@ -729,8 +688,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
   // tiled kernel below); otherwise bin slices and a fixed-order sum
   if (g.T > 64) return BL_ERR_UNSUPPORTED;
   const float2* Et = nullptr;  // E[bin][t], built once per plan
-  const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
-  const bl_status_t ts = plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, &Et);
+  const bl_status_t ts = wgrad_table(p, &Et);
   if (ts != BL_OK) return ts;
   if (p->wg_groups > 0) {  // 16 x 16 channel tiles over all bins
     const int tmax = wgrad_tmax(g.T), NG = p->wg_groups;
@@ -813,11 +771,7 @@ bl_status_t launch_wgrad_idft(const bl_conv_plan_s* p, const float2* DW, float* 
       else st = go(k_wgrad_idft<64, 1>);
   }
   if (st != BL_OK || g.chunks * g.nsplit == 1) return st;
-  const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
-  return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks * g.nsplit + 1), 0.0, s,
-                      [&](hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, e0, e1, 0, part, dw, g);
-  });
+  return launch_wgrad_reduce(p, part, dw, g, s);
 }
 
 bl_status_t launch_contract_generic(const bl_conv_plan_s* p, Contract which, const void* A, const void* Bm, float2* O,

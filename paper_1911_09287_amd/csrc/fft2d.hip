@@ -25,6 +25,7 @@
 
 #include "common.hpp"
 #include "filt.hpp"
+#include "wgrad.hpp"
 
 namespace blc {
 namespace {
@@ -335,16 +336,16 @@ __global__ __launch_bounds__(kThreads) void k_fft2_fwd_filt(const float* __restr
     spec_filt_block<KH, KW, S>(w, roots, wout, fg, blockIdx.x - nx, gridDim.x - nx, sm);
 }
 
+// One block (id of nb) of the inverse transform; sm: the launch's LDS.
 template <int MH, int MW, bool SPLIT, bool PARTS>
-__global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
-                                                       Fft2Args g) {
+__device__ __forceinline__ void fft2_inv_block(const float2* __restrict__ in, float* __restrict__ out,
+                                               const Fft2Args& g, unsigned id, unsigned nb, float2* sm) {
   constexpr int LH = 2 * MH, LW = 2 * MW, LW1 = LW + 1, LH1 = LH + 1;
-  extern __shared__ float2 sm[];
   float2* Zs = sm;                           // column results, column-major per plane
   float* ys = reinterpret_cast<float*>(sm);  // output staging: G*OH grid rows of LW1 floats; aliases Zs
   const int tid = threadIdx.x;
   const int OH = g.Hin, OW = g.Win;
-  const unsigned p0 = plane_group(blockIdx.x, gridDim.x, g.K & ~kInvVec4) * (unsigned)g.G;
+  const unsigned p0 = plane_group(id, nb, g.K & ~kInvVec4) * (unsigned)g.G;
   const int np = (int)min((unsigned)g.G, g.P - p0);
 
   if constexpr (SPLIT) {
@@ -463,6 +464,35 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict_
   }
 }
 
+template <int MH, int MW, bool SPLIT, bool PARTS>
+__global__ __launch_bounds__(kThreads) void k_fft2_inv(const float2* __restrict__ in, float* __restrict__ out,
+                                                       Fft2Args g) {
+  extern __shared__ float2 sm[];
+  fft2_inv_block<MH, MW, SPLIT, PARTS>(in, out, g, blockIdx.x, gridDim.x, sm);
+}
+
+// The input-gradient inverse and the sliced weight-gradient inverse DFT of a
+// backward pass in one launch (they are independent): blocks [0, nx) invert
+// planes of DX, the rest are weight-gradient blocks (channel block j % wx,
+// slice j / wx).  The weight-gradient launch is short and latency-bound;
+// beside the transform its blocks fill the CUs that the transform's last
+// blocks leave idle, and one launch is saved.
+template <int MH, int MW, bool SPLIT, bool PARTS, int TMAX, int TC>
+__global__ __launch_bounds__(kThreads) void k_fft2_inv_wgrad(const float2* __restrict__ in, float* __restrict__ out,
+                                                             Fft2Args g, unsigned nx, const float2* __restrict__ DW,
+                                                             const float2* __restrict__ Et, float* __restrict__ dw,
+                                                             float* __restrict__ part, WgradGeom wg, unsigned wx,
+                                                             unsigned wslices) {
+  extern __shared__ float2 sm[];
+  __shared__ float res[wgrad_res_floats<TMAX, TC>()];
+  if (blockIdx.x < nx) {
+    fft2_inv_block<MH, MW, SPLIT, PARTS>(in, out, g, blockIdx.x, nx, sm);
+  } else {
+    const unsigned j = blockIdx.x - nx;
+    wgrad_idft_block<TMAX, TC>(DW, Et, dw, part, wg, j % wx, j / wx, wslices > 1, sm, res);
+  }
+}
+
 // ceil(2^32 / d) for d > 1 (d = 1 is handled by the kernels directly).
 unsigned magic_for(unsigned d) { return d > 1 ? (unsigned)((0x100000000ull + d - 1) / d) : 0u; }
 
@@ -548,9 +578,18 @@ bl_status_t launch_fwd_t(const bl_conv_plan_s* p, const float* in, void* out, lo
   });
 }
 
+// Launch geometry of the inverse transform.
+struct InvSetup {
+  Fft2Args g;
+  long blocks;
+  size_t lds;
+  double bytes, flops;
+  bool split;
+};
+
 template <int MH, int MW>
-bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
-                         int cj, hipStream_t s, int nsplit, size_t pstride) {
+bl_status_t inv_setup(const bl_conv_plan_s* p, long P, int OH, int OW, int ci, int cj, int nsplit, size_t pstride,
+                      InvSetup& f) {
   constexpr int LH = 2 * MH, LW = 2 * MW;
   if ((double)p->kept * P >= 2147483647.0 || P >= 2147483647L) return BL_ERR_UNSUPPORTED;
   const bool vec4 = OW % 4 == 0;
@@ -571,24 +610,77 @@ bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, 
   if (OH > kThreads || lds_for(G) > kMaxLds) return BL_ERR_UNSUPPORTED;
   g.G = G;
   g.K = line_groups(G, 8) | (vec4 ? kInvVec4 : 0u);
-  const long blocks = (P + G - 1) / G;
-  const double bytes = (double)P * p->kept * 8 * g.nsplit + (double)P * OH * OW * 4;
-  const double flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
-  const bool split = column_split(false, MH, G, p->V);
-  return timed_launch("spec_inv_2d", bytes, flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
-    const dim3 grid((unsigned)blocks), block(kThreads);
-    const size_t lds = lds_for(G);
+  f.g = g;
+  f.blocks = (P + G - 1) / G;
+  f.lds = lds_for(G);
+  f.bytes = (double)P * p->kept * 8 * g.nsplit + (double)P * OH * OW * 4;
+  f.flops = (double)P * (p->V * 5.0 * LH * std::log2((double)LH) + OH * 2.5 * LW * std::log2((double)LW));
+  f.split = column_split(false, MH, G, p->V);
+  return BL_OK;
+}
+
+template <int MH, int MW>
+bl_status_t launch_inv_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                         int cj, hipStream_t s, int nsplit, size_t pstride) {
+  InvSetup f;
+  const bl_status_t is = inv_setup<MH, MW>(p, P, OH, OW, ci, cj, nsplit, pstride, f);
+  if (is != BL_OK) return is;
+  const Fft2Args g = f.g;
+  const size_t lds = f.lds;
+  return timed_launch("spec_inv_2d", f.bytes, f.flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+    const dim3 grid((unsigned)f.blocks), block(kThreads);
     if (g.nsplit > 1) {
-      if (split)
+      if (f.split)
         hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true, true>), grid, block, lds, s, e0, e1, 0, in, out, g);
       else
         hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false, true>), grid, block, lds, s, e0, e1, 0, in, out, g);
-    } else if (split) {
+    } else if (f.split) {
       hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, true, false>), grid, block, lds, s, e0, e1, 0, in, out, g);
     } else {
       hipExtLaunchKernelGGL((k_fft2_inv<MH, MW, false, false>), grid, block, lds, s, e0, e1, 0, in, out, g);
     }
   });
+}
+
+// The input-gradient inverse beside the sliced weight-gradient inverse DFT
+// (3 x 3 filters), then the weight gradient's slice sum if it has slices.
+template <int MH, int MW>
+bl_status_t launch_inv_wgrad_t(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW, int ci,
+                               int cj, int nsplit, size_t pstride, const float2* DW, float* dw, float* part,
+                               int wnsplit, hipStream_t s) {
+  if (p->Kh != 3 || p->Kw != 3) return BL_ERR_UNSUPPORTED;
+  InvSetup f;
+  bl_status_t st = inv_setup<MH, MW>(p, P, OH, OW, ci, cj, nsplit, pstride, f);
+  if (st != BL_OK) return st;
+  WgradGeom wg;
+  long wx;
+  int slices, tc;
+  size_t wlds;
+  const float2* Et;
+  if (!wgrad_sliced_setup(p, wnsplit, wg, &wx, &slices, &wlds, &tc, &Et)) return BL_ERR_UNSUPPORTED;
+  const long total = f.blocks + wx * slices;
+  if (total >= 2147483647L) return BL_ERR_UNSUPPORTED;
+  const Fft2Args g = f.g;
+  const size_t lds = std::max(f.lds, wlds);
+  const unsigned nx = (unsigned)f.blocks, wxu = (unsigned)wx, ws = (unsigned)slices;
+  const double wbytes = (double)p->Cin * p->Cout * ((double)p->kept * 8 * wg.nsplit + wg.T * 4);
+  auto go = [&](auto kern) {
+    return timed_launch("spec_inv_wgrad_2d", f.bytes + wbytes, f.flops, s, [&](hipEvent_t e0, hipEvent_t e1) {
+      hipExtLaunchKernelGGL(kern, dim3((unsigned)total), dim3(kThreads), lds, s, e0, e1, 0, in, out, g, nx, DW, Et, dw,
+                            part, wg, wxu, ws);
+    });
+  };
+  if (g.nsplit > 1)
+    st = f.split ? (tc == 8 ? go(k_fft2_inv_wgrad<MH, MW, true, true, 9, 8>) : go(k_fft2_inv_wgrad<MH, MW, true, true, 9, 1>))
+                 : (tc == 8 ? go(k_fft2_inv_wgrad<MH, MW, false, true, 9, 8>)
+                            : go(k_fft2_inv_wgrad<MH, MW, false, true, 9, 1>));
+  else
+    st = f.split ? (tc == 8 ? go(k_fft2_inv_wgrad<MH, MW, true, false, 9, 8>)
+                            : go(k_fft2_inv_wgrad<MH, MW, true, false, 9, 1>))
+                 : (tc == 8 ? go(k_fft2_inv_wgrad<MH, MW, false, false, 9, 8>)
+                            : go(k_fft2_inv_wgrad<MH, MW, false, false, 9, 1>));
+  if (st != BL_OK || slices == 1) return st;
+  return launch_wgrad_reduce(p, part, dw, wg, s);
 }
 
 // The forward transform of x beside the filter transform (3 x 3 filters).
@@ -652,6 +744,17 @@ bl_status_t launch_fft2_fwd_filt(const bl_conv_plan_s* p, const float* in, void*
 #define X(a, b)                         \
   if (p->Lh == 2 * a && p->Lw == 2 * b) \
     return launch_fwd_filt_t<a, b>(p, in, out, P, Hin, Win, oi, oj, w, wout, s);
+  BL_FFT2_GRIDS(X)
+#undef X
+  return BL_ERR_UNSUPPORTED;
+}
+
+bl_status_t launch_fft2_inv_wgrad(const bl_conv_plan_s* p, const float2* in, float* out, long P, int OH, int OW,
+                                  int ci, int cj, int nsplit, size_t pstride, const float2* DW, float* dw, float* part,
+                                  int wnsplit, hipStream_t s) {
+#define X(a, b)                                                                                                   \
+  if (p->Lh == 2 * a && p->Lw == 2 * b)                                                                           \
+    return launch_inv_wgrad_t<a, b>(p, in, out, P, OH, OW, ci, cj, nsplit, pstride, DW, dw, part, wnsplit, s);
   BL_FFT2_GRIDS(X)
 #undef X
   return BL_ERR_UNSUPPORTED;
