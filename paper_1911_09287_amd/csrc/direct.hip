@@ -235,58 +235,12 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restri
   dw[((size_t)f * g.C + c) * g.T + t] = tot;
 }
 
-// Wide layers (many (c, f) pairs): one block per 64 consecutive pairs and all
-// bins, its four waves each reducing a quarter of the bins; the quarters are
-// added in a fixed order through LDS and written straight to dw, so no
-// partial sums leave the block.  E comes from a table built once per plan.
 template <int TMAX, int NW>
 __global__ __launch_bounds__(64 * NW) void k_wgrad_wide(const float2* __restrict__ DW, const float2* __restrict__ Et,
                                                         float* __restrict__ dw, WgradGeom g) {
   extern __shared__ float2 E[];  // [kept][TMAX], zero beyond T: the bin loop has no branches
-  __shared__ float red[NW][64][TMAX];
-  const int B = g.R * g.V;
-  for (int e = threadIdx.x; e < B * TMAX; e += blockDim.x) {
-    const int bb = e / TMAX, t = e - bb * TMAX;
-    E[e] = t < g.T ? Et[bb * g.T + t] : make_float2(0.f, 0.f);
-  }
-  __syncthreads();
-  const unsigned Q = (unsigned)g.C * g.F;
-  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
-  const unsigned q = blockIdx.x * 64u + lane;
-  const bool valid = q < Q;
-  const int bb0 = grp * B / NW, bb1 = (grp + 1) * B / NW;
-  float acc[TMAX];
-#pragma unroll
-  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
-  const float2* src = DW + (valid ? q : 0u);
-  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
-  for (int bb = bb0; bb < bb1; bb += 8) {
-    float2 d[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, bb1 - 1) * Q];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const bool in = bb + j < bb1;
-      const float2 dj = in ? d[j] : make_float2(0.f, 0.f);
-      const float2* Eb = E + min(bb + j, bb1 - 1) * TMAX;
-#pragma unroll
-      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < TMAX; ++t) red[grp][lane][t] = acc[t];
-  __syncthreads();
-  if (grp == 0 && valid) {
-    const int c = (int)(q / g.F), f = (int)(q % g.F);
-    float* o = dw + ((size_t)f * g.C + c) * g.T;
-#pragma unroll
-    for (int t = 0; t < TMAX; ++t) {
-      float sum = red[0][lane][t];
-#pragma unroll
-      for (int w = 1; w < NW; ++w) sum += red[w][lane][t];
-      if (t < g.T) o[t] = sum;
-    }
-  }
+  __shared__ float red[NW * 64 * TMAX];
+  wgrad_wide_block<TMAX, NW>(DW, Et, dw, g, blockIdx.x, E, red);
 }
 
 // Layers of 128 to 511 tiles of 16 x 16 channel pairs: a block
@@ -611,8 +565,6 @@ bl_status_t launch_spec_filt(const bl_conv_plan_s* p, const float* w, void* out,
   return BL_ERR_UNSUPPORTED;
 }
 
-namespace {
-// The one-pass wide path applies (see launch_wgrad_idft).
 bool wgrad_wide(const bl_conv_plan_s* p) {
   const long Q = (long)p->Cin * p->Cout;
   const int B = (int)p->kept, T = p->Kh * p->Kw;
@@ -625,7 +577,6 @@ bl_status_t wgrad_table(const bl_conv_plan_s* p, const float2** Et) {
   const std::vector<long> key{2, p->Lh, p->Lw, p->r_h, p->R, p->V, p->Kh, p->Kw};
   return plan_table(p, key, [&](std::vector<float2>& h) { host_wgrad_weights(p, h); }, Et);
 }
-}  // namespace
 
 bool wgrad_sliced_setup(const bl_conv_plan_s* p, int nsplit, WgradGeom& g, long* xblocks, int* slices, size_t* lds,
                         int* tc, const float2** Et) {

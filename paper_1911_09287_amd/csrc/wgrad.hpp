@@ -116,6 +116,66 @@ __device__ __forceinline__ void wgrad_idft_block(const float2* __restrict__ DW, 
   }
 }
 
+// Wide layers (many (c, f) pairs): one block per 64 consecutive pairs and all
+// bins, its four waves each reducing a quarter of the bins; the quarters are
+// added in a fixed order through LDS and written straight to dw, so no
+// partial sums leave the block.  E comes from a table built once per plan.
+// E: the launch's dynamic LDS ([kept][TMAX] float2, zero beyond T: the bin loop
+// has no branches); red: NW * 64 * TMAX floats.  Block bx of 64 * NW threads.
+template <int TMAX, int NW>
+__device__ __forceinline__ void wgrad_wide_block(const float2* __restrict__ DW, const float2* __restrict__ Et,
+                                                 float* __restrict__ dw, const WgradGeom& g, unsigned bx, float2* E,
+                                                 float* red) {
+  const int B = g.R * g.V;
+  for (int e = threadIdx.x; e < B * TMAX; e += blockDim.x) {
+    const int bb = e / TMAX, t = e - bb * TMAX;
+    E[e] = t < g.T ? Et[bb * g.T + t] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  const unsigned Q = (unsigned)g.C * g.F;
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const unsigned q = bx * 64u + lane;
+  const bool valid = q < Q;
+  const int bb0 = grp * B / NW, bb1 = (grp + 1) * B / NW;
+  float acc[TMAX];
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
+  const float2* src = DW + (valid ? q : 0u);
+  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
+  for (int bb = bb0; bb < bb1; bb += 8) {
+    float2 d[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, bb1 - 1) * Q];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = bb + j < bb1;
+      const float2 dj = in ? d[j] : make_float2(0.f, 0.f);
+      const float2* Eb = E + min(bb + j, bb1 - 1) * TMAX;
+#pragma unroll
+      for (int t = 0; t < TMAX; ++t) acc[t] = fmaf(dj.x, Eb[t].x, fmaf(-dj.y, Eb[t].y, acc[t]));
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < TMAX; ++t) red[(grp * 64 + lane) * TMAX + t] = acc[t];
+  __syncthreads();
+  if (grp == 0 && valid) {
+    const int c = (int)(q / g.F), f = (int)(q % g.F);
+    float* o = dw + ((size_t)f * g.C + c) * g.T;
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t) {
+      float sum = red[lane * TMAX + t];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sum += red[(w * 64 + lane) * TMAX + t];
+      if (t < g.T) o[t] = sum;
+    }
+  }
+}
+
+// The one-pass wide path applies to a plan (see launch_wgrad_idft).
+bool wgrad_wide(const bl_conv_plan_s* p);
+// Its E table (E[bin][t], built once per plan).
+bl_status_t wgrad_table(const bl_conv_plan_s* p, const float2** Et);
+
 // Geometry of the sliced path for a plan (nsplit partial spectra of DW): the
 // channel blocks, slices (nsplit x bin chunks), dynamic LDS bytes, channel
 // tile and the E table; false when the plan's inverse DFT takes another path
