@@ -25,7 +25,7 @@ LIBRARY_NAMES = OrderedDict([
     ("spec_fwd_2d", r"k_fft2_fwd<"),
     ("spec_fwd_filt_2d", r"k_fft2_fwd_filt<"),
     ("spec_inv_2d", r"k_fft2_inv<"),
-    ("spec_inv_wgrad_2d", r"k_fft2_inv_wgrad<"),
+    ("spec_inv_wgrad_2d", r"k_fft2_inv_wgrad(_wide)?<"),
     ("spec_fwd_1d", r"k_bluestein1k<[02],"),
     ("spec_inv_1d", r"k_bluestein1k<[13],"),
     ("spec_fwd_direct", r"k_spec_fwd<"),
