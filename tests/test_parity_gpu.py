@@ -398,6 +398,60 @@ def test_combined_backward(torch):
         assert max(gaps) <= 1e-5, gaps
 
 
+def test_combined_backward_random_medium(torch):
+    """Forward and bl_conv_backward on random medium layers whose channel and
+    batch counts reach the tiled contractions (multiples of the tile sizes and
+    ragged counts, up to about 600 channels), so that the plan's choices of
+    tile shape, pairing of the two backward contractions and k splits (partial
+    spectra added by the inverses or the weight-gradient slices) vary from case
+    to case; 2-D and 1-D, against the oracle and the separate backward calls."""
+    rng = np.random.default_rng(3100)
+    chans = [16, 32, 48, 64, 96, 128, 160, 192, 256, 320, 384, 512, 17, 33, 70, 130, 200, 260, 513, 600]
+    dev = torch.device("cuda:0")
+    done = 0
+    while done < 14:
+        ndim = 2 if done < 10 else 1
+        N = int(rng.choice([1, 2, 8, 32, 64, 100, 128, 160]))
+        ci, co = int(rng.choice(chans)), int(rng.choice(chans))
+        K = int(rng.choice([3, 3, 3, 1, 5]))
+        if ndim == 2:
+            H = int(rng.choice([4, 6, 8, 12, 16, 20]))
+            layer = synth.Layer("rand_med2d", 2, N, ci, co, H, H, K, (K // 2,) * 4, "blur")
+            size = N * ci * co * H * H
+        else:
+            H = int(rng.integers(100, 600))
+            layer = synth.Layer("rand_med1d", 1, N, ci, co, H, 1, K, (K // 2, K // 2), "walk")
+            size = N * ci * co * H
+        if size > 4e8:
+            continue
+        c = float(rng.choice([0.0, 0.25, 0.5, 0.75]))
+        say(f"[backward-rand] {layer} c={c}")
+        x, w, dy = synth.random_inputs(layer, 3200 + done)
+        done += 1
+        plan = blconv.plan_for_layer(layer, c)
+        ws = plan.workspace(dev)
+        ws.fill_(0xFF)
+        xt, wt, dyt = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        y = torch.full(plan.y_shape(), float("nan"), device=dev)
+        dx = torch.full(plan.x_shape(), float("nan"), device=dev)
+        dw = torch.full(plan.w_shape(), float("nan"), device=dev)
+        plan.forward(xt, wt, y, ws)
+        plan.backward(dyt, None, None, dx, dw, ws, flags=blconv.BL_REUSE_W | blconv.BL_REUSE_X)
+        sdx = torch.full(plan.x_shape(), float("nan"), device=dev)
+        sdw = torch.full(plan.w_shape(), float("nan"), device=dev)
+        plan.backward_input(dyt, wt, sdx, ws)
+        plan.backward_weight(xt, dyt, sdw, ws)
+        torch.cuda.synchronize()
+        got = (y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy())
+        ref = oracle_passes(layer, c, x, w, dy)
+        errs = [err(a, b) for a, b in zip(got, ref)]
+        gaps = [rel(a, b.cpu().numpy()) for a, b in zip(got[1:], (sdx, sdw))]
+        say(f"    err y={errs[0]:.2e} dx={errs[1]:.2e} dw={errs[2]:.2e}; vs separate calls {gaps}")
+        assert all(np.isfinite(a).all() for a in got)
+        assert max(errs) <= TOL, errs
+        assert max(gaps) <= 1e-5, gaps
+
+
 def test_thin_contractions(torch):
     """Layers where a contraction size (batch, input or output channels) is at
     most 8, which run the memory-bound vector-ALU contraction: lanes over
