@@ -494,8 +494,9 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv_wgrad(const float2* __res
 }
 
 // The same with the one-pass wide weight-gradient body (64 pairs and all bins
-// per block, four waves each over a quarter of the bins).
-template <int MH, int MW, bool SPLIT, bool PARTS, int TMAX>
+// per block, four waves each over a quarter of the bins); WPARTS: DW arrives
+// as partial spectra, summed as they are loaded.
+template <int MH, int MW, bool SPLIT, bool PARTS, int TMAX, bool WPARTS>
 __global__ __launch_bounds__(kThreads) void k_fft2_inv_wgrad_wide(const float2* __restrict__ in,
                                                                   float* __restrict__ out, Fft2Args g, unsigned nx,
                                                                   const float2* __restrict__ DW,
@@ -506,7 +507,7 @@ __global__ __launch_bounds__(kThreads) void k_fft2_inv_wgrad_wide(const float2* 
   if (blockIdx.x < nx)
     fft2_inv_block<MH, MW, SPLIT, PARTS>(in, out, g, blockIdx.x, nx, sm);
   else
-    wgrad_wide_block<TMAX, 4>(DW, Et, dw, wg, blockIdx.x - nx, sm, red);
+    wgrad_wide_block<TMAX, 4, WPARTS>(DW, Et, dw, wg, blockIdx.x - nx, sm, red);
 }
 
 // ceil(2^32 / d) for d > 1 (d = 1 is handled by the kernels directly).
@@ -674,17 +675,18 @@ bl_status_t launch_inv_wgrad_t(const bl_conv_plan_s* p, const float2* in, float*
   size_t wlds;
   const float2* Et;
   if (!wgrad_sliced_setup(p, wnsplit, wg, &wx, &slices, &wlds, &tc, &Et)) {
-    // the wide one-pass body, whole spectra only
-    if (wnsplit > 1 || !wgrad_wide(p) || wgrad_table(p, &Et) != BL_OK) return BL_ERR_UNSUPPORTED;
-    wg = WgradGeom{p->Cout, p->Cin, p->Kh, p->Kw, 9, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0, 0, 1, 0};
+    // the wide one-pass body (partial spectra summed as they are loaded)
+    if (!wgrad_wide(p) || wgrad_table(p, &Et) != BL_OK) return BL_ERR_UNSUPPORTED;
     const long Q = (long)p->Cin * p->Cout;
+    wg = WgradGeom{p->Cout, p->Cin, p->Kh, p->Kw, 9, p->Lh, p->Lw, p->r_h, p->R, p->V, 0, 0, 0,
+                   std::max(1, wnsplit), (unsigned long long)p->kept * Q};
     const long wblocks = (Q + 63) / 64;
     const long total = f.blocks + wblocks;
     if (total >= 2147483647L) return BL_ERR_UNSUPPORTED;
     const size_t lds = std::max(f.lds, (size_t)p->kept * 9 * sizeof(float2));
     const Fft2Args g = f.g;
     const unsigned nx = (unsigned)f.blocks;
-    const double wbytes = (double)Q * ((double)p->kept * 8 + 9 * 4);
+    const double wbytes = (double)Q * ((double)p->kept * 8 * wg.nsplit + 9 * 4);
     auto go = [&](auto kern) {
       // the dynamic part (at most 64 KB) plus the static reduction buffer can pass 64 KB
       const bl_status_t at = lds_opt_in(reinterpret_cast<const void*>(kern), 96 * 1024);
@@ -694,9 +696,15 @@ bl_status_t launch_inv_wgrad_t(const bl_conv_plan_s* p, const float2* in, float*
                               dw, wg);
       });
     };
+    if (g.nsplit > 1 && wg.nsplit > 1) return BL_ERR_UNSUPPORTED;  // the plan splits one pass at most
     if (g.nsplit > 1)
-      return f.split ? go(k_fft2_inv_wgrad_wide<MH, MW, true, true, 9>) : go(k_fft2_inv_wgrad_wide<MH, MW, false, true, 9>);
-    return f.split ? go(k_fft2_inv_wgrad_wide<MH, MW, true, false, 9>) : go(k_fft2_inv_wgrad_wide<MH, MW, false, false, 9>);
+      return f.split ? go(k_fft2_inv_wgrad_wide<MH, MW, true, true, 9, false>)
+                     : go(k_fft2_inv_wgrad_wide<MH, MW, false, true, 9, false>);
+    if (wg.nsplit > 1)
+      return f.split ? go(k_fft2_inv_wgrad_wide<MH, MW, true, false, 9, true>)
+                     : go(k_fft2_inv_wgrad_wide<MH, MW, false, false, 9, true>);
+    return f.split ? go(k_fft2_inv_wgrad_wide<MH, MW, true, false, 9, false>)
+                   : go(k_fft2_inv_wgrad_wide<MH, MW, false, false, 9, false>);
   }
   const long total = f.blocks + wx * slices;
   if (total >= 2147483647L) return BL_ERR_UNSUPPORTED;

@@ -117,12 +117,13 @@ __device__ __forceinline__ void wgrad_idft_block(const float2* __restrict__ DW, 
 }
 
 // Wide layers (many (c, f) pairs): one block per 64 consecutive pairs and all
-// bins, its four waves each reducing a quarter of the bins; the quarters are
+// bins (of one spectrum, or with PARTS the sum of g.nsplit partial spectra
+// g.pstride apart), its waves each reducing a share of the bins; the shares are
 // added in a fixed order through LDS and written straight to dw, so no
 // partial sums leave the block.  E comes from a table built once per plan.
 // E: the launch's dynamic LDS ([kept][TMAX] float2, zero beyond T: the bin loop
 // has no branches); red: NW * 64 * TMAX floats.  Block bx of 64 * NW threads.
-template <int TMAX, int NW>
+template <int TMAX, int NW, bool PARTS = false>
 __device__ __forceinline__ void wgrad_wide_block(const float2* __restrict__ DW, const float2* __restrict__ Et,
                                                  float* __restrict__ dw, const WgradGeom& g, unsigned bx, float2* E,
                                                  float* red) {
@@ -141,11 +142,22 @@ __device__ __forceinline__ void wgrad_wide_block(const float2* __restrict__ DW, 
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) acc[t] = 0.f;
   const float2* src = DW + (valid ? q : 0u);
-  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed)
+  // 8 bins' loads in flight at a time (indices clamped, surplus values zeroed);
+  // with partial spectra (nsplit > 1) each bin is their sum, taken in order
   for (int bb = bb0; bb < bb1; bb += 8) {
     float2 d[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) d[j] = src[(size_t)min(bb + j, bb1 - 1) * Q];
+    if constexpr (PARTS) {
+      for (int sp = 1; sp < g.nsplit; ++sp) {
+        const float2* ps = src + (size_t)sp * g.pstride;
+        float2 e[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) e[j] = ps[(size_t)min(bb + j, bb1 - 1) * Q];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) d[j] = make_float2(d[j].x + e[j].x, d[j].y + e[j].y);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const bool in = bb + j < bb1;

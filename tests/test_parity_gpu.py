@@ -347,11 +347,14 @@ def test_combined_backward(torch):
     two, its partials added as more bin slices), the 128-channel layer (no
     split), the 256-channel layer (different tiles: two launches) and the
     512-channel layer (grad-input split in four, added by the 2-D inverse as
-    it loads); then a ragged layer, a 1-D layer (grad-input partials summed
-    before the chirp-z inverse), a layer whose grad-weight partials are summed
-    before the one-pass inverse DFT, and a bfloat16 plan."""
+    it loads); the 64-channel layer at c = 0 and 0.75 (grad-weight partials
+    summed by the one-pass inverse DFT as it loads them); then a ragged layer,
+    a 1-D layer (grad-input partials summed before the chirp-z inverse), a
+    layer whose grad-weight partials the one-pass inverse DFT sums beside the
+    2-D inverse, and a bfloat16 plan."""
     # (layer, rate, plan flags, workload (config, layer) or None for random inputs)
     cases = [(synth.WORKLOADS[3].layers[i], 0.5, 0, (3, i)) for i in range(4)]
+    cases += [(synth.WORKLOADS[3].layers[0], c, 0, (3, 0)) for c in (0.0, 0.75)]
     cases += [(synth.Layer("ragged", 2, 70, 66, 130, 6, 6, 3, (1, 1, 1, 1), "blur"), 0.0, 0, None),
               (synth.WORKLOADS[2].layers[1], 0.5, 0, (2, 1)),
               (synth.Layer("split_wide", 2, 128, 32, 32, 8, 8, 3, (1, 1, 1, 1), "blur"), 0.0, 0, None),
