@@ -169,3 +169,10 @@ def test_traffic_scaled_by_copy(tmp_path):
     assert e["fetch_bytes_per_launch"] == pytest.approx(2000 * 1024 * 2.0)
     assert e["write_bytes_per_launch"] == pytest.approx(600 * 1024)
     assert e["traffic_bytes_per_launch"] == pytest.approx(2000 * 2048 + 600 * 1024)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    out = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], cwd=ROOT, capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 2
+    assert "one GPU" in (out.stdout + out.stderr)
