@@ -215,24 +215,34 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_idft(const float2* __restric
 // partial sums, combined pairwise at the end).
 __global__ __launch_bounds__(kThreads) void k_wgrad_reduce(const float* __restrict__ part, float* __restrict__ dw,
                                                            WgradGeom g) {
+  // four lanes per output value: lane j of a quad sums slices j, j + 4, ...
+  // in order (all of its loads in flight together, eight at a time), and the
+  // quad adds its four sums as (s0 + s1) + (s2 + s3); the order is fixed
   const long Q = (long)g.C * g.F;
-  const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;  // e = t * Q + q
-  if (e >= Q * g.T) return;
+  const long e = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 2;  // e = t * Q + q
+  const int j = threadIdx.x & 3;
+  const bool live = e < Q * g.T;
+  const size_t stride = (size_t)g.T * Q;
+  const float* src = part + (live ? e : 0);
+  const int slices = g.chunks * max(1, g.nsplit);
+  float acc = 0.f;
+  for (int k0 = j; k0 < slices; k0 += 32) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = k0 + 4 * i;
+      v[i] = k < slices ? src[(size_t)k * stride] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += v[i];
+  }
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  if (!live || j != 0) return;
   const long q = e % Q;
   const int t = (int)(e / Q);
-  const size_t stride = (size_t)g.T * Q;
-  const float* src = part + e;
-  const int slices = g.chunks * max(1, g.nsplit);
-  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  int k = 0;
-  for (; k + 8 <= slices; k += 8) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) s[i] += src[(size_t)(k + i) * stride];
-  }
-  for (int i = 0; k < slices; ++k, ++i) s[i] += src[(size_t)k * stride];
-  const float tot = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
   const int c = (int)(q / g.F), f = (int)(q % g.F);
-  dw[((size_t)f * g.C + c) * g.T + t] = tot;
+  dw[((size_t)f * g.C + c) * g.T + t] = acc;
 }
 
 template <int TMAX, int NW>
@@ -605,7 +615,7 @@ bool wgrad_sliced_setup(const bl_conv_plan_s* p, int nsplit, WgradGeom& g, long*
 bl_status_t launch_wgrad_reduce(const bl_conv_plan_s* p, const float* part, float* dw, const WgradGeom& g,
                                 hipStream_t s) {
   const long Q = (long)p->Cin * p->Cout;
-  const long rblocks = (Q * g.T + kThreads - 1) / kThreads;
+  const long rblocks = (4 * Q * g.T + kThreads - 1) / kThreads;  // four lanes per value
   return timed_launch("wgrad_reduce", (double)Q * g.T * 4 * (g.chunks * g.nsplit + 1), 0.0, s,
                       [&](hipEvent_t e0, hipEvent_t e1) {
     hipExtLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)rblocks), dim3(kThreads), 0, s, e0, e1, 0, part, dw, g);
