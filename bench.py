@@ -376,6 +376,10 @@ def main():
         rc, _ = profile_steps(torch, blconv, Ls, args.steps)
         eagg, eks = kernel_table(rc)
         extra["roofline"] = roofline(eagg)
+        et = measured_traffic(extra["roofline"]["kernel"], f"config {args.extra_config} c={args.c}")
+        extra["roofline"]["traffic"] = et
+        if et is not None:
+            extra["roofline"]["traffic_over_algorithmic"] = et / extra["roofline"]["per_launch_bytes"]
         extra["kernels"] = eks
         del Ls
 
